@@ -1,0 +1,297 @@
+/*
+ * c3.h -- C ABI of the MI355X (gfx950) hot path of Consensus Collective
+ * Communication (C3): per-chunk signatures and numerical summaries of R
+ * replica copies resident in one GPU's HBM, strict-majority or robust
+ * statistical consensus across the replicas, and a (replica, chunk) outlier
+ * list.
+ *
+ * Paper: "SCOUT: Symmetric Consensus Outlier Detection for Failure
+ * Localization in LLM Pre-Training" (arXiv 2608.11034).  C3 maps one
+ * diagnostic object per peer of an ordered peer group G = (r_0 .. r_{N-1})
+ * to a result R = (s, B, E): a status, an N-bit outlier bitmap and the
+ * gathered evidence (Sec. 5.1, Algorithm 1).  Here the N peers are R replica
+ * copies on one GPU, peer i is replica i (the caller keeps the mapping from
+ * replica index to global rank), the evidence E is the chunk-record table,
+ * and s and B are produced per chunk.
+ *
+ * Common conventions
+ *   - Device pointers are plain HIP device addresses owned by the caller.
+ *     The library allocates no device or host memory that outlives a call
+ *     and keeps no state between calls.
+ *   - Host arrays passed in (pointer tables, tensor metadata) are consumed
+ *     before the call returns; the caller may free them immediately.
+ *   - Every call enqueues work on `stream` and returns without waiting; its
+ *     outputs are valid once the stream has been synchronized.  A NULL
+ *     stream is the default (null) stream.
+ *   - Errors are returned as negative codes (c3_status_t); nothing is thrown
+ *     across the ABI and nothing is launched when an argument check fails.
+ *   - Calls on different streams with disjoint outputs and workspaces may
+ *     run concurrently.
+ *   - Outputs are deterministic: identical inputs give identical bits
+ *     whatever the grid size.
+ */
+#ifndef C3_H_
+#define C3_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Binary-compatible with hipStream_t / hipEvent_t. */
+typedef struct ihipStream_t *c3_stream_t;
+typedef struct ihipEvent_t *c3_event_t;
+
+#define C3_ABI_VERSION 1
+#define C3_MAX_REPLICAS 64 /* one 64-bit outlier bitmap word per unit */
+#define C3_MAX_NDIM 8
+
+typedef enum {
+    C3_OK = 0,
+    C3_E_INVAL = -1,       /* bad size, count, code or NULL pointer        */
+    C3_E_ALIGN = -2,       /* a pointer or stride violates its alignment   */
+    C3_E_UNSUPPORTED = -3, /* valid request this build does not implement  */
+    C3_E_WORKSPACE = -4,   /* workspace NULL, misaligned or too small      */
+    C3_E_HIP = -5          /* a HIP runtime call or kernel launch failed   */
+} c3_status_t;
+
+/* Element types of checked tensors.  RAW tensors are hashed only. */
+typedef enum { C3_F32 = 0, C3_BF16 = 1, C3_F16 = 2, C3_RAW = 3 } c3_dtype_t;
+
+/* Comparison mode of Algorithm 1. */
+typedef enum { C3_EXACT = 0, C3_STATISTICAL = 1 } c3_mode_t;
+
+/* How one evidence value is stored.  EXACT compares raw bits of any kind;
+ * STATISTICAL reads F32 or F64 values. */
+typedef enum { C3_EV_U64 = 0, C3_EV_U32 = 1, C3_EV_F32 = 2, C3_EV_F64 = 3 } c3_evidence_kind_t;
+
+/* Status s of a result (Sec. 5.1): Agree -- the evidence satisfies the rule
+ * and B = 0; Attributed -- B names one or more outliers; Inconclusive --
+ * peers disagree but no attribution is justified, B = 0. */
+typedef enum { C3_AGREE = 0, C3_ATTRIBUTED = 1, C3_INCONCLUSIVE = 2 } c3_verdict_t;
+
+/* Iglewicz-Hoaglin modified z-score cut 3.5 expressed against the raw MAD. */
+#define C3_KAPPA_DEFAULT (3.5 / 0.6745)
+
+/* Metadata of one checked tensor: H_w hashes dtype and shape with the bytes
+ * (Sec. 5.2).  The tensor occupies prod(shape) * element_size contiguous
+ * bytes (element sizes 4, 2, 2, 1 for F32, BF16, F16, RAW); ndim 0 is a
+ * scalar. */
+typedef struct {
+    int32_t dtype;
+    int32_t ndim;
+    int64_t shape[C3_MAX_NDIM];
+} c3_tensor_meta_t;
+
+/* Evidence of one (replica, chunk): the C3SIG-1 signature and the numerical
+ * summary of the chunk's finite elements.  64 bytes.
+ *   sig        64-bit signature over dtype, shape, chunk index, byte length
+ *              and bytes (Sec. 5.2 read per chunk; construction C3SIG-1)
+ *   n_elems    elements in the chunk (bytes for RAW)
+ *   nan_count, inf_count   non-finite elements (exponent field all ones)
+ *   tensor, chunk_in_tensor  position of the chunk
+ *   absmax     max |x| over finite x (0 if none)
+ *   sum, sumsq sum and sum of squares over finite x, accumulated in fp64
+ *              with compensated combination (relative error far below 1e-6)
+ *   RAW chunks have zero counts and floats. */
+typedef struct {
+    uint64_t sig;
+    uint64_t n_elems;
+    uint32_t nan_count;
+    uint32_t inf_count;
+    uint32_t tensor;
+    uint32_t chunk_in_tensor;
+    double absmax;
+    double sum;
+    double sumsq;
+    uint64_t reserved;
+} c3_chunk_record_t;
+
+/* One localized outlier: unit (chunk), replica, the lowest replica holding
+ * the majority value, and the summaries of both ([0] outlier, [1] majority).
+ * 80 bytes. */
+typedef struct {
+    int64_t chunk;
+    int32_t replica;
+    int32_t majority_replica;
+    uint32_t nan_count[2];
+    uint32_t inf_count[2];
+    double absmax[2];
+    double sum[2];
+    double sumsq[2];
+} c3_outlier_t;
+
+/* Per-rank verdict of temporal confirmation (c3_confirm).  24 bytes.
+ *   flags: bit 0 confirmed straggler (flagged in more than half of some
+ *          window of W consecutive iterations); bit 1 protocol outlier
+ *          (fingerprint attributed in some iteration); bit 2 flagged in two
+ *          consecutive iterations at least once (the paper's own rule).
+ *   first_divergent_iter  first iteration with an attributed fingerprint, -1
+ *   divergent_count       iterations with an attributed fingerprint
+ *   slow_count            iterations with an attributed timing
+ *   max_window_slow       largest attributed-timing count in one window
+ *   first_straggler_window start of the first window over the threshold, -1 */
+typedef struct {
+    uint32_t flags;
+    int32_t first_divergent_iter;
+    uint32_t divergent_count;
+    uint32_t slow_count;
+    uint32_t max_window_slow;
+    int32_t first_straggler_window;
+} c3_rank_verdict_t;
+
+#define C3_RANK_STRAGGLER 1u
+#define C3_RANK_PROTOCOL 2u
+#define C3_RANK_CONSEC2 4u
+
+/* Optional launch controls for c3_signature_ex.
+ *   ev_kernel_begin / ev_kernel_end: if non-NULL, recorded on the stream
+ *     immediately before and after the streaming signature kernel (for
+ *     timing that kernel alone).
+ *   grid_blocks: workgroups of the streaming kernel; 0 chooses one per tile.
+ *     Results do not depend on it.
+ *   tile_bytes: bytes one workgroup folds into one partial; 0 chooses the
+ *     default.  Must be a power-of-two multiple of 1024 dividing chunk_bytes
+ *     (checked); the fp64 sums may differ in the last bits between tile
+ *     sizes, everything else is identical. */
+typedef struct {
+    c3_event_t ev_kernel_begin;
+    c3_event_t ev_kernel_end;
+    int32_t grid_blocks;
+    int32_t reserved;
+    uint64_t tile_bytes;
+} c3_launch_opts_t;
+
+/* Number of chunks C of the chunk plan: each tensor is split on its own into
+ * ceil(nbytes / chunk_bytes) chunks (the last may be partial; an empty
+ * tensor has one empty chunk so its dtype and shape are still compared);
+ * chunk ids run over tensors in the given order.  Returns C, or a negative
+ * c3_status_t for invalid metadata or chunk_bytes. */
+int64_t c3_num_chunks(const c3_tensor_meta_t *metas, int T, uint64_t chunk_bytes);
+
+/* Device workspace bytes c3_signature needs for this plan (0 on invalid
+ * arguments). */
+size_t c3_signature_workspace_size(const c3_tensor_meta_t *metas, int T, int R,
+                                   uint64_t chunk_bytes);
+
+/* Workspace bytes for a caller-chosen tile size (c3_launch_opts_t.tile_bytes;
+ * 0 = default).  0 on invalid arguments. */
+size_t c3_signature_workspace_size_ex(const c3_tensor_meta_t *metas, int T, int R,
+                                      uint64_t chunk_bytes, uint64_t tile_bytes);
+
+/*
+ * c3_signature -- comparable evidence per chunk (Sec. 5.2; Algorithm 1, the
+ * line that turns x_i into e_i).  Reads every replica byte exactly once.
+ *
+ *   ptrs        host array [R * T] of device pointers, replica-major:
+ *               ptrs[r * T + t] is replica r's copy of tensor t.  Each must
+ *               be 16-byte aligned (C3_E_ALIGN) and non-NULL unless the
+ *               tensor is empty.
+ *   metas       host array [T]; shared by all replicas.
+ *   T, R        tensors per replica (>= 1) and replicas (2..64; R = 1 is a
+ *               singleton group with nothing to compare, Sec. 4: C3_E_INVAL).
+ *   chunk_bytes positive multiple of 1024.
+ *   records     device [R][C] c3_chunk_record_t, 8-byte aligned; written.
+ *   ws, ws_bytes  device workspace of at least
+ *               c3_signature_workspace_size(...) bytes, 256-byte aligned;
+ *               contents need no initialization and are clobbered.
+ */
+int c3_signature(const void *const *ptrs, const c3_tensor_meta_t *metas, int T, int R,
+                 uint64_t chunk_bytes, c3_chunk_record_t *records, void *ws, size_t ws_bytes,
+                 c3_stream_t stream);
+
+/* c3_signature with launch controls (opts may be NULL). */
+int c3_signature_ex(const void *const *ptrs, const c3_tensor_meta_t *metas, int T, int R,
+                    uint64_t chunk_bytes, c3_chunk_record_t *records, void *ws, size_t ws_bytes,
+                    c3_stream_t stream, const c3_launch_opts_t *opts);
+
+/*
+ * c3_consensus -- the decision of Algorithm 1 for n_units independent units
+ * (chunks, or (iteration, group) records), each with R peer values.
+ *
+ * Replica r's value for unit u is read at
+ *   (const char *)evidence + u * unit_stride_bytes + r * replica_stride_bytes
+ * e.g. signatures inside the record table: evidence = &records[0].sig,
+ * replica_stride = C * 64, unit_stride = 64.  Strides and the base must be
+ * multiples of the value size (8 for U64/F64, 4 for U32/F32): C3_E_ALIGN.
+ *
+ *   EXACT (Sec. 5.3): c* = count of the most frequent value; if 2 c* <= R the
+ *     unit is Inconclusive with B = 0; otherwise bit r of B is set iff
+ *     replica r differs from the majority value, status Attributed if B != 0
+ *     else Agree, majority_idx = lowest replica holding the majority value.
+ *   STATISTICAL (Sec. 5.4), evidence kind F32 or F64, in fp64: a non-finite
+ *     value marks its replica; if finite values are not a strict majority the
+ *     unit is Inconclusive; m = median of the finite values; d = MAD, else
+ *     half the type-7 interquartile range, else range / n_finite; if d = 0
+ *     only non-finite replicas are marked; otherwise replica r is marked iff
+ *     |x_r - m| > kappa * d.  majority_idx = replica at the lower median.
+ *     kappa > 0 (C3_KAPPA_DEFAULT recommended); ignored for EXACT.
+ *
+ *   status [n_units] u8 (c3_verdict_t), bitmap [n_units] u64 (8-byte
+ *   aligned), majority_idx [n_units] i32 (-1 when Inconclusive); device.
+ *   R in 1..64 (R = 1 gives Agree), n_units >= 0.
+ */
+int c3_consensus(const void *evidence, int evidence_kind, int64_t replica_stride_bytes,
+                 int64_t unit_stride_bytes, int R, int64_t n_units, int mode, double kappa,
+                 uint8_t *status, uint64_t *bitmap, int32_t *majority_idx, c3_stream_t stream);
+
+/* Device workspace bytes c3_localize needs for n_units. */
+size_t c3_localize_workspace_size(int64_t n_units);
+
+/*
+ * c3_localize -- turns per-unit results into lists: which replica, which
+ * chunk, what summary (Sec. 5.1: B[i] = 1 attributes the divergence to peer
+ * i; Sec. 9: reports keep the peers and bitmaps).
+ *
+ *   outliers   device [out_cap]: one entry per set bitmap bit, ordered by
+ *              (unit ascending, replica ascending).  With records (device
+ *              [R][n_units], may be NULL) each entry carries the outlier's
+ *              and the majority replica's summary; without, those are 0.
+ *   undecided  device [und_cap] i64: Inconclusive units, ascending.
+ *   counts     device [3] i64: total outliers, total undecided units, units
+ *              with at least one outlier.  Totals are always exact; only
+ *              min(total, cap) entries are written, so the caller detects
+ *              truncation by comparing counts with the caps.
+ *   ws         device workspace of c3_localize_workspace_size(n_units)
+ *              bytes, 256-byte aligned.
+ */
+int c3_localize(const uint8_t *status, const uint64_t *bitmap, const int32_t *majority_idx,
+                const c3_chunk_record_t *records, int R, int64_t n_units, c3_outlier_t *outliers,
+                int64_t out_cap, int64_t *undecided, int64_t und_cap, int64_t *counts, void *ws,
+                size_t ws_bytes, c3_stream_t stream);
+
+/* Device workspace bytes c3_confirm needs. */
+size_t c3_confirm_workspace_size(int R, int64_t G, int64_t T);
+
+/*
+ * c3_confirm -- temporal confirmation of per-iteration results for G peer
+ * groups of R ranks over T consecutive iterations (Sec. 10 protocol: a
+ * straggler must recur across timing rounds before it is reported; Sec. 7:
+ * a minority collective fingerprint is a protocol outlier).
+ *
+ *   fp_bitmap, time_bitmap  device [T][G] u64: the bitmaps c3_consensus
+ *             produced for the fingerprint (EXACT) and timing (STATISTICAL)
+ *             evidence of unit (t, g).
+ *   window    W >= 1 (capped at T): a rank is a confirmed straggler when its
+ *             timing is attributed in more than W/2 iterations of some
+ *             window of W consecutive iterations.
+ *   verdicts  device [R * G], rank = r * G + g (row-major placement with
+ *             the replica index major, as in the Sec. 4 example).
+ */
+int c3_confirm(const uint64_t *fp_bitmap, const uint64_t *time_bitmap, int R, int64_t G,
+               int64_t T, int window, c3_rank_verdict_t *verdicts, void *ws, size_t ws_bytes,
+               c3_stream_t stream);
+
+/* Static description of a status code. */
+const char *c3_status_string(int code);
+
+/* C3_ABI_VERSION of the loaded library. */
+int c3_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* C3_H_ */

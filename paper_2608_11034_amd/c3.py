@@ -1,0 +1,325 @@
+"""Python binding of libc3.so (include/c3.h) for torch tensors on a ROCm device.
+
+Argument marshalling only: every step of the hot path runs in the HIP
+kernels of libc3.so.  There is no CPU fallback; if the library is missing or
+the tensors are not on a GPU the functions raise.
+
+Entry points (same names as the C ABI):
+
+* ``signature(replicas, chunk_bytes)``  -> records [R, C] (64-byte rows)
+* ``consensus(evidence, mode, ...)``     -> status, bitmap, majority index
+* ``localize(status, bitmap, majority_idx, records, R)`` -> lists + counts
+* ``confirm(fp_bitmap, time_bitmap, R, window)`` -> per-rank verdicts
+
+Records, outliers and verdicts are returned as raw device tensors
+(``torch.uint8`` rows); ``records_numpy`` & co. view host copies as numpy
+structured arrays with the C field names.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+import torch  # imported before libc3.so so both use torch's HIP runtime
+
+from . import build as _build
+
+F32, BF16, F16, RAW = 0, 1, 2, 3
+EXACT, STATISTICAL = 0, 1
+EV_U64, EV_U32, EV_F32, EV_F64 = 0, 1, 2, 3
+AGREE, ATTRIBUTED, INCONCLUSIVE = 0, 1, 2
+KAPPA_DEFAULT = 3.5 / 0.6745
+RANK_STRAGGLER, RANK_PROTOCOL, RANK_CONSEC2 = 1, 2, 4
+
+RECORD_DTYPE = np.dtype([("sig", "<u8"), ("n_elems", "<u8"), ("nan_count", "<u4"),
+                         ("inf_count", "<u4"), ("tensor", "<u4"), ("chunk_in_tensor", "<u4"),
+                         ("absmax", "<f8"), ("sum", "<f8"), ("sumsq", "<f8"), ("reserved", "<u8")])
+OUTLIER_DTYPE = np.dtype([("chunk", "<i8"), ("replica", "<i4"), ("majority_replica", "<i4"),
+                          ("nan_count", "<u4", (2,)), ("inf_count", "<u4", (2,)),
+                          ("absmax", "<f8", (2,)), ("sum", "<f8", (2,)), ("sumsq", "<f8", (2,))])
+VERDICT_DTYPE = np.dtype([("flags", "<u4"), ("first_divergent_iter", "<i4"),
+                          ("divergent_count", "<u4"), ("slow_count", "<u4"),
+                          ("max_window_slow", "<u4"), ("first_straggler_window", "<i4")])
+assert RECORD_DTYPE.itemsize == 64 and OUTLIER_DTYPE.itemsize == 80 and VERDICT_DTYPE.itemsize == 24
+
+_TORCH_CODE = {torch.float32: F32, torch.bfloat16: BF16, torch.float16: F16, torch.uint8: RAW}
+
+
+class C3Error(RuntimeError):
+    pass
+
+
+class TensorMeta(ctypes.Structure):
+    _fields_ = [("dtype", ctypes.c_int32), ("ndim", ctypes.c_int32), ("shape", ctypes.c_int64 * 8)]
+
+
+class LaunchOpts(ctypes.Structure):
+    _fields_ = [("ev_kernel_begin", ctypes.c_void_p), ("ev_kernel_end", ctypes.c_void_p),
+                ("grid_blocks", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("tile_bytes", ctypes.c_uint64)]
+
+
+_lib = None
+
+
+def library_path() -> str:
+    return _build.LIB
+
+
+def lib():
+    """The loaded libc3.so; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_build.LIB):
+            raise C3Error(f"{_build.LIB} is not built; run __graft_entry__.build() first")
+        L = ctypes.CDLL(_build.LIB)
+        vp, i32, i64, u64, sz, dbl = (ctypes.c_void_p, ctypes.c_int, ctypes.c_int64,
+                                      ctypes.c_uint64, ctypes.c_size_t, ctypes.c_double)
+        L.c3_abi_version.restype = i32
+        L.c3_status_string.restype = ctypes.c_char_p
+        L.c3_status_string.argtypes = [i32]
+        L.c3_num_chunks.restype = i64
+        L.c3_num_chunks.argtypes = [vp, i32, u64]
+        L.c3_signature_workspace_size.restype = sz
+        L.c3_signature_workspace_size.argtypes = [vp, i32, i32, u64]
+        L.c3_signature_workspace_size_ex.restype = sz
+        L.c3_signature_workspace_size_ex.argtypes = [vp, i32, i32, u64, u64]
+        L.c3_signature.restype = i32
+        L.c3_signature.argtypes = [vp, vp, i32, i32, u64, vp, vp, sz, vp]
+        L.c3_signature_ex.restype = i32
+        L.c3_signature_ex.argtypes = [vp, vp, i32, i32, u64, vp, vp, sz, vp, vp]
+        L.c3_consensus.restype = i32
+        L.c3_consensus.argtypes = [vp, i32, i64, i64, i32, i64, i32, dbl, vp, vp, vp, vp]
+        L.c3_localize_workspace_size.restype = sz
+        L.c3_localize_workspace_size.argtypes = [i64]
+        L.c3_localize.restype = i32
+        L.c3_localize.argtypes = [vp, vp, vp, vp, i32, i64, vp, i64, vp, i64, vp, vp, sz, vp]
+        L.c3_confirm_workspace_size.restype = sz
+        L.c3_confirm_workspace_size.argtypes = [i32, i64, i64]
+        L.c3_confirm.restype = i32
+        L.c3_confirm.argtypes = [vp, vp, i32, i64, i64, i32, vp, vp, sz, vp]
+        if L.c3_abi_version() != 1:
+            raise C3Error("libc3.so ABI version mismatch")
+        _lib = L
+    return _lib
+
+
+def _check(rc: int, what: str):
+    if rc != 0:
+        raise C3Error(f"{what}: {lib().c3_status_string(rc).decode()} ({rc})")
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _dev_tensor(t: torch.Tensor, name: str) -> torch.Tensor:
+    if not isinstance(t, torch.Tensor) or t.device.type != "cuda":
+        raise C3Error(f"{name} must be a tensor on a ROCm GPU device")
+    if not t.is_contiguous():
+        raise C3Error(f"{name} must be contiguous")
+    return t
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
+
+
+def _empty(shape, dtype, device):
+    return torch.empty(shape, dtype=dtype, device=device)
+
+
+def make_metas(tensors) -> ctypes.Array:
+    """c3_tensor_meta_t[T] from torch tensors (dtype code and shape)."""
+    metas = (TensorMeta * len(tensors))()
+    for i, t in enumerate(tensors):
+        if t.dtype not in _TORCH_CODE:
+            raise C3Error(f"unsupported dtype {t.dtype}")
+        if t.dim() > 8:
+            raise C3Error("at most 8 dimensions")
+        metas[i].dtype = _TORCH_CODE[t.dtype]
+        metas[i].ndim = t.dim()
+        for d, n in enumerate(t.shape):
+            metas[i].shape[d] = int(n)
+    return metas
+
+
+def num_chunks(tensors, chunk_bytes: int) -> int:
+    metas = make_metas(tensors)
+    c = lib().c3_num_chunks(metas, len(tensors), chunk_bytes)
+    if c < 0:
+        _check(int(c), "c3_num_chunks")
+    return int(c)
+
+
+def signature_workspace_size(tensors, R: int, chunk_bytes: int, tile_bytes: int = 0) -> int:
+    metas = make_metas(tensors)
+    n = lib().c3_signature_workspace_size_ex(metas, len(tensors), R, chunk_bytes, tile_bytes)
+    if n == 0:
+        raise C3Error("invalid signature plan")
+    return int(n)
+
+
+class SignaturePlan:
+    """Host-side marshalling of one replica set: pointer table and metadata.
+
+    Building it once and calling ``run`` repeatedly only avoids re-marshalling
+    in Python; the library still stages the plan on every call.
+    """
+
+    def __init__(self, replicas, chunk_bytes: int, tile_bytes: int = 0):
+        if len(replicas) < 2:
+            raise C3Error("need at least two replicas")
+        T = len(replicas[0])
+        dev = replicas[0][0].device
+        for r, rep in enumerate(replicas):
+            if len(rep) != T:
+                raise C3Error("every replica must hold the same tensors")
+            for t, x in enumerate(rep):
+                _dev_tensor(x, f"replicas[{r}][{t}]")
+                if x.device != dev:
+                    raise C3Error("all replicas must be on one device")
+                ref = replicas[0][t]
+                if x.dtype != ref.dtype or x.shape != ref.shape:
+                    raise C3Error(f"tensor {t} differs in dtype or shape between replicas")
+        self.R, self.T, self.device = len(replicas), T, dev
+        self.chunk_bytes, self.tile_bytes = int(chunk_bytes), int(tile_bytes)
+        self.keep = [x for rep in replicas for x in rep]
+        self.ptrs = (ctypes.c_void_p * (self.R * T))(*[x.data_ptr() for x in self.keep])
+        self.metas = make_metas(replicas[0])
+        self.C = num_chunks(replicas[0], chunk_bytes)
+        self.ws_bytes = signature_workspace_size(replicas[0], self.R, chunk_bytes, tile_bytes)
+
+    def new_records(self):
+        return _empty((self.R, self.C, 64), torch.uint8, self.device)
+
+    def new_workspace(self):
+        return _empty((self.ws_bytes,), torch.uint8, self.device)
+
+    def run(self, records, workspace, stream=None, ev_begin=None, ev_end=None, grid_blocks=0):
+        opts = LaunchOpts(ev_begin.cuda_event if ev_begin is not None else None,
+                          ev_end.cuda_event if ev_end is not None else None,
+                          int(grid_blocks), 0, self.tile_bytes)
+        rc = lib().c3_signature_ex(self.ptrs, self.metas, self.T, self.R, self.chunk_bytes,
+                                   _ptr(records), _ptr(workspace), workspace.numel(),
+                                   _stream(stream), ctypes.byref(opts))
+        _check(rc, "c3_signature")
+        return records
+
+
+def signature(replicas, chunk_bytes: int, stream=None, grid_blocks: int = 0, tile_bytes: int = 0):
+    """Records [R, C, 64] (uint8) of R replica lists of T device tensors."""
+    plan = SignaturePlan(replicas, chunk_bytes, tile_bytes)
+    rec = plan.new_records()
+    ws = plan.new_workspace()
+    plan.run(rec, ws, stream=stream, grid_blocks=grid_blocks)
+    return rec
+
+
+def consensus(evidence: torch.Tensor, mode: int = EXACT, *, kind: int = None, R: int = None,
+              replica_stride: int = None, unit_stride: int = None, n_units: int = None,
+              kappa: float = KAPPA_DEFAULT, stream=None, out=None):
+    """Per-unit status, bitmap and majority index.
+
+    ``evidence`` is either the records tensor [R, C, 64] (signatures are voted)
+    or a value tensor [U, R] / [..., R] of int64/float32/float64 with the
+    replicas on the last axis.  Strides are in bytes.
+    """
+    _dev_tensor(evidence, "evidence")
+    if evidence.dtype == torch.uint8 and evidence.dim() == 3 and evidence.shape[2] == 64:
+        R_, C = evidence.shape[0], evidence.shape[1]
+        kind = EV_U64 if kind is None else kind
+        R = R_ if R is None else R
+        replica_stride = C * 64 if replica_stride is None else replica_stride
+        unit_stride = 64 if unit_stride is None else unit_stride
+        n_units = C if n_units is None else n_units
+    else:
+        if kind is None:
+            kind = {torch.int64: EV_U64, torch.int32: EV_U32, torch.float32: EV_F32,
+                    torch.float64: EV_F64}[evidence.dtype]
+        R = evidence.shape[-1] if R is None else R
+        es = evidence.element_size()
+        replica_stride = es if replica_stride is None else replica_stride
+        unit_stride = R * es if unit_stride is None else unit_stride
+        n_units = evidence.numel() // R if n_units is None else n_units
+    dev = evidence.device
+    if out is not None:
+        status, bitmap, maj = out
+    else:
+        status = _empty((n_units,), torch.uint8, dev)
+        bitmap = _empty((n_units,), torch.int64, dev)
+        maj = _empty((n_units,), torch.int32, dev)
+    rc = lib().c3_consensus(_ptr(evidence), kind, replica_stride, unit_stride, R, n_units, mode,
+                            float(kappa), _ptr(status), _ptr(bitmap), _ptr(maj), _stream(stream))
+    _check(rc, "c3_consensus")
+    return status, bitmap, maj
+
+
+def localize(status, bitmap, majority_idx, records=None, R: int = None, out_cap: int = None,
+             und_cap: int = None, stream=None, out=None, workspace=None):
+    """Outlier entries [out_cap, 80] (uint8), undecided [und_cap] int64, counts [3] int64."""
+    n_units = status.numel()
+    if R is None:
+        if records is None:
+            raise C3Error("R is required without records")
+        R = records.shape[0]
+    dev = status.device
+    out_cap = n_units * R if out_cap is None else out_cap
+    und_cap = n_units if und_cap is None else und_cap
+    if out is not None:
+        outliers, undecided, counts = out
+        out_cap = min(out_cap, outliers.shape[0])
+        und_cap = min(und_cap, undecided.numel())
+    else:
+        outliers = _empty((max(out_cap, 1), 80), torch.uint8, dev)
+        undecided = _empty((max(und_cap, 1),), torch.int64, dev)
+        counts = _empty((3,), torch.int64, dev)
+    ws_bytes = int(lib().c3_localize_workspace_size(n_units))
+    ws = _empty((ws_bytes,), torch.uint8, dev) if workspace is None else workspace
+    if ws.numel() < ws_bytes:
+        raise C3Error("localize workspace too small")
+    ws_bytes = ws.numel()
+    rc = lib().c3_localize(_ptr(status), _ptr(bitmap), _ptr(majority_idx), _ptr(records), R, n_units,
+                           _ptr(outliers), out_cap, _ptr(undecided), und_cap, _ptr(counts),
+                           _ptr(ws), ws_bytes, _stream(stream))
+    _check(rc, "c3_localize")
+    return outliers, undecided, counts
+
+
+def localize_workspace_size(n_units: int) -> int:
+    return int(lib().c3_localize_workspace_size(n_units))
+
+
+def confirm(fp_bitmap, time_bitmap, R: int, window: int = 16, stream=None):
+    """Per-rank verdicts [R * G, 24] (uint8) from [T, G] bitmaps; rank = r * G + g."""
+    _dev_tensor(fp_bitmap, "fp_bitmap")
+    _dev_tensor(time_bitmap, "time_bitmap")
+    T, G = fp_bitmap.shape
+    dev = fp_bitmap.device
+    out = _empty((R * G, 24), torch.uint8, dev)
+    ws_bytes = int(lib().c3_confirm_workspace_size(R, G, T))
+    ws = _empty((max(ws_bytes, 256),), torch.uint8, dev)
+    rc = lib().c3_confirm(_ptr(fp_bitmap), _ptr(time_bitmap), R, G, T, window, _ptr(out), _ptr(ws),
+                          ws_bytes, _stream(stream))
+    _check(rc, "c3_confirm")
+    return out
+
+
+# ---------------------------------------------------------------------------
+# host views
+# ---------------------------------------------------------------------------
+def records_numpy(records: torch.Tensor) -> np.ndarray:
+    a = records.detach().cpu().contiguous().numpy()
+    return a.reshape(-1).view(RECORD_DTYPE).reshape(a.shape[:-1])
+
+
+def outliers_numpy(outliers: torch.Tensor, counts: torch.Tensor) -> np.ndarray:
+    n = min(int(counts[0]), outliers.shape[0])
+    return outliers[:n].detach().cpu().contiguous().numpy().reshape(-1).view(OUTLIER_DTYPE)
+
+
+def verdicts_numpy(verdicts: torch.Tensor) -> np.ndarray:
+    return verdicts.detach().cpu().contiguous().numpy().reshape(-1).view(VERDICT_DTYPE)

@@ -1,0 +1,285 @@
+// Host side of the C3 C ABI (include/c3.h): argument checks, the chunk and
+// tile plan, descriptor staging into the caller's workspace, and launches.
+// Nothing here computes evidence or verdicts; all of that runs in the HIP
+// kernels.
+#include <string.h>
+
+#include <vector>
+
+#include "c3_internal.h"
+
+namespace {
+
+using c3::SigPlan;
+using c3::TensorInfo;
+
+inline uint64_t align_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
+
+int elem_size(int dtype) {
+    switch (dtype) {
+        case C3_F32: return 4;
+        case C3_BF16: return 2;
+        case C3_F16: return 2;
+        case C3_RAW: return 1;
+        default: return 0;
+    }
+}
+
+// Bytes of one tensor, or -1 on invalid metadata / overflow.
+int64_t tensor_nbytes(const c3_tensor_meta_t& m) {
+    const int es = elem_size(m.dtype);
+    if (es == 0 || m.ndim < 0 || m.ndim > C3_MAX_NDIM) return -1;
+    unsigned __int128 n = (unsigned __int128)es;
+    for (int d = 0; d < m.ndim; ++d) {
+        if (m.shape[d] < 0) return -1;
+        n *= (unsigned __int128)m.shape[d];
+        if (n > (unsigned __int128)(INT64_MAX / 2)) return -1;
+    }
+    return (int64_t)n;
+}
+
+// Largest power-of-two multiple of 1024 dividing chunk_bytes, capped.
+uint64_t default_tile(uint64_t chunk_bytes) {
+    uint64_t t = 1024;
+    while (t * 2 <= c3::kDefaultTileMax && chunk_bytes % (t * 2) == 0) t *= 2;
+    return t;
+}
+
+struct Plan {
+    SigPlan h;
+    std::vector<int64_t> tile_base, chunk_base, gtile;
+    std::vector<int32_t> order;
+    std::vector<TensorInfo> tinfo;
+    c3::SigGroups groups;
+};
+
+// Builds the plan; returns C3_OK or an error code.
+int make_plan(const c3_tensor_meta_t* metas, int T, int R, uint64_t chunk_bytes,
+              uint64_t tile_bytes, Plan& p) {
+    if (metas == nullptr || T < 1 || R < 2 || R > C3_MAX_REPLICAS) return C3_E_INVAL;
+    if (chunk_bytes == 0 || chunk_bytes % 1024 != 0 || chunk_bytes > (1ull << 40)) return C3_E_INVAL;
+    if (tile_bytes == 0) tile_bytes = default_tile(chunk_bytes);
+    if (tile_bytes < 1024 || (tile_bytes & (tile_bytes - 1)) != 0 || chunk_bytes % tile_bytes != 0 ||
+        tile_bytes > (1ull << 24))
+        return C3_E_INVAL;
+    p.tile_base.assign(T + 1, 0);
+    p.chunk_base.assign(T + 1, 0);
+    p.tinfo.resize(T);
+    for (int t = 0; t < T; ++t) {
+        const int64_t nb = tensor_nbytes(metas[t]);
+        if (nb < 0) return C3_E_INVAL;
+        const int64_t nc = nb == 0 ? 1 : (int64_t)(((uint64_t)nb + chunk_bytes - 1) / chunk_bytes);
+        const int64_t nt = nb == 0 ? 1 : (int64_t)(((uint64_t)nb + tile_bytes - 1) / tile_bytes);
+        p.chunk_base[t + 1] = p.chunk_base[t] + nc;
+        p.tile_base[t + 1] = p.tile_base[t] + nt;
+        TensorInfo& ti = p.tinfo[t];
+        memset(&ti, 0, sizeof(ti));
+        ti.nbytes = (uint64_t)nb;
+        ti.dtype = metas[t].dtype;
+        ti.ndim = metas[t].ndim;
+        for (int d = 0; d < metas[t].ndim; ++d) ti.shape[d] = metas[t].shape[d];
+    }
+    // tensors grouped by dtype, call order kept inside a group
+    p.order.clear();
+    p.gtile.assign(T + 1, 0);
+    for (int d = 0; d < 4; ++d) {
+        p.groups.k0[d] = (int)p.order.size();
+        p.groups.tiles[d] = 0;
+        for (int t = 0; t < T; ++t) {
+            if (metas[t].dtype != d) continue;
+            const int64_t nt = p.tile_base[t + 1] - p.tile_base[t];
+            p.gtile[p.order.size() + 1] = p.gtile[p.order.size()] + nt;
+            p.groups.tiles[d] += nt;
+            p.order.push_back(t);
+        }
+        p.groups.k1[d] = (int)p.order.size();
+    }
+    SigPlan& h = p.h;
+    memset(&h, 0, sizeof(h));
+    h.R = R;
+    h.T = T;
+    h.C = p.chunk_base[T];
+    h.tiles_per_replica = p.tile_base[T];
+    h.chunk_bytes = chunk_bytes;
+    h.tile_bytes = tile_bytes;
+    h.tiles_per_chunk = (uint32_t)(chunk_bytes / tile_bytes);
+    h.direct = h.tiles_per_chunk == 1 ? 1u : 0u;
+    uint64_t off = align_up(sizeof(SigPlan), 256);
+    h.off_ptrs = off;
+    off = align_up(off + 8ull * (uint64_t)R * (uint64_t)T, 256);
+    h.off_tile_base = off;
+    off = align_up(off + 8ull * (uint64_t)(T + 1), 256);
+    h.off_chunk_base = off;
+    off = align_up(off + 8ull * (uint64_t)(T + 1), 256);
+    h.off_tmeta = off;
+    off = align_up(off + sizeof(TensorInfo) * (uint64_t)T, 256);
+    h.off_order = off;
+    off = align_up(off + 4ull * (uint64_t)T, 256);
+    h.off_gtile = off;
+    off = align_up(off + 8ull * (uint64_t)(T + 1), 256);
+    h.off_partials = off;
+    if (!h.direct) off += sizeof(c3::TilePartial) * (uint64_t)h.tiles_per_replica * (uint64_t)R;
+    h.total_bytes = align_up(off, 256);
+    return C3_OK;
+}
+
+inline bool aligned(const void* p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
+
+}  // namespace
+
+extern "C" {
+
+int c3_abi_version(void) { return C3_ABI_VERSION; }
+
+const char* c3_status_string(int code) {
+    switch (code) {
+        case C3_OK: return "ok";
+        case C3_E_INVAL: return "invalid argument";
+        case C3_E_ALIGN: return "misaligned pointer or stride";
+        case C3_E_UNSUPPORTED: return "unsupported request";
+        case C3_E_WORKSPACE: return "workspace missing, misaligned or too small";
+        case C3_E_HIP: return "HIP runtime error";
+        default: return "unknown status";
+    }
+}
+
+int64_t c3_num_chunks(const c3_tensor_meta_t* metas, int T, uint64_t chunk_bytes) {
+    Plan p;
+    const int rc = make_plan(metas, T, 2, chunk_bytes, 0, p);
+    return rc == C3_OK ? p.h.C : rc;
+}
+
+size_t c3_signature_workspace_size(const c3_tensor_meta_t* metas, int T, int R,
+                                   uint64_t chunk_bytes) {
+    Plan p;
+    return make_plan(metas, T, R, chunk_bytes, 0, p) == C3_OK ? (size_t)p.h.total_bytes : 0;
+}
+
+size_t c3_signature_workspace_size_ex(const c3_tensor_meta_t* metas, int T, int R,
+                                      uint64_t chunk_bytes, uint64_t tile_bytes) {
+    Plan p;
+    return make_plan(metas, T, R, chunk_bytes, tile_bytes, p) == C3_OK ? (size_t)p.h.total_bytes : 0;
+}
+
+int c3_signature_ex(const void* const* ptrs, const c3_tensor_meta_t* metas, int T, int R,
+                    uint64_t chunk_bytes, c3_chunk_record_t* records, void* ws, size_t ws_bytes,
+                    c3_stream_t stream, const c3_launch_opts_t* opts) {
+    if (ptrs == nullptr || records == nullptr) return C3_E_INVAL;
+    Plan p;
+    const uint64_t tile = opts ? opts->tile_bytes : 0;
+    const int rc = make_plan(metas, T, R, chunk_bytes, tile, p);
+    if (rc != C3_OK) return rc;
+    if (ws == nullptr || !aligned(ws, 256) || ws_bytes < p.h.total_bytes) return C3_E_WORKSPACE;
+    if (!aligned(records, 8)) return C3_E_ALIGN;
+    for (int r = 0; r < R; ++r)
+        for (int t = 0; t < T; ++t) {
+            const void* q = ptrs[(size_t)r * T + t];
+            if (p.tinfo[t].nbytes == 0) continue;
+            if (q == nullptr) return C3_E_INVAL;
+            if (!aligned(q, 16)) return C3_E_ALIGN;
+        }
+    // stage the plan: header, pointer table, bases, tensor info
+    std::vector<unsigned char> buf(p.h.off_partials, 0);
+    memcpy(buf.data(), &p.h, sizeof(SigPlan));
+    for (size_t i = 0; i < (size_t)R * (size_t)T; ++i) {
+        const uint64_t a = (uint64_t)(uintptr_t)ptrs[i];
+        memcpy(buf.data() + p.h.off_ptrs + 8 * i, &a, 8);
+    }
+    memcpy(buf.data() + p.h.off_tile_base, p.tile_base.data(), 8ull * (T + 1));
+    memcpy(buf.data() + p.h.off_chunk_base, p.chunk_base.data(), 8ull * (T + 1));
+    memcpy(buf.data() + p.h.off_tmeta, p.tinfo.data(), sizeof(TensorInfo) * (size_t)T);
+    memcpy(buf.data() + p.h.off_order, p.order.data(), 4ull * T);
+    memcpy(buf.data() + p.h.off_gtile, p.gtile.data(), 8ull * (T + 1));
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    if (hipMemcpyAsync(ws, buf.data(), buf.size(), hipMemcpyHostToDevice, s) != hipSuccess)
+        return C3_E_HIP;
+    const hipError_t e = c3::launch_signature(
+        static_cast<const SigPlan*>(ws), p.h, p.groups, records, opts ? opts->grid_blocks : 0, s,
+        opts ? reinterpret_cast<hipEvent_t>(opts->ev_kernel_begin) : nullptr,
+        opts ? reinterpret_cast<hipEvent_t>(opts->ev_kernel_end) : nullptr);
+    return e == hipSuccess ? C3_OK : C3_E_HIP;
+}
+
+int c3_signature(const void* const* ptrs, const c3_tensor_meta_t* metas, int T, int R,
+                 uint64_t chunk_bytes, c3_chunk_record_t* records, void* ws, size_t ws_bytes,
+                 c3_stream_t stream) {
+    return c3_signature_ex(ptrs, metas, T, R, chunk_bytes, records, ws, ws_bytes, stream, nullptr);
+}
+
+int c3_consensus(const void* evidence, int evidence_kind, int64_t replica_stride_bytes,
+                 int64_t unit_stride_bytes, int R, int64_t n_units, int mode, double kappa,
+                 uint8_t* status, uint64_t* bitmap, int32_t* majority_idx, c3_stream_t stream) {
+    if (R < 1 || R > C3_MAX_REPLICAS || n_units < 0) return C3_E_INVAL;
+    if (mode != C3_EXACT && mode != C3_STATISTICAL) return C3_E_INVAL;
+    int vsize;
+    switch (evidence_kind) {
+        case C3_EV_U64: case C3_EV_F64: vsize = 8; break;
+        case C3_EV_U32: case C3_EV_F32: vsize = 4; break;
+        default: return C3_E_INVAL;
+    }
+    if (mode == C3_STATISTICAL) {
+        if (evidence_kind != C3_EV_F32 && evidence_kind != C3_EV_F64) return C3_E_INVAL;
+        if (!(kappa > 0.0) || kappa != kappa || kappa > 1e300) return C3_E_INVAL;
+    }
+    if (n_units == 0) return C3_OK;
+    if (evidence == nullptr || status == nullptr || bitmap == nullptr || majority_idx == nullptr)
+        return C3_E_INVAL;
+    if (!aligned(evidence, vsize) || replica_stride_bytes % vsize != 0 ||
+        unit_stride_bytes % vsize != 0 || !aligned(bitmap, 8) || !aligned(majority_idx, 4))
+        return C3_E_ALIGN;
+    const hipError_t e = c3::launch_consensus(evidence, evidence_kind, replica_stride_bytes,
+                                              unit_stride_bytes, R, n_units, mode, kappa, status,
+                                              bitmap, majority_idx,
+                                              reinterpret_cast<hipStream_t>(stream));
+    return e == hipSuccess ? C3_OK : C3_E_HIP;
+}
+
+size_t c3_localize_workspace_size(int64_t n_units) {
+    return n_units < 0 ? 0 : c3::localize_ws_bytes(n_units);
+}
+
+int c3_localize(const uint8_t* status, const uint64_t* bitmap, const int32_t* majority_idx,
+                const c3_chunk_record_t* records, int R, int64_t n_units, c3_outlier_t* outliers,
+                int64_t out_cap, int64_t* undecided, int64_t und_cap, int64_t* counts, void* ws,
+                size_t ws_bytes, c3_stream_t stream) {
+    if (R < 1 || R > C3_MAX_REPLICAS || n_units < 0 || out_cap < 0 || und_cap < 0)
+        return C3_E_INVAL;
+    if (counts == nullptr) return C3_E_INVAL;
+    if (n_units > 0 && (status == nullptr || bitmap == nullptr || majority_idx == nullptr))
+        return C3_E_INVAL;
+    if ((out_cap > 0 && outliers == nullptr) || (und_cap > 0 && undecided == nullptr))
+        return C3_E_INVAL;
+    if (ws == nullptr || !aligned(ws, 256) || ws_bytes < c3::localize_ws_bytes(n_units))
+        return C3_E_WORKSPACE;
+    if (!aligned(bitmap, 8) || !aligned(majority_idx, 4) || !aligned(counts, 8) ||
+        !aligned(outliers, 8) || !aligned(undecided, 8) || !aligned(records, 8))
+        return C3_E_ALIGN;
+    const hipError_t e = c3::launch_localize(status, bitmap, majority_idx, records, R, n_units,
+                                             outliers, out_cap, undecided, und_cap, counts, ws,
+                                             reinterpret_cast<hipStream_t>(stream));
+    return e == hipSuccess ? C3_OK : C3_E_HIP;
+}
+
+size_t c3_confirm_workspace_size(int R, int64_t G, int64_t T) {
+    if (R < 1 || R > C3_MAX_REPLICAS || G < 0 || T < 0) return 0;
+    return c3::confirm_ws_bytes(R, G, T);
+}
+
+int c3_confirm(const uint64_t* fp_bitmap, const uint64_t* time_bitmap, int R, int64_t G,
+               int64_t T, int window, c3_rank_verdict_t* verdicts, void* ws, size_t ws_bytes,
+               c3_stream_t stream) {
+    if (R < 1 || R > C3_MAX_REPLICAS || G < 0 || T < 0 || window < 1) return C3_E_INVAL;
+    if (T > 0x7FFFFFFF || (int64_t)R * G > 0x7FFFFFFF) return C3_E_INVAL;
+    if ((int64_t)R * G == 0) return C3_OK;
+    if (verdicts == nullptr || (T > 0 && (fp_bitmap == nullptr || time_bitmap == nullptr)))
+        return C3_E_INVAL;
+    if (ws == nullptr || !aligned(ws, 256) || ws_bytes < c3::confirm_ws_bytes(R, G, T))
+        return C3_E_WORKSPACE;
+    if (!aligned(fp_bitmap, 8) || !aligned(time_bitmap, 8) || !aligned(verdicts, 4))
+        return C3_E_ALIGN;
+    const hipError_t e = c3::launch_confirm(fp_bitmap, time_bitmap, R, G, T, window, verdicts, ws,
+                                            reinterpret_cast<hipStream_t>(stream));
+    return e == hipSuccess ? C3_OK : C3_E_HIP;
+}
+
+}  // extern "C"

@@ -1,0 +1,192 @@
+// Localization kernels of C3 for gfx950: per-unit results -> ordered lists of
+// (unit, replica) outliers with both replicas' numerical summaries, plus the
+// undecided (Inconclusive) units.
+//
+// Deterministic three-pass compaction with no atomics:
+//   1. count   -- each workgroup counts outlier bits, undecided units and
+//                 attributed units over its segment of kSegUnits units;
+//   2. scan    -- one workgroup turns the segment counts into exclusive
+//                 offsets (in segment order) and writes the totals;
+//   3. emit    -- each workgroup recomputes its per-thread counts, scans them
+//                 across the wave with an inclusive prefix and across waves
+//                 through LDS, and writes entries at segment offset + local
+//                 offset while that position is below the caller's capacity.
+// A thread owns kPerThread consecutive units, so list order is (unit
+// ascending, replica ascending) by construction.
+#include "c3_device.h"
+#include "c3_internal.h"
+
+namespace c3 {
+
+constexpr int kLocThreads = 256;
+constexpr int kPerThread = 8;
+constexpr int64_t kSegUnits = (int64_t)kLocThreads * kPerThread;
+
+struct SegCount {
+    int64_t n_out, n_und, n_att;
+};
+
+__device__ inline void thread_counts(const uint8_t* status, const uint64_t* bitmap, int64_t u0,
+                                     int64_t n_units, int64_t& o, int64_t& un, int64_t& at) {
+    o = un = at = 0;
+    for (int i = 0; i < kPerThread; ++i) {
+        const int64_t u = u0 + i;
+        if (u >= n_units) break;
+        const uint8_t s = status[u];
+        if (s == C3_INCONCLUSIVE) {
+            ++un;
+        } else {
+            const uint64_t b = bitmap[u];
+            if (b) {
+                ++at;
+                o += __builtin_popcountll(b);
+            }
+        }
+    }
+}
+
+// Inclusive prefix sum over the 256 threads of a workgroup (fixed order).
+__device__ inline int64_t block_inclusive_scan(int64_t v, int64_t* lds_wave, int64_t& total) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    int64_t x = v;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const int64_t y = (int64_t)shfl_u64((uint64_t)x, lane >= d ? lane - d : lane);
+        if (lane >= d) x += y;
+    }
+    if (lane == 63) lds_wave[wave] = x;
+    __syncthreads();
+    int64_t before = 0;
+    total = 0;
+    for (int w = 0; w < kLocThreads / 64; ++w) {
+        if (w < wave) before += lds_wave[w];
+        total += lds_wave[w];
+    }
+    __syncthreads();
+    return x + before;
+}
+
+__global__ void __launch_bounds__(kLocThreads) localize_count_kernel(
+    const uint8_t* __restrict__ status, const uint64_t* __restrict__ bitmap, int64_t n_units,
+    SegCount* __restrict__ seg) {
+    __shared__ int64_t lds[3][kLocThreads / 64];
+    const int64_t u0 = (int64_t)blockIdx.x * kSegUnits + (int64_t)threadIdx.x * kPerThread;
+    int64_t o, un, at;
+    thread_counts(status, bitmap, u0, n_units, o, un, at);
+    int64_t to, tu, ta;
+    block_inclusive_scan(o, lds[0], to);
+    block_inclusive_scan(un, lds[1], tu);
+    block_inclusive_scan(at, lds[2], ta);
+    if (threadIdx.x == 0) seg[blockIdx.x] = SegCount{to, tu, ta};
+}
+
+// One workgroup: exclusive offsets of the segments and the totals.
+__global__ void __launch_bounds__(kLocThreads) localize_scan_kernel(SegCount* __restrict__ seg,
+                                                                     int64_t n_seg,
+                                                                     int64_t* __restrict__ counts) {
+    __shared__ int64_t lds[3][kLocThreads / 64];
+    int64_t carry_o = 0, carry_u = 0, carry_a = 0;
+    for (int64_t base = 0; base < n_seg; base += kLocThreads) {
+        const int64_t s = base + threadIdx.x;
+        SegCount c = s < n_seg ? seg[s] : SegCount{0, 0, 0};
+        int64_t to, tu, ta;
+        const int64_t io = block_inclusive_scan(c.n_out, lds[0], to);
+        const int64_t iu = block_inclusive_scan(c.n_und, lds[1], tu);
+        block_inclusive_scan(c.n_att, lds[2], ta);
+        if (s < n_seg) seg[s] = SegCount{carry_o + io - c.n_out, carry_u + iu - c.n_und, 0};
+        carry_o += to;
+        carry_u += tu;
+        carry_a += ta;
+    }
+    if (threadIdx.x == 0) {
+        counts[0] = carry_o;
+        counts[1] = carry_u;
+        counts[2] = carry_a;
+    }
+}
+
+__global__ void __launch_bounds__(kLocThreads) localize_emit_kernel(
+    const uint8_t* __restrict__ status, const uint64_t* __restrict__ bitmap,
+    const int32_t* __restrict__ majority_idx, const c3_chunk_record_t* __restrict__ records, int R,
+    int64_t n_units, const SegCount* __restrict__ seg, c3_outlier_t* __restrict__ outliers,
+    int64_t out_cap, int64_t* __restrict__ undecided, int64_t und_cap) {
+    __shared__ int64_t lds[2][kLocThreads / 64];
+    const int64_t u0 = (int64_t)blockIdx.x * kSegUnits + (int64_t)threadIdx.x * kPerThread;
+    int64_t o, un, at;
+    thread_counts(status, bitmap, u0, n_units, o, un, at);
+    int64_t to, tu;
+    int64_t po = block_inclusive_scan(o, lds[0], to) - o + seg[blockIdx.x].n_out;
+    int64_t pu = block_inclusive_scan(un, lds[1], tu) - un + seg[blockIdx.x].n_und;
+    for (int i = 0; i < kPerThread; ++i) {
+        const int64_t u = u0 + i;
+        if (u >= n_units) break;
+        if (status[u] == C3_INCONCLUSIVE) {
+            if (pu < und_cap) undecided[pu] = u;
+            ++pu;
+            continue;
+        }
+        uint64_t b = bitmap[u];
+        if (!b) continue;
+        const int32_t mj = majority_idx[u];
+        while (b) {
+            const int r = __builtin_ctzll(b);
+            b &= b - 1;
+            if (po < out_cap) {
+                c3_outlier_t e;
+                e.chunk = u;
+                e.replica = r;
+                e.majority_replica = mj;
+                for (int z = 0; z < 2; ++z) {
+                    const int rr = z == 0 ? r : mj;
+                    if (records != nullptr && rr >= 0 && rr < R) {
+                        const c3_chunk_record_t& rec = records[(int64_t)rr * n_units + u];
+                        e.nan_count[z] = rec.nan_count;
+                        e.inf_count[z] = rec.inf_count;
+                        e.absmax[z] = rec.absmax;
+                        e.sum[z] = rec.sum;
+                        e.sumsq[z] = rec.sumsq;
+                    } else {
+                        e.nan_count[z] = 0;
+                        e.inf_count[z] = 0;
+                        e.absmax[z] = 0.0;
+                        e.sum[z] = 0.0;
+                        e.sumsq[z] = 0.0;
+                    }
+                }
+                outliers[po] = e;
+            }
+            ++po;
+        }
+    }
+}
+
+size_t localize_ws_bytes(int64_t n_units) {
+    const int64_t n_seg = n_units > 0 ? (n_units + kSegUnits - 1) / kSegUnits : 0;
+    return (size_t)(n_seg * (int64_t)sizeof(SegCount)) + 256;
+}
+
+hipError_t launch_localize(const uint8_t* status, const uint64_t* bitmap,
+                           const int32_t* majority_idx, const c3_chunk_record_t* records, int R,
+                           int64_t n_units, c3_outlier_t* outliers, int64_t out_cap,
+                           int64_t* undecided, int64_t und_cap, int64_t* counts, void* ws,
+                           hipStream_t stream) {
+    const int64_t n_seg = n_units > 0 ? (n_units + kSegUnits - 1) / kSegUnits : 0;
+    if (n_seg > 0x7FFFFFFF) return hipErrorInvalidValue;
+    SegCount* seg = static_cast<SegCount*>(ws);
+    if (n_seg > 0) {
+        hipLaunchKernelGGL(localize_count_kernel, dim3((unsigned)n_seg), dim3(kLocThreads), 0, stream,
+                           status, bitmap, n_units, seg);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(localize_scan_kernel, dim3(1), dim3(kLocThreads), 0, stream, seg, n_seg,
+                       counts);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || n_seg == 0) return e;
+    hipLaunchKernelGGL(localize_emit_kernel, dim3((unsigned)n_seg), dim3(kLocThreads), 0, stream,
+                       status, bitmap, majority_idx, records, R, n_units, seg, outliers, out_cap,
+                       undecided, und_cap);
+    return hipGetLastError();
+}
+
+}  // namespace c3

@@ -1,0 +1,435 @@
+// Streaming signature kernel of C3 for gfx950.
+//
+// Per (replica, chunk) it computes the C3SIG-1 signature -- a per-chunk
+// reading of the paper's comparable evidence H_w(dtype, shape, bytes)
+// (Sec. 5.2) -- and, in the same single pass over HBM, the chunk's NaN/Inf
+// counts, absmax and fp64 sum / sum of squares of the finite elements.
+//
+// C3SIG-1 over a chunk of n bytes: the bytes, zero-padded to a multiple of 16,
+// are little-endian u32 words m[0..D-1], D = 4 ceil(n / 16).  Keys K[i] are
+// the low 32 bits of SplitMix64 outputs i = 0..257 from a fixed seed.  For
+// each word pair p = 2i, with q = p mod 256 and beta = (p div 256) * 0x9E3779B9
+// (all u32 arithmetic wraps):
+//     A += (m[p] + K[q] + beta) * (m[p+1] + K[q+1] + beta)      (u64, wraps)
+//     B += (m[p] + K[q+2] + beta) * (m[p+1] + K[q+3] + beta)
+// which is the NH hash of UMAC with a Toeplitz-shifted second key row.  The
+// signature is an fmix64 chain over (tag ^ dtype << 32 ^ ndim, shape dims,
+// chunk index, n, A, B).  A and B are sums, so any partition of the chunk
+// gives the same bits.
+//
+// Work decomposition: a chunk is cut into tiles of tile_bytes (a power of two
+// >= 1 KiB dividing chunk_bytes).  One 256-thread workgroup folds one tile:
+// its four waves take the tile's 1 KiB blocks round-robin, every lane loads
+// 16 bytes of a block with one 128-bit load, so one wave-wide load covers
+// exactly 256 words and lane l always owns key positions 4l .. 4l+5 (held in
+// VGPRs for the whole kernel) while beta is wave-uniform.  Lanes reduce with
+// xor butterflies, waves combine through LDS in a fixed order, and each tile
+// writes one 64-byte partial.  When a chunk is a single tile the workgroup
+// writes the chunk record directly; otherwise a finalize kernel combines the
+// chunk's partials in tile order.  The per-tile arithmetic never depends on
+// which workgroup runs it, so results are independent of the grid size.
+//
+// Non-finite screen: a lane sums its elements in fp64 without looking at
+// them.  A non-finite element is the only way its sum or sum of squares can
+// become non-finite (finite fp32/bf16/fp16 values cannot overflow fp64 here),
+// so a lane whose sums end non-finite re-reads its own segments and
+// classifies every element.  Healthy data never takes that path.
+#include "c3_device.h"
+#include "c3_internal.h"
+
+namespace c3 {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint16_t u16x2 __attribute__((ext_vector_type(2)));
+typedef const __attribute__((address_space(1))) u32x4 gu32x4;
+
+struct LaneKeys {
+    uint32_t k0, k1, k2, k3, k4, k5;
+};
+
+// 128-bit streaming load from global memory, non-temporal (read once).
+__device__ inline u32x4 load16(const u32x4* p) {
+    return __builtin_nontemporal_load((gu32x4*)p);
+}
+
+// NH over one 16-byte segment (two word pairs) at key offset 4 * lane.
+__device__ inline void nh16(const u32x4 v, const LaneKeys& K, uint32_t beta, uint64_t& A,
+                            uint64_t& B) {
+    A += (uint64_t)(v.x + K.k0 + beta) * (uint64_t)(v.y + K.k1 + beta);
+    B += (uint64_t)(v.x + K.k2 + beta) * (uint64_t)(v.y + K.k3 + beta);
+    A += (uint64_t)(v.z + K.k2 + beta) * (uint64_t)(v.w + K.k3 + beta);
+    B += (uint64_t)(v.z + K.k4 + beta) * (uint64_t)(v.w + K.k5 + beta);
+}
+
+__device__ inline double f16_to_f64(uint32_t h) {
+    _Float16 x = __builtin_bit_cast(_Float16, (uint16_t)h);
+    return (double)(float)x;
+}
+
+// ---------------------------------------------------------------------------
+// fast statistics: no classification; `mx` collects magnitude bits (two
+// packed u16 lanes for the 16-bit types)
+// ---------------------------------------------------------------------------
+template <int DT>
+__device__ inline void stats_fast(const u32x4 v, double& s, double& q, uint32_t& mx) {
+    if constexpr (DT == C3_F32) {
+        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            double d = (double)__uint_as_float(w[i]);
+            s += d;
+            q = __fma_rn(d, d, q);
+            mx = max(mx, w[i] & 0x7FFFFFFFu);
+        }
+    } else if constexpr (DT == C3_BF16 || DT == C3_F16) {
+        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+        u16x2 m2 = __builtin_bit_cast(u16x2, mx);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            double lo, hi;
+            if constexpr (DT == C3_BF16) {
+                lo = (double)__uint_as_float(w[i] << 16);
+                hi = (double)__uint_as_float(w[i] & 0xFFFF0000u);
+            } else {
+                lo = f16_to_f64(w[i] & 0xFFFFu);
+                hi = f16_to_f64(w[i] >> 16);
+            }
+            s += lo;
+            q = __fma_rn(lo, lo, q);
+            s += hi;
+            q = __fma_rn(hi, hi, q);
+            m2 = __builtin_elementwise_max(m2, __builtin_bit_cast(u16x2, w[i] & 0x7FFF7FFFu));
+        }
+        mx = __builtin_bit_cast(uint32_t, m2);
+    }
+}
+
+// slow statistics: classify each element; `mx` is a plain magnitude
+template <int DT>
+__device__ inline void stats_slow(const u32x4 v, double& s, double& q, uint32_t& mx,
+                                  uint32_t& nan_c, uint32_t& inf_c) {
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+    if constexpr (DT == C3_F32) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            uint32_t mag = w[i] & 0x7FFFFFFFu;
+            if (mag >= 0x7F800000u) {
+                if (mag > 0x7F800000u) ++nan_c; else ++inf_c;
+                continue;
+            }
+            double d = (double)__uint_as_float(w[i]);
+            s += d;
+            q = __fma_rn(d, d, q);
+            mx = max(mx, mag);
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            uint32_t h = (i & 1) ? (w[i >> 1] >> 16) : (w[i >> 1] & 0xFFFFu);
+            uint32_t mag = h & 0x7FFFu;
+            const uint32_t inf_bits = (DT == C3_BF16) ? 0x7F80u : 0x7C00u;
+            if (mag >= inf_bits) {
+                if (mag > inf_bits) ++nan_c; else ++inf_c;
+                continue;
+            }
+            double d = (DT == C3_BF16) ? (double)__uint_as_float(h << 16) : f16_to_f64(h);
+            s += d;
+            q = __fma_rn(d, d, q);
+            mx = max(mx, mag);
+        }
+    }
+}
+
+// Tail segment of a tile: bytes [0, rem) of a 16-byte segment, rest zero.
+__device__ inline u32x4 load_partial(const uint8_t* p, uint32_t rem) {
+    uint32_t w[4] = {0u, 0u, 0u, 0u};
+    for (uint32_t b = 0; b < rem; ++b) w[b >> 2] |= (uint32_t)p[b] << (8 * (b & 3));
+    u32x4 v;
+    v.x = w[0];
+    v.y = w[1];
+    v.z = w[2];
+    v.w = w[3];
+    return v;
+}
+
+struct LaneFold {
+    uint64_t A, B;
+    double s, q;
+    uint32_t mx, nan_c, inf_c;
+};
+
+// One wave's share of a tile: blocks wave, wave + 4, ... of `len` bytes.
+template <int DT, int U>
+__device__ inline LaneFold fold_lane(const uint8_t* tile, uint32_t len, uint32_t blk0,
+                                     const LaneKeys& K, int wave, int lane) {
+    LaneFold f{0, 0, 0.0, 0.0, 0u, 0u, 0u};
+    const u32x4* p = reinterpret_cast<const u32x4*>(tile) + lane;
+    const int nfull = (int)(len >> 10);
+    const uint32_t tail = len & 1023u;
+    int k = wave;
+    for (; k + 4 * (U - 1) < nfull; k += 4 * U) {
+        u32x4 v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) v[u] = load16(p + (size_t)(k + 4 * u) * 64);
+        // keep all U loads in flight before the first use
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const uint32_t beta = (blk0 + (uint32_t)(k + 4 * u)) * kBlockMul;
+            nh16(v[u], K, beta, f.A, f.B);
+            stats_fast<DT>(v[u], f.s, f.q, f.mx);
+        }
+    }
+    for (; k < nfull; k += 4) {
+        u32x4 v = load16(p + (size_t)k * 64);
+        nh16(v, K, (blk0 + (uint32_t)k) * kBlockMul, f.A, f.B);
+        stats_fast<DT>(v, f.s, f.q, f.mx);
+    }
+    const uint32_t off = (uint32_t)lane * 16u;
+    const bool has_tail = tail != 0u && (nfull & 3) == wave && off < tail;
+    if (has_tail) {
+        const uint8_t* seg = tile + ((size_t)nfull << 10) + off;
+        u32x4 v = (off + 16u <= tail) ? load16(reinterpret_cast<const u32x4*>(seg))
+                                      : load_partial(seg, tail - off);
+        nh16(v, K, (blk0 + (uint32_t)nfull) * kBlockMul, f.A, f.B);
+        stats_fast<DT>(v, f.s, f.q, f.mx);
+    }
+    if constexpr (DT == C3_BF16 || DT == C3_F16) f.mx = max(f.mx & 0xFFFFu, f.mx >> 16);
+    if constexpr (DT != C3_RAW) {
+        if (!__builtin_isfinite(f.s) || !__builtin_isfinite(f.q)) {
+            // rare: this lane saw a NaN or Inf; redo its statistics classifying
+            f.s = 0.0;
+            f.q = 0.0;
+            f.mx = 0u;
+            for (int kk = wave; kk < nfull; kk += 4)
+                stats_slow<DT>(load16(p + (size_t)kk * 64), f.s, f.q, f.mx, f.nan_c, f.inf_c);
+            if (has_tail) {
+                const uint8_t* seg = tile + ((size_t)nfull << 10) + off;
+                u32x4 v = (off + 16u <= tail) ? load16(reinterpret_cast<const u32x4*>(seg))
+                                              : load_partial(seg, tail - off);
+                stats_slow<DT>(v, f.s, f.q, f.mx, f.nan_c, f.inf_c);
+            }
+        }
+    }
+    return f;
+}
+
+__device__ inline TilePartial wave_reduce(const LaneFold& f) {
+    TilePartial p;
+    p.A = f.A;
+    p.B = f.B;
+    p.s = f.s;
+    p.sc = 0.0;
+    p.q = f.q;
+    p.qc = 0.0;
+    p.maxbits = f.mx;
+    p.nan_count = f.nan_c;
+    p.inf_count = f.inf_c;
+    p.pad = 0u;
+    // Lane sums meet in a fixed six-level butterfly of plain fp64 adds (error
+    // at most 6 ulp of the sum of magnitudes); compensation starts at the
+    // cross-wave level.
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) {
+        p.A += shfl_xor_u64(p.A, m);
+        p.B += shfl_xor_u64(p.B, m);
+        p.s += shfl_xor_f64(p.s, m);
+        p.q += shfl_xor_f64(p.q, m);
+        p.maxbits = max(p.maxbits, shfl_xor_u32(p.maxbits, m));
+    }
+    if (ballot64(f.nan_c != 0u || f.inf_c != 0u) != 0ull) {
+#pragma unroll
+        for (int m = 32; m >= 1; m >>= 1) {
+            p.nan_count += shfl_xor_u32(p.nan_count, m);
+            p.inf_count += shfl_xor_u32(p.inf_count, m);
+        }
+    }
+    return p;
+}
+
+__device__ inline void partial_add(TilePartial& a, const TilePartial& b) {
+    a.A += b.A;
+    a.B += b.B;
+    comp_add(a.s, a.sc, b.s, b.sc);
+    comp_add(a.q, a.qc, b.q, b.qc);
+    a.maxbits = max(a.maxbits, b.maxbits);
+    a.nan_count += b.nan_count;
+    a.inf_count += b.inf_count;
+}
+
+__device__ inline int find_segment(const int64_t* base, int n, int64_t j) {
+    // largest t in [0, n) with base[t] <= j  (base[0] = 0, base ascending)
+    int lo = 0, hi = n;
+    while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (base[mid] <= j) lo = mid; else hi = mid;
+    }
+    return lo;
+}
+
+__device__ inline double maxbits_to_f64(uint32_t bits, int dtype) {
+    if (dtype == C3_F32) return (double)__uint_as_float(bits);
+    if (dtype == C3_BF16) return (double)__uint_as_float(bits << 16);
+    if (dtype == C3_F16) return f16_to_f64(bits);
+    return 0.0;
+}
+
+__device__ inline void write_record(c3_chunk_record_t* rec, const TensorInfo* tip, int t,
+                                    uint64_t k, uint64_t n, const TilePartial& p) {
+    const int dtype = tip->dtype, ndim = tip->ndim;
+    uint64_t h = fmix64(kTag ^ ((uint64_t)(uint32_t)dtype << 32) ^ (uint64_t)(uint32_t)ndim);
+    for (int d = 0; d < ndim; ++d) h = fmix64(h ^ (uint64_t)tip->shape[d]);
+    h = fmix64(h ^ k);
+    h = fmix64(h ^ n);
+    h = fmix64(h ^ p.A);
+    h = fmix64(h ^ p.B);
+    const uint64_t es = dtype == C3_F32 ? 4 : (dtype == C3_RAW ? 1 : 2);
+    rec->sig = h;
+    rec->n_elems = n / es;
+    rec->nan_count = p.nan_count;
+    rec->inf_count = p.inf_count;
+    rec->tensor = (uint32_t)t;
+    rec->chunk_in_tensor = (uint32_t)k;
+    rec->absmax = maxbits_to_f64(p.maxbits, dtype);
+    rec->sum = p.s + p.sc;
+    rec->sumsq = p.q + p.qc;
+    rec->reserved = 0;
+}
+
+// One launch per element type present in the plan.  The plan lists the
+// tensors grouped by type (order[], stable in call order) with a tile prefix
+// over that order (gtile[]); this launch covers group positions [gk0, gk1)
+// of every replica.
+template <int DT, int U>
+__global__ void __launch_bounds__(kSigThreads, 8) signature_kernel(const SigPlan* __restrict__ plan,
+                                                                c3_chunk_record_t* __restrict__ records,
+                                                                int gk0, int gk1, int64_t gtiles) {
+    __shared__ TilePartial lds[kSigThreads / 64];
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const char* pb = reinterpret_cast<const char*>(plan);
+    const uint64_t* ptrs = reinterpret_cast<const uint64_t*>(pb + plan->off_ptrs);
+    const int64_t* tile_base = reinterpret_cast<const int64_t*>(pb + plan->off_tile_base);
+    const int64_t* chunk_base = reinterpret_cast<const int64_t*>(pb + plan->off_chunk_base);
+    const int32_t* order = reinterpret_cast<const int32_t*>(pb + plan->off_order);
+    const int64_t* gtile = reinterpret_cast<const int64_t*>(pb + plan->off_gtile);
+    const TensorInfo* tinfo = reinterpret_cast<const TensorInfo*>(pb + plan->off_tmeta);
+    TilePartial* partials = reinterpret_cast<TilePartial*>(const_cast<char*>(pb) + plan->off_partials);
+    const int T = plan->T;
+    const int64_t ntiles = gtiles * plan->R;
+    const uint64_t tile_bytes = plan->tile_bytes;
+    const uint32_t tpc = plan->tiles_per_chunk;
+    const int64_t g0 = gtile[gk0];
+
+    LaneKeys K;
+    K.k0 = nh_key(4u * lane + 0u);
+    K.k1 = nh_key(4u * lane + 1u);
+    K.k2 = nh_key(4u * lane + 2u);
+    K.k3 = nh_key(4u * lane + 3u);
+    K.k4 = nh_key(4u * lane + 4u);
+    K.k5 = nh_key(4u * lane + 5u);
+
+    for (int64_t i = blockIdx.x; i < ntiles; i += gridDim.x) {
+        const int64_t r = i / gtiles;
+        const int64_t j = g0 + (i - r * gtiles);
+        const int k = gk0 + find_segment(gtile + gk0, gk1 - gk0, j);
+        const int t = order[k];
+        const int64_t lt = j - gtile[k];
+        const uint64_t nbytes = tinfo[t].nbytes;
+        const uint64_t toff = (uint64_t)lt * tile_bytes;
+        const uint32_t len = nbytes > toff ? (uint32_t)min(tile_bytes, nbytes - toff) : 0u;
+        const uint32_t blk0 = (uint32_t)(((uint64_t)(lt % tpc) * tile_bytes) >> 10);
+        const uint8_t* tile = reinterpret_cast<const uint8_t*>(ptrs[r * T + t]) + toff;
+
+        const LaneFold f = fold_lane<DT, U>(tile, len, blk0, K, wave, lane);
+        const TilePartial wp = wave_reduce(f);
+        if (lane == 0) lds[wave] = wp;
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            TilePartial p = lds[0];
+#pragma unroll
+            for (int w = 1; w < kSigThreads / 64; ++w) partial_add(p, lds[w]);
+            if (plan->direct) {
+                const uint64_t kc = (uint64_t)lt;  // one tile per chunk
+                const uint64_t n = nbytes > toff ? min(plan->chunk_bytes, nbytes - toff) : 0;
+                write_record(&records[r * plan->C + chunk_base[t] + (int64_t)kc], tinfo + t, t, kc, n, p);
+            } else {
+                partials[r * plan->tiles_per_replica + tile_base[t] + lt] = p;
+            }
+        }
+        __syncthreads();
+    }
+}
+
+// Combine the partials of each (replica, chunk) in tile order.
+__global__ void __launch_bounds__(256) finalize_kernel(const SigPlan* __restrict__ plan,
+                                                       c3_chunk_record_t* __restrict__ records) {
+    const char* pb = reinterpret_cast<const char*>(plan);
+    const int64_t* tile_base = reinterpret_cast<const int64_t*>(pb + plan->off_tile_base);
+    const int64_t* chunk_base = reinterpret_cast<const int64_t*>(pb + plan->off_chunk_base);
+    const TensorInfo* tinfo = reinterpret_cast<const TensorInfo*>(pb + plan->off_tmeta);
+    const TilePartial* partials = reinterpret_cast<const TilePartial*>(pb + plan->off_partials);
+    const int64_t C = plan->C;
+    const int64_t total = C * plan->R;
+    for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
+         idx += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t r = idx / C;
+        const int64_t c = idx - r * C;
+        const int t = find_segment(chunk_base, plan->T, c);
+        const uint64_t k = (uint64_t)(c - chunk_base[t]);
+        const uint64_t nbytes = tinfo[t].nbytes;
+        const int64_t tiles_t = tile_base[t + 1] - tile_base[t];
+        const int64_t lt0 = (int64_t)k * plan->tiles_per_chunk;
+        const int64_t nt = min((int64_t)plan->tiles_per_chunk, tiles_t - lt0);
+        const TilePartial* pp = partials + r * plan->tiles_per_replica + tile_base[t] + lt0;
+        TilePartial p = pp[0];
+        for (int64_t x = 1; x < nt; ++x) partial_add(p, pp[x]);
+        const uint64_t coff = k * plan->chunk_bytes;
+        const uint64_t n = nbytes > coff ? min(plan->chunk_bytes, nbytes - coff) : 0;
+        write_record(&records[idx], tinfo + t, t, k, n, p);
+    }
+}
+
+template <int DT>
+static hipError_t launch_group(const SigPlan* dplan, c3_chunk_record_t* records, int gk0, int gk1,
+                               int64_t gtiles, int R, int grid_blocks, hipStream_t stream) {
+    const int64_t ntiles = gtiles * R;
+    if (ntiles <= 0) return hipSuccess;
+    int64_t grid = grid_blocks > 0 ? grid_blocks : ntiles;
+    if (grid > ntiles) grid = ntiles;
+    if (grid > 0x7FFFFFFF) grid = 0x7FFFFFFF;
+    hipLaunchKernelGGL((signature_kernel<DT, kUnroll>), dim3((unsigned)grid), dim3(kSigThreads), 0,
+                       stream, dplan, records, gk0, gk1, gtiles);
+    return hipGetLastError();
+}
+
+hipError_t launch_signature(const SigPlan* dplan, const SigPlan& hplan, const SigGroups& groups,
+                            c3_chunk_record_t* records, int grid_blocks, hipStream_t stream,
+                            hipEvent_t ev0, hipEvent_t ev1) {
+    hipError_t e;
+    if (ev0 && (e = hipEventRecord(ev0, stream)) != hipSuccess) return e;
+    for (int d = 0; d < 4; ++d) {
+        const int gk0 = groups.k0[d], gk1 = groups.k1[d];
+        if (gk1 <= gk0) continue;
+        const int64_t gt = groups.tiles[d];
+        switch (d) {
+            case C3_F32: e = launch_group<C3_F32>(dplan, records, gk0, gk1, gt, hplan.R, grid_blocks, stream); break;
+            case C3_BF16: e = launch_group<C3_BF16>(dplan, records, gk0, gk1, gt, hplan.R, grid_blocks, stream); break;
+            case C3_F16: e = launch_group<C3_F16>(dplan, records, gk0, gk1, gt, hplan.R, grid_blocks, stream); break;
+            default: e = launch_group<C3_RAW>(dplan, records, gk0, gk1, gt, hplan.R, grid_blocks, stream); break;
+        }
+        if (e != hipSuccess) return e;
+    }
+    if (ev1 && (e = hipEventRecord(ev1, stream)) != hipSuccess) return e;
+    if (!hplan.direct) {
+        const int64_t total = hplan.C * hplan.R;
+        const int64_t blocks = (total + 255) / 256 < 65536 ? (total + 255) / 256 : 65536;
+        hipLaunchKernelGGL(finalize_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, dplan,
+                           records);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+}  // namespace c3
