@@ -16,8 +16,10 @@
  *
  * Common conventions
  *   - Device pointers are plain HIP device addresses owned by the caller.
- *     The library allocates no device or host memory that outlives a call
- *     and keeps no state between calls.
+ *     The library allocates no device memory.  Its only state between calls
+ *     is a 2 MiB ring of pinned host memory per device (allocated on first
+ *     use, kept until the process ends) through which c3_signature stages
+ *     its plan, so that staging never makes the host wait for the GPU.
  *   - Host arrays passed in (pointer tables, tensor metadata) are consumed
  *     before the call returns; the caller may free them immediately.
  *   - Every call enqueues work on `stream` and returns without waiting; its
@@ -152,6 +154,11 @@ typedef struct {
  *     timing that kernel alone).
  *   grid_blocks: workgroups of the streaming kernel; 0 chooses one per tile.
  *     Results do not depend on it.
+ *   flags: C3_OPT_PLAN_STAGED -- the workspace still holds the plan that a
+ *     previous c3_signature[_ex] call staged there with identical ptrs,
+ *     metas, T, R, chunk_bytes and tile_bytes, and the caller has not written
+ *     to the workspace since; staging is skipped.  The caller is responsible
+ *     for that promise: a stale plan reads stale pointers.
  *   tile_bytes: bytes one workgroup folds into one partial; 0 chooses the
  *     default.  Must be a power-of-two multiple of 1024 dividing chunk_bytes
  *     (checked); the fp64 sums may differ in the last bits between tile
@@ -160,9 +167,11 @@ typedef struct {
     c3_event_t ev_kernel_begin;
     c3_event_t ev_kernel_end;
     int32_t grid_blocks;
-    int32_t reserved;
+    int32_t flags;
     uint64_t tile_bytes;
 } c3_launch_opts_t;
+
+#define C3_OPT_PLAN_STAGED 1
 
 /* Number of chunks C of the chunk plan: each tensor is split on its own into
  * ceil(nbytes / chunk_bytes) chunks (the last may be partial; an empty

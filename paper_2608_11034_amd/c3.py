@@ -31,6 +31,7 @@ EV_U64, EV_U32, EV_F32, EV_F64 = 0, 1, 2, 3
 AGREE, ATTRIBUTED, INCONCLUSIVE = 0, 1, 2
 KAPPA_DEFAULT = 3.5 / 0.6745
 RANK_STRAGGLER, RANK_PROTOCOL, RANK_CONSEC2 = 1, 2, 4
+OPT_PLAN_STAGED = 1
 
 RECORD_DTYPE = np.dtype([("sig", "<u8"), ("n_elems", "<u8"), ("nan_count", "<u4"),
                          ("inf_count", "<u4"), ("tensor", "<u4"), ("chunk_in_tensor", "<u4"),
@@ -56,7 +57,7 @@ class TensorMeta(ctypes.Structure):
 
 class LaunchOpts(ctypes.Structure):
     _fields_ = [("ev_kernel_begin", ctypes.c_void_p), ("ev_kernel_end", ctypes.c_void_p),
-                ("grid_blocks", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("grid_blocks", ctypes.c_int32), ("flags", ctypes.c_int32),
                 ("tile_bytes", ctypes.c_uint64)]
 
 
@@ -199,10 +200,15 @@ class SignaturePlan:
     def new_workspace(self):
         return _empty((self.ws_bytes,), torch.uint8, self.device)
 
-    def run(self, records, workspace, stream=None, ev_begin=None, ev_end=None, grid_blocks=0):
+    def run(self, records, workspace, stream=None, ev_begin=None, ev_end=None, grid_blocks=0,
+            plan_staged=False):
+        """Launch c3_signature.  plan_staged=True promises that `workspace` still
+        holds the plan a previous run of this object staged (see
+        C3_OPT_PLAN_STAGED)."""
         opts = LaunchOpts(ev_begin.cuda_event if ev_begin is not None else None,
                           ev_end.cuda_event if ev_end is not None else None,
-                          int(grid_blocks), 0, self.tile_bytes)
+                          int(grid_blocks), OPT_PLAN_STAGED if plan_staged else 0,
+                          self.tile_bytes)
         rc = lib().c3_signature_ex(self.ptrs, self.metas, self.T, self.R, self.chunk_bytes,
                                    _ptr(records), _ptr(workspace), workspace.numel(),
                                    _stream(stream), ctypes.byref(opts))

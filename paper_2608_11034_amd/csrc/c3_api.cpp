@@ -4,6 +4,7 @@
 // kernels.
 #include <string.h>
 
+#include <mutex>
 #include <vector>
 
 #include "c3_internal.h"
@@ -125,6 +126,65 @@ int make_plan(const c3_tensor_meta_t* metas, int T, int R, uint64_t chunk_bytes,
 
 inline bool aligned(const void* p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
 
+// ---------------------------------------------------------------------------
+// Plan staging.  A copy from pageable host memory makes the host wait for the
+// stream before it returns, and a copy-engine transfer costs a cross-engine
+// synchronization on each side.  Plans are therefore written into a small
+// ring of pinned host slots per device (allocated on first use, kept until
+// the process ends) and pulled into the workspace by a kernel on the caller's
+// stream; a slot is reused only after the kernel that read it has completed.
+// Plans larger than a slot (256 KB, about 1,500 tensors at R = 8) fall back
+// to a pageable copy.  The buffer holds whole 16-byte words, so the
+// staged size is rounded up to 16.
+// ---------------------------------------------------------------------------
+constexpr int kStageSlots = 8;
+constexpr size_t kStageSlotBytes = 256 * 1024;
+constexpr int kMaxDevices = 64;
+
+struct Stager {
+    std::mutex mu;
+    bool ready = false;
+    bool failed = false;
+    unsigned char* host = nullptr;
+    hipEvent_t ev[kStageSlots] = {};
+    bool pending[kStageSlots] = {};
+    int next = 0;
+};
+
+Stager g_stagers[kMaxDevices];
+
+// Copies `bytes` of `src` to device `dst` on `s`; returns a HIP error code.
+hipError_t stage_to_device(void* dst, const void* src, size_t bytes, hipStream_t s) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices || bytes > kStageSlotBytes)
+        return hipMemcpyAsync(dst, src, bytes, hipMemcpyHostToDevice, s);
+    Stager& st = g_stagers[dev];
+    std::lock_guard<std::mutex> lock(st.mu);
+    if (!st.ready && !st.failed) {
+        if (hipHostMalloc(reinterpret_cast<void**>(&st.host), kStageSlots * kStageSlotBytes,
+                          hipHostMallocDefault) != hipSuccess) {
+            st.failed = true;
+        } else {
+            for (int i = 0; i < kStageSlots && !st.failed; ++i)
+                if (hipEventCreateWithFlags(&st.ev[i], hipEventDisableTiming) != hipSuccess)
+                    st.failed = true;
+            st.ready = !st.failed;
+        }
+    }
+    if (!st.ready) return hipMemcpyAsync(dst, src, bytes, hipMemcpyHostToDevice, s);
+    const int slot = st.next;
+    st.next = (st.next + 1) % kStageSlots;
+    if (st.pending[slot] && (e = hipEventSynchronize(st.ev[slot])) != hipSuccess) return e;
+    unsigned char* h = st.host + (size_t)slot * kStageSlotBytes;
+    memcpy(h, src, bytes);
+    if ((e = c3::launch_plan_fetch(h, dst, bytes, s)) != hipSuccess) return e;
+    if ((e = hipEventRecord(st.ev[slot], s)) != hipSuccess) return e;
+    st.pending[slot] = true;
+    return hipSuccess;
+}
+
 }  // namespace
 
 extern "C" {
@@ -179,7 +239,7 @@ int c3_signature_ex(const void* const* ptrs, const c3_tensor_meta_t* metas, int 
             if (!aligned(q, 16)) return C3_E_ALIGN;
         }
     // stage the plan: header, pointer table, bases, tensor info
-    std::vector<unsigned char> buf(p.h.off_partials, 0);
+    std::vector<unsigned char> buf(align_up(p.h.off_partials, 16), 0);
     memcpy(buf.data(), &p.h, sizeof(SigPlan));
     for (size_t i = 0; i < (size_t)R * (size_t)T; ++i) {
         const uint64_t a = (uint64_t)(uintptr_t)ptrs[i];
@@ -191,8 +251,8 @@ int c3_signature_ex(const void* const* ptrs, const c3_tensor_meta_t* metas, int 
     memcpy(buf.data() + p.h.off_order, p.order.data(), 4ull * T);
     memcpy(buf.data() + p.h.off_gtile, p.gtile.data(), 8ull * (T + 1));
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    if (hipMemcpyAsync(ws, buf.data(), buf.size(), hipMemcpyHostToDevice, s) != hipSuccess)
-        return C3_E_HIP;
+    const bool staged = opts != nullptr && (opts->flags & C3_OPT_PLAN_STAGED) != 0;
+    if (!staged && stage_to_device(ws, buf.data(), buf.size(), s) != hipSuccess) return C3_E_HIP;
     const hipError_t e = c3::launch_signature(
         static_cast<const SigPlan*>(ws), p.h, p.groups, records, opts ? opts->grid_blocks : 0, s,
         opts ? reinterpret_cast<hipEvent_t>(opts->ev_kernel_begin) : nullptr,

@@ -53,9 +53,20 @@ static_assert(sizeof(c3_chunk_record_t) == 64, "record layout");
 static_assert(sizeof(c3_outlier_t) == 80, "outlier layout");
 static_assert(sizeof(c3_rank_verdict_t) == 24, "verdict layout");
 
-constexpr uint64_t kDefaultTileMax = 256 * 1024;
+// Tuning knobs of the streaming kernel (compile-time; results do not depend
+// on them except for the last bits of the fp64 sums through the tile size).
+#ifndef C3_SIG_TILE_MAX
+#define C3_SIG_TILE_MAX (1024 * 1024)
+#endif
+#ifndef C3_SIG_UNROLL
+#define C3_SIG_UNROLL 16
+#endif
+#ifndef C3_SIG_WAVES_PER_EU
+#define C3_SIG_WAVES_PER_EU 4
+#endif
+constexpr uint64_t kDefaultTileMax = C3_SIG_TILE_MAX;
 constexpr int kSigThreads = 256;
-constexpr int kUnroll = 4;
+constexpr int kUnroll = C3_SIG_UNROLL;
 
 // Position range [k0, k1) of each dtype in the grouped tensor order and the
 // tiles per replica of that group.
@@ -67,6 +78,10 @@ struct SigGroups {
 hipError_t launch_signature(const SigPlan* dplan, const SigPlan& hplan, const SigGroups& groups,
                             c3_chunk_record_t* records, int grid_blocks, hipStream_t stream,
                             hipEvent_t ev0, hipEvent_t ev1);
+
+// Copies `bytes` (rounded up to 16) from pinned, device-visible host memory
+// to device memory with a kernel on `stream`.
+hipError_t launch_plan_fetch(const void* host_src, void* dst, size_t bytes, hipStream_t stream);
 
 hipError_t launch_consensus(const void* evidence, int kind, int64_t rstride, int64_t ustride, int R,
                             int64_t n_units, int mode, double kappa, uint8_t* status,

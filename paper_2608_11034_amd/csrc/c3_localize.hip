@@ -45,7 +45,8 @@ __device__ inline void thread_counts(const uint8_t* status, const uint64_t* bitm
     }
 }
 
-// Inclusive prefix sum over the 256 threads of a workgroup (fixed order).
+// Inclusive prefix sum over the NT threads of a workgroup (fixed order).
+template <int NT = kLocThreads>
 __device__ inline int64_t block_inclusive_scan(int64_t v, int64_t* lds_wave, int64_t& total) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     int64_t x = v;
@@ -58,7 +59,7 @@ __device__ inline int64_t block_inclusive_scan(int64_t v, int64_t* lds_wave, int
     __syncthreads();
     int64_t before = 0;
     total = 0;
-    for (int w = 0; w < kLocThreads / 64; ++w) {
+    for (int w = 0; w < NT / 64; ++w) {
         if (w < wave) before += lds_wave[w];
         total += lds_wave[w];
     }
@@ -105,6 +106,43 @@ __global__ void __launch_bounds__(kLocThreads) localize_scan_kernel(SegCount* __
     }
 }
 
+__device__ inline void emit_units(const uint8_t* __restrict__ status,
+                                  const uint64_t* __restrict__ bitmap,
+                                  const int32_t* __restrict__ majority_idx,
+                                  const c3_chunk_record_t* __restrict__ records, int R,
+                                  int64_t n_units, int64_t u0, int64_t po, int64_t pu,
+                                  c3_outlier_t* __restrict__ outliers, int64_t out_cap,
+                                  int64_t* __restrict__ undecided, int64_t und_cap);
+
+// One outlier entry: unit, replica, majority replica and both summaries
+// (zeros when no record table is given).
+__device__ inline void write_outlier(c3_outlier_t* dst, int64_t u, int r, int32_t mj,
+                                     const c3_chunk_record_t* __restrict__ records, int R,
+                                     int64_t n_units) {
+    c3_outlier_t e;
+    e.chunk = u;
+    e.replica = r;
+    e.majority_replica = mj;
+    for (int z = 0; z < 2; ++z) {
+        const int rr = z == 0 ? r : mj;
+        if (records != nullptr && rr >= 0 && rr < R) {
+            const c3_chunk_record_t& rec = records[(int64_t)rr * n_units + u];
+            e.nan_count[z] = rec.nan_count;
+            e.inf_count[z] = rec.inf_count;
+            e.absmax[z] = rec.absmax;
+            e.sum[z] = rec.sum;
+            e.sumsq[z] = rec.sumsq;
+        } else {
+            e.nan_count[z] = 0;
+            e.inf_count[z] = 0;
+            e.absmax[z] = 0.0;
+            e.sum[z] = 0.0;
+            e.sumsq[z] = 0.0;
+        }
+    }
+    *dst = e;
+}
+
 __global__ void __launch_bounds__(kLocThreads) localize_emit_kernel(
     const uint8_t* __restrict__ status, const uint64_t* __restrict__ bitmap,
     const int32_t* __restrict__ majority_idx, const c3_chunk_record_t* __restrict__ records, int R,
@@ -117,6 +155,19 @@ __global__ void __launch_bounds__(kLocThreads) localize_emit_kernel(
     int64_t to, tu;
     int64_t po = block_inclusive_scan(o, lds[0], to) - o + seg[blockIdx.x].n_out;
     int64_t pu = block_inclusive_scan(un, lds[1], tu) - un + seg[blockIdx.x].n_und;
+    emit_units(status, bitmap, majority_idx, records, R, n_units, u0, po, pu, outliers, out_cap,
+               undecided, und_cap);
+}
+
+// Writes the entries of units [u0, u0 + kPerThread) starting at list
+// positions po (outliers) and pu (undecided).
+__device__ inline void emit_units(const uint8_t* __restrict__ status,
+                                  const uint64_t* __restrict__ bitmap,
+                                  const int32_t* __restrict__ majority_idx,
+                                  const c3_chunk_record_t* __restrict__ records, int R,
+                                  int64_t n_units, int64_t u0, int64_t po, int64_t pu,
+                                  c3_outlier_t* __restrict__ outliers, int64_t out_cap,
+                                  int64_t* __restrict__ undecided, int64_t und_cap) {
     for (int i = 0; i < kPerThread; ++i) {
         const int64_t u = u0 + i;
         if (u >= n_units) break;
@@ -131,32 +182,81 @@ __global__ void __launch_bounds__(kLocThreads) localize_emit_kernel(
         while (b) {
             const int r = __builtin_ctzll(b);
             b &= b - 1;
-            if (po < out_cap) {
-                c3_outlier_t e;
-                e.chunk = u;
-                e.replica = r;
-                e.majority_replica = mj;
-                for (int z = 0; z < 2; ++z) {
-                    const int rr = z == 0 ? r : mj;
-                    if (records != nullptr && rr >= 0 && rr < R) {
-                        const c3_chunk_record_t& rec = records[(int64_t)rr * n_units + u];
-                        e.nan_count[z] = rec.nan_count;
-                        e.inf_count[z] = rec.inf_count;
-                        e.absmax[z] = rec.absmax;
-                        e.sum[z] = rec.sum;
-                        e.sumsq[z] = rec.sumsq;
-                    } else {
-                        e.nan_count[z] = 0;
-                        e.inf_count[z] = 0;
-                        e.absmax[z] = 0.0;
-                        e.sum[z] = 0.0;
-                        e.sumsq[z] = 0.0;
-                    }
-                }
-                outliers[po] = e;
-            }
+            if (po < out_cap) write_outlier(&outliers[po], u, r, mj, records, R, n_units);
             ++po;
         }
+    }
+}
+
+// Small inputs: one workgroup of kSingleThreads walks the units in rounds of
+// kSingleThreads * kPerThread, carrying list offsets between rounds.  One
+// launch instead of three.  Each thread loads its units once and keeps them
+// in registers; the three per-thread counts travel through a single scan
+// packed into 21-bit fields of one 64-bit word (a round holds at most
+// 1024 * 8 * 64 = 2^19 outliers, so no field overflows).
+constexpr int kSingleThreads = 1024;
+constexpr int64_t kSingleMaxUnits = 4 * (int64_t)kSingleThreads * kPerThread;
+constexpr int kField = 21;
+constexpr int64_t kFieldMask = (1ll << kField) - 1;
+
+__global__ void __launch_bounds__(kSingleThreads) localize_single_kernel(
+    const uint8_t* __restrict__ status, const uint64_t* __restrict__ bitmap,
+    const int32_t* __restrict__ majority_idx, const c3_chunk_record_t* __restrict__ records, int R,
+    int64_t n_units, c3_outlier_t* __restrict__ outliers, int64_t out_cap,
+    int64_t* __restrict__ undecided, int64_t und_cap, int64_t* __restrict__ counts) {
+    __shared__ int64_t lds[kSingleThreads / 64];
+    int64_t carry_o = 0, carry_u = 0, carry_a = 0;
+    for (int64_t base = 0; base < n_units; base += (int64_t)kSingleThreads * kPerThread) {
+        const int64_t u0 = base + (int64_t)threadIdx.x * kPerThread;
+        uint8_t st[kPerThread];
+        uint64_t bm[kPerThread];
+#pragma unroll
+        for (int i = 0; i < kPerThread; ++i) {
+            const int64_t u = u0 + i;
+            st[i] = u < n_units ? status[u] : (uint8_t)C3_AGREE;
+            bm[i] = u < n_units ? bitmap[u] : 0ull;
+        }
+        int64_t o = 0, un = 0, at = 0;
+#pragma unroll
+        for (int i = 0; i < kPerThread; ++i) {
+            if (st[i] == C3_INCONCLUSIVE) {
+                ++un;
+            } else if (bm[i]) {
+                ++at;
+                o += __builtin_popcountll(bm[i]);
+            }
+        }
+        const int64_t packed = o | (un << kField) | (at << (2 * kField));
+        int64_t tot;
+        const int64_t excl = block_inclusive_scan<kSingleThreads>(packed, lds, tot) - packed;
+        int64_t po = carry_o + (excl & kFieldMask);
+        int64_t pu = carry_u + ((excl >> kField) & kFieldMask);
+#pragma unroll
+        for (int i = 0; i < kPerThread; ++i) {
+            const int64_t u = u0 + i;
+            if (st[i] == C3_INCONCLUSIVE) {
+                if (pu < und_cap) undecided[pu] = u;
+                ++pu;
+                continue;
+            }
+            uint64_t b = bm[i];
+            if (!b) continue;
+            const int32_t mj = majority_idx[u];
+            while (b) {
+                const int r = __builtin_ctzll(b);
+                b &= b - 1;
+                if (po < out_cap) write_outlier(&outliers[po], u, r, mj, records, R, n_units);
+                ++po;
+            }
+        }
+        carry_o += tot & kFieldMask;
+        carry_u += (tot >> kField) & kFieldMask;
+        carry_a += (tot >> (2 * kField)) & kFieldMask;
+    }
+    if (threadIdx.x == 0) {
+        counts[0] = carry_o;
+        counts[1] = carry_u;
+        counts[2] = carry_a;
     }
 }
 
@@ -170,7 +270,13 @@ hipError_t launch_localize(const uint8_t* status, const uint64_t* bitmap,
                            int64_t n_units, c3_outlier_t* outliers, int64_t out_cap,
                            int64_t* undecided, int64_t und_cap, int64_t* counts, void* ws,
                            hipStream_t stream) {
-    const int64_t n_seg = n_units > 0 ? (n_units + kSegUnits - 1) / kSegUnits : 0;
+    if (n_units <= kSingleMaxUnits) {
+        hipLaunchKernelGGL(localize_single_kernel, dim3(1), dim3(kSingleThreads), 0, stream, status,
+                           bitmap, majority_idx, records, R, n_units, outliers, out_cap, undecided,
+                           und_cap, counts);
+        return hipGetLastError();
+    }
+    const int64_t n_seg = (n_units + kSegUnits - 1) / kSegUnits;
     if (n_seg > 0x7FFFFFFF) return hipErrorInvalidValue;
     SegCount* seg = static_cast<SegCount*>(ws);
     if (n_seg > 0) {

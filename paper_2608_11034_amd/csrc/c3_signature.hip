@@ -301,7 +301,7 @@ __device__ inline void write_record(c3_chunk_record_t* rec, const TensorInfo* ti
 // over that order (gtile[]); this launch covers group positions [gk0, gk1)
 // of every replica.
 template <int DT, int U>
-__global__ void __launch_bounds__(kSigThreads, 8) signature_kernel(const SigPlan* __restrict__ plan,
+__global__ void __launch_bounds__(kSigThreads, C3_SIG_WAVES_PER_EU) signature_kernel(const SigPlan* __restrict__ plan,
                                                                 c3_chunk_record_t* __restrict__ records,
                                                                 int gk0, int gk1, int64_t gtiles) {
     __shared__ TilePartial lds[kSigThreads / 64];
@@ -388,6 +388,23 @@ __global__ void __launch_bounds__(256) finalize_kernel(const SigPlan* __restrict
         const uint64_t n = nbytes > coff ? min(plan->chunk_bytes, nbytes - coff) : 0;
         write_record(&records[idx], tinfo + t, t, k, n, p);
     }
+}
+
+// Copies the staged plan from pinned host memory into the workspace on the
+// compute queue (no copy engine, so no cross-engine synchronization).
+__global__ void __launch_bounds__(256) plan_fetch_kernel(const u32x4* __restrict__ src,
+                                                         u32x4* __restrict__ dst, int64_t n16) {
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n16; i += (int64_t)gridDim.x * 256)
+        dst[i] = src[i];
+}
+
+hipError_t launch_plan_fetch(const void* host_src, void* dst, size_t bytes, hipStream_t stream) {
+    const int64_t n16 = (int64_t)((bytes + 15) / 16);
+    const int64_t blocks = (n16 + 255) / 256 < 64 ? (n16 + 255) / 256 : 64;
+    if (n16 == 0) return hipSuccess;
+    hipLaunchKernelGGL(plan_fetch_kernel, dim3((unsigned)blocks), dim3(256), 0, stream,
+                       static_cast<const u32x4*>(host_src), static_cast<u32x4*>(dst), n16);
+    return hipGetLastError();
 }
 
 template <int DT>

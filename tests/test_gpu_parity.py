@@ -200,6 +200,39 @@ def test_argument_errors():
     torch.cuda.synchronize()
 
 
+def test_reused_plan_sees_new_data():
+    _print_case("reused plan")
+    w = workloads.make(1, device=DEV, scale="small")
+    plan = c3.SignaturePlan(w.replicas, w.chunk_bytes)
+    rec = plan.new_records()
+    ws = plan.new_workspace()
+    plan.run(rec, ws)
+    first = c3.records_numpy(rec)
+    w.replicas[0][0].view(torch.uint8)[100] ^= 0x10     # same pointers, new bytes
+    plan.run(rec, ws, plan_staged=True)
+    torch.cuda.synchronize()
+    second = c3.records_numpy(rec)
+    ref = oracle.signature(_host_reps(w), w.metas, w.chunk_bytes)
+    compare_all_records(second, ref)
+    assert second["sig"][0, 0] != first["sig"][0, 0]
+
+
+def test_plan_larger_than_a_staging_slot():
+    _print_case("large plan")
+    R, T = 64, 600
+    gen = torch.Generator(device=DEV)
+    gen.manual_seed(600)
+    base = torch.randn(T * 16, generator=gen, device=DEV)
+    bufs = [base.clone() for _ in range(R)]
+    bufs[37][16 * 599 + 3] = float("nan")
+    reps = [[b[16 * t: 16 * t + 16] for t in range(T)] for b in bufs]
+    w = workloads.ReplicaWorkload("many_tensors", R, [(workloads.F32, (16,))] * T, 1024, reps)
+    g = _gpu_pipeline(w)
+    ref = oracle.signature(_host_reps(w), w.metas, w.chunk_bytes)
+    compare_all_records(g["records"], ref)
+    assert g["outliers"]["replica"].tolist() == [37] and g["outliers"]["chunk"].tolist() == [599]
+
+
 def test_grid_size_and_tile_size_invariance():
     _print_case("grid and tile invariance")
     w = workloads.make(4, device=DEV, scale="small")
@@ -269,7 +302,7 @@ def test_statistical_closed_forms_on_gpu():
         assert (int(st[0]), int(bm[0])) == (code, want), ln
 
 
-@pytest.mark.parametrize("U", [0, 1, 2047, 2048, 2049, 70000])
+@pytest.mark.parametrize("U", [0, 1, 2047, 2048, 2049, 32768, 32769, 70000])
 def test_localize_matches_oracle(U):
     _print_case("localize", U)
     rng = np.random.default_rng(U)
