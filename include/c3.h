@@ -217,6 +217,22 @@ int c3_signature_ex(const void *const *ptrs, const c3_tensor_meta_t *metas, int 
                     c3_stream_t stream, const c3_launch_opts_t *opts);
 
 /*
+ * c3_tensor_signature -- one signature per (replica, tensor), the paper's own
+ * evidence granularity (Sec. 5.2), from the chunk records of c3_signature:
+ *     fmix64(fmix64(0x4333534947540001 ^ n_chunks) ^ (sum of the tensor's
+ *     chunk signatures mod 2^64)).
+ *
+ *   records  device [R][C] as written by c3_signature (tensor ids must be
+ *            non-decreasing along each replica's row, as c3_signature
+ *            writes them).
+ *   T        number of tensors (>= 1).
+ *   out      device [R][T] u64, 8-byte aligned.  Vote on it with
+ *            c3_consensus(out, C3_EV_U64, T * 8, 8, R, T, C3_EXACT, ...).
+ */
+int c3_tensor_signature(const c3_chunk_record_t *records, int R, int64_t C, int T, uint64_t *out,
+                        c3_stream_t stream);
+
+/*
  * c3_consensus -- the decision of Algorithm 1 for n_units independent units
  * (chunks, or (iteration, group) records), each with R peer values.
  *

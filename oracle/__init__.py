@@ -12,6 +12,8 @@ function cites the paper passage it follows:
                        bytes), read per chunk as C3SIG-1; numerical summary
                        (NaN/Inf counts, absmax, compensated sum and sum of
                        squares of the finite elements).
+* ``tensor_signature`` Sec. 5.2 at the paper's own granularity: one value per
+                       tensor, combined from its chunk signatures.
 * ``vote_exact``       Sec. 5.3, Algorithm 1 Exact branch.
 * ``vote_bytes``       the plain definition of the exact result: equality of
                        raw chunk bytes instead of equality of signatures.
@@ -63,6 +65,7 @@ def _load():
         _lib.c3o_num_chunks.argtypes = [vp, vp, vp, ctypes.c_int, u64]
         _lib.c3o_signature.argtypes = [vp, vp, vp, vp, ctypes.c_int, ctypes.c_int, u64,
                                        vp, vp, vp, vp, vp, vp, vp, vp, vp]
+        _lib.c3o_tensor_signature.argtypes = [vp, vp, ctypes.c_int, i64, ctypes.c_int, vp]
         _lib.c3o_vote_exact.argtypes = [vp, ctypes.c_int, i64, i64, ctypes.c_int, i64,
                                         vp, vp, vp]
         _lib.c3o_vote_bytes.argtypes = [vp, vp, ctypes.c_int, i64, vp, vp, vp]
@@ -195,6 +198,16 @@ def chunk_views(replicas, metas, chunk_bytes: int):
                 row.append(a[k * chunk_bytes:min(nb, (k + 1) * chunk_bytes)])
         views.append(row)
     return views
+
+
+def tensor_signature(rec: dict, T: int) -> np.ndarray:
+    """Per-tensor signatures [R, T] from the chunk records of ``signature``."""
+    sig = np.ascontiguousarray(rec["sig"], np.uint64)
+    tid = np.ascontiguousarray(rec["tensor"], np.uint32)
+    R, C = sig.shape
+    out = np.zeros((R, T), np.uint64)
+    _load().c3o_tensor_signature(_p(sig), _p(tid), R, C, T, _p(out))
+    return out
 
 
 # --------------------------------------------------------------------------

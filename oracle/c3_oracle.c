@@ -40,6 +40,8 @@
  *                           single-bit-flip detection, big-integer
  *                           recomputation on tiny inputs.
  *                           stats: pinned against numpy / math.fsum.
+ *   c3o_tensor_signature    pinned indirectly: its vote equals the byte-equality
+ *                           vote over whole tensors
  *   c3o_vote_exact          pinned (brute force over all label vectors, paper
  *                           cases, Boyer-Moore MJRTY)
  *   c3o_vote_bytes          the definition itself (byte equality)
@@ -325,6 +327,37 @@ int c3o_signature(const uint8_t *const *ptrs, const int32_t *dtypes,
                 tensor_id[o] = (uint32_t)t;
                 chunk_id[o] = (uint32_t)k;
             }
+        }
+    }
+    return 0;
+}
+
+/* ------------------------------------------------------------------ */
+/* Per-tensor signature (Sec. 5.2 evidence at the paper's granularity,  */
+/* one value per tensor): fmix64 of a tagged header carrying the        */
+/* tensor's chunk count, xor the wrapping sum of its chunk signatures,  */
+/* finalized once more.  Each chunk signature already covers dtype,     */
+/* shape, chunk position, length and bytes, so the sum keeps position   */
+/* sensitivity while allowing any reduction order.                      */
+/* sig and tensor_id are [R][C]; out is [R][T].                         */
+/* ------------------------------------------------------------------ */
+#define O_TAG_TENSOR 0x4333534947540001ULL
+
+int c3o_tensor_signature(const uint64_t *sig, const uint32_t *tensor_id, int R, int64_t C, int T,
+                         uint64_t *out)
+{
+    int r, t;
+    int64_t c;
+    for (r = 0; r < R; r++) {
+        for (t = 0; t < T; t++) {
+            uint64_t sum = 0, n = 0;
+            for (c = 0; c < C; c++) {
+                if (tensor_id[(int64_t)r * C + c] == (uint32_t)t) {
+                    sum += sig[(int64_t)r * C + c];
+                    n++;
+                }
+            }
+            out[(int64_t)r * T + t] = c3o_fmix64(c3o_fmix64(O_TAG_TENSOR ^ n) ^ sum);
         }
     }
     return 0;

@@ -7,6 +7,7 @@ the tensors are not on a GPU the functions raise.
 Entry points (same names as the C ABI):
 
 * ``signature(replicas, chunk_bytes)``  -> records [R, C] (64-byte rows)
+* ``tensor_signature(records, T)``       -> per-tensor signatures [R, T]
 * ``consensus(evidence, mode, ...)``     -> status, bitmap, majority index
 * ``localize(status, bitmap, majority_idx, records, R)`` -> lists + counts
 * ``confirm(fp_bitmap, time_bitmap, R, window)`` -> per-rank verdicts
@@ -90,6 +91,8 @@ def lib():
         L.c3_signature.argtypes = [vp, vp, i32, i32, u64, vp, vp, sz, vp]
         L.c3_signature_ex.restype = i32
         L.c3_signature_ex.argtypes = [vp, vp, i32, i32, u64, vp, vp, sz, vp, vp]
+        L.c3_tensor_signature.restype = i32
+        L.c3_tensor_signature.argtypes = [vp, i32, i64, i32, vp, vp]
         L.c3_consensus.restype = i32
         L.c3_consensus.argtypes = [vp, i32, i64, i64, i32, i64, i32, dbl, vp, vp, vp, vp]
         L.c3_localize_workspace_size.restype = sz
@@ -223,6 +226,16 @@ def signature(replicas, chunk_bytes: int, stream=None, grid_blocks: int = 0, til
     ws = plan.new_workspace()
     plan.run(rec, ws, stream=stream, grid_blocks=grid_blocks)
     return rec
+
+
+def tensor_signature(records: torch.Tensor, T: int, stream=None) -> torch.Tensor:
+    """Per-tensor signatures [R, T] (int64 bit patterns) from records [R, C, 64]."""
+    _dev_tensor(records, "records")
+    R, C = records.shape[0], records.shape[1]
+    out = _empty((R, T), torch.int64, records.device)
+    rc = lib().c3_tensor_signature(_ptr(records), R, C, T, _ptr(out), _stream(stream))
+    _check(rc, "c3_tensor_signature")
+    return out
 
 
 def consensus(evidence: torch.Tensor, mode: int = EXACT, *, kind: int = None, R: int = None,

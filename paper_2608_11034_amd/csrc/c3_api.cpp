@@ -266,6 +266,17 @@ int c3_signature(const void* const* ptrs, const c3_tensor_meta_t* metas, int T, 
     return c3_signature_ex(ptrs, metas, T, R, chunk_bytes, records, ws, ws_bytes, stream, nullptr);
 }
 
+int c3_tensor_signature(const c3_chunk_record_t* records, int R, int64_t C, int T, uint64_t* out,
+                        c3_stream_t stream) {
+    if (R < 1 || R > C3_MAX_REPLICAS || C < 0 || T < 1 || C > (int64_t)0x7FFFFFFF * 64)
+        return C3_E_INVAL;
+    if (out == nullptr || (C > 0 && records == nullptr)) return C3_E_INVAL;
+    if (!aligned(records, 8) || !aligned(out, 8)) return C3_E_ALIGN;
+    const hipError_t e = c3::launch_tensor_signature(records, R, C, T, out,
+                                                     reinterpret_cast<hipStream_t>(stream));
+    return e == hipSuccess ? C3_OK : C3_E_HIP;
+}
+
 int c3_consensus(const void* evidence, int evidence_kind, int64_t replica_stride_bytes,
                  int64_t unit_stride_bytes, int R, int64_t n_units, int mode, double kappa,
                  uint8_t* status, uint64_t* bitmap, int32_t* majority_idx, c3_stream_t stream) {

@@ -83,6 +83,9 @@ hipError_t launch_signature(const SigPlan* dplan, const SigPlan& hplan, const Si
 // to device memory with a kernel on `stream`.
 hipError_t launch_plan_fetch(const void* host_src, void* dst, size_t bytes, hipStream_t stream);
 
+hipError_t launch_tensor_signature(const c3_chunk_record_t* records, int R, int64_t C, int T,
+                                   uint64_t* out, hipStream_t stream);
+
 hipError_t launch_consensus(const void* evidence, int kind, int64_t rstride, int64_t ustride, int R,
                             int64_t n_units, int mode, double kappa, uint8_t* status,
                             uint64_t* bitmap, int32_t* majority_idx, hipStream_t stream);

@@ -1,0 +1,121 @@
+"""The C ABI library loads and exports every symbol include/c3.h declares.
+
+Host-side checks only: symbol presence, the chunk plan and workspace sizes,
+status strings and argument validation that returns before any GPU work.
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "c3.h")
+
+c3 = pytest.importorskip("paper_2608_11034_amd.c3")
+
+
+def _declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    names = re.findall(r"^\s*(?:const\s+)?[A-Za-z_][\w\s\*]*?\b(c3_\w+)\s*\(", src, flags=re.M)
+    return sorted(set(names))
+
+
+def test_header_declares_the_boundary():
+    names = _declared_functions()
+    for n in ("c3_signature", "c3_signature_ex", "c3_consensus", "c3_localize", "c3_confirm",
+              "c3_tensor_signature", "c3_num_chunks", "c3_signature_workspace_size",
+              "c3_localize_workspace_size", "c3_confirm_workspace_size", "c3_status_string",
+              "c3_abi_version"):
+        assert n in names, n
+
+
+def test_library_exports_every_declared_symbol():
+    L = c3.lib()
+    for n in _declared_functions():
+        assert hasattr(L, n), f"{n} declared in include/c3.h but not exported"
+    assert L.c3_abi_version() == 1
+
+
+def test_struct_sizes_match_the_header():
+    assert ctypes.sizeof(c3.TensorMeta) == 72
+    assert ctypes.sizeof(c3.LaunchOpts) == 32
+    assert c3.RECORD_DTYPE.itemsize == 64
+    assert c3.OUTLIER_DTYPE.itemsize == 80
+    assert c3.VERDICT_DTYPE.itemsize == 24
+
+
+def _metas(shapes_dtypes):
+    metas = (c3.TensorMeta * len(shapes_dtypes))()
+    for i, (d, shape) in enumerate(shapes_dtypes):
+        metas[i].dtype = d
+        metas[i].ndim = len(shape)
+        for j, n in enumerate(shape):
+            metas[i].shape[j] = n
+    return metas
+
+
+@pytest.mark.parametrize("chunk_bytes", [1024, 3072, 1 << 20])
+def test_chunk_plan_matches_oracle(chunk_bytes):
+    md = [(c3.F32, (1000,)), (c3.BF16, (0,)), (c3.F16, (3, 5, 7)), (c3.RAW, (4097,)), (c3.BF16, ()),
+          (c3.F32, (2048, 1024))]
+    L = c3.lib()
+    got = L.c3_num_chunks(_metas(md), len(md), chunk_bytes)
+    assert got == oracle.num_chunks(md, chunk_bytes)
+
+
+def test_plan_rejects_bad_arguments():
+    L = c3.lib()
+    md = _metas([(c3.F32, (1000,))])
+    assert L.c3_num_chunks(md, 1, 1000) == -1           # not a multiple of 1024
+    assert L.c3_num_chunks(md, 0, 1024) == -1           # no tensors
+    assert L.c3_num_chunks(_metas([(7, (10,))]), 1, 1024) == -1     # unknown dtype
+    assert L.c3_num_chunks(_metas([(c3.F32, (-1,))]), 1, 1024) == -1
+    assert L.c3_signature_workspace_size(md, 1, 1, 1024) == 0        # R = 1
+    assert L.c3_signature_workspace_size(md, 1, 65, 1024) == 0       # R > 64
+    assert L.c3_signature_workspace_size(md, 1, 8, 1024) > 0
+    assert L.c3_signature_workspace_size_ex(md, 1, 8, 4096, 3072) == 0   # tile not a power of 2
+    assert L.c3_signature_workspace_size_ex(md, 1, 8, 4096, 8192) == 0   # tile larger than chunk
+
+
+def test_argument_errors_return_before_gpu_work():
+    L = c3.lib()
+    md = _metas([(c3.F32, (1000,))])
+    ptrs = (ctypes.c_void_p * 2)(16, 32)
+    null = ctypes.c_void_p(0)
+    rec = ctypes.c_void_p(64)
+    ws = ctypes.c_void_p(256)
+    assert L.c3_signature(ptrs, md, 1, 1, 1024, rec, ws, 1 << 20, null) == -1     # R = 1
+    assert L.c3_signature(ptrs, md, 1, 2, 1000, rec, ws, 1 << 20, null) == -1     # chunk
+    assert L.c3_signature(ptrs, md, 1, 2, 1024, rec, null, 1 << 20, null) == -4   # workspace
+    assert L.c3_signature(ptrs, md, 1, 2, 1024, rec, ws, 8, null) == -4           # too small
+    bad = (ctypes.c_void_p * 2)(16, 40)
+    assert L.c3_signature(bad, md, 1, 2, 1024, rec, ws, 1 << 20, null) == -2      # alignment
+    assert L.c3_consensus(ctypes.c_void_p(8), c3.EV_U64, 8, 64, 0, 10, c3.EXACT, 1.0,
+                          ctypes.c_void_p(8), ctypes.c_void_p(8), ctypes.c_void_p(8), null) == -1
+    assert L.c3_consensus(ctypes.c_void_p(8), c3.EV_U64, 8, 64, 4, 10, c3.STATISTICAL, 1.0,
+                          ctypes.c_void_p(8), ctypes.c_void_p(8), ctypes.c_void_p(8), null) == -1
+    assert L.c3_consensus(ctypes.c_void_p(8), c3.EV_F64, 8, 64, 4, 10, c3.STATISTICAL, -1.0,
+                          ctypes.c_void_p(8), ctypes.c_void_p(8), ctypes.c_void_p(8), null) == -1
+    assert L.c3_consensus(ctypes.c_void_p(4), c3.EV_U64, 8, 64, 4, 10, c3.EXACT, 1.0,
+                          ctypes.c_void_p(8), ctypes.c_void_p(8), ctypes.c_void_p(8), null) == -2
+    assert L.c3_consensus(ctypes.c_void_p(8), c3.EV_U64, 8, 64, 4, 0, c3.EXACT, 1.0,
+                          null, null, null, null) == 0                          # nothing to do
+    assert L.c3_localize(null, null, null, null, 4, 10, null, 0, null, 0, ctypes.c_void_p(8),
+                         ctypes.c_void_p(256), 4096, null) == -1
+    assert L.c3_confirm(null, null, 8, 4, 16, 0, ctypes.c_void_p(8), ctypes.c_void_p(256), 4096,
+                        null) == -1                                              # window 0
+    assert L.c3_tensor_signature(null, 8, 10, 0, ctypes.c_void_p(8), null) == -1
+    for code in (0, -1, -2, -3, -4, -5, -99):
+        assert isinstance(L.c3_status_string(code), bytes)
+
+
+def test_binding_has_no_cpu_fallback():
+    import torch
+    x = torch.zeros(1024)
+    with pytest.raises(c3.C3Error):
+        c3.signature([[x], [x]], 1024)

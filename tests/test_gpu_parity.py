@@ -93,6 +93,23 @@ def test_small_config_records_and_lists_match_oracle(k):
     assert set(g["undecided"].tolist()) == want_und
 
 
+@pytest.mark.parametrize("k", [1, 2, 3, 4])
+def test_tensor_signatures_match_oracle(k):
+    _print_case("tensor signatures", k)
+    w = workloads.make(k, device=DEV, scale="small")
+    rec = c3.signature(w.replicas, w.chunk_bytes)
+    T = len(w.metas)
+    ts = c3.tensor_signature(rec, T)
+    st, bm, mj = c3.consensus(ts, c3.EXACT, replica_stride=T * 8, unit_stride=8, n_units=T, R=w.R)
+    torch.cuda.synchronize()
+    ref = oracle.signature(_host_reps(w), w.metas, w.chunk_bytes)
+    want = oracle.tensor_signature(ref, T)
+    assert np.array_equal(ts.cpu().numpy().view(np.uint64), want)
+    ost, obm, omj = oracle.vote_bytes(_host_reps(w))
+    assert np.array_equal(st.cpu().numpy(), ost) and np.array_equal(bm.cpu().numpy().view(np.uint64), obm)
+    assert np.array_equal(mj.cpu().numpy(), omj)
+
+
 def test_three_step_protocol_on_gpu():
     _print_case("three-step protocol")
     w = workloads.make(3, device=DEV, scale="small")

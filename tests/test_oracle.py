@@ -351,6 +351,28 @@ def test_byte_vote_equals_signature_vote_random_splits():
             assert np.array_equal(a, b), trial
 
 
+@pytest.mark.parametrize("k", [1, 2, 3, 4])
+def test_tensor_vote_equals_whole_tensor_byte_vote(k):
+    w = workloads.make(k, device="cpu", scale="small")
+    reps = [[workloads.host_bytes(t) for t in rep] for rep in w.replicas]
+    rec = oracle.signature(reps, w.metas, w.chunk_bytes)
+    ts = oracle.tensor_signature(rec, len(w.metas))
+    s1 = oracle.vote_exact(ts)
+    s2 = oracle.vote_bytes([[a for a in rep] for rep in reps])
+    for a, b in zip(s1, s2):
+        assert np.array_equal(a, b)
+    assert s1[0].max() > 0                                # some tensor is not unanimous
+
+
+def test_tensor_signature_sees_shape_and_chunk_count():
+    d = np.arange(512, dtype=np.float32).view(np.uint8)
+    r1 = oracle.signature([[d], [d.copy()]], [(oracle.F32, (512,))], 1024)
+    r2 = oracle.signature([[d], [d.copy()]], [(oracle.F32, (16, 32))], 1024)
+    r3 = oracle.signature([[d], [d.copy()]], [(oracle.F32, (512,))], 2048)
+    t1, t2, t3 = (oracle.tensor_signature(r, 1) for r in (r1, r2, r3))
+    assert t1[0, 0] == t1[1, 0] and t1[0, 0] != t2[0, 0] and t1[0, 0] != t3[0, 0]
+
+
 # ---------------------------------------------------------------------------
 # statistical vote: closed forms and numpy
 # ---------------------------------------------------------------------------
