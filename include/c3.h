@@ -219,8 +219,8 @@ int c3_signature_ex(const void *const *ptrs, const c3_tensor_meta_t *metas, int 
 /*
  * c3_tensor_signature -- one signature per (replica, tensor), the paper's own
  * evidence granularity (Sec. 5.2), from the chunk records of c3_signature:
- *     fmix64(fmix64(0x4333534947540001 ^ n_chunks) ^ (sum of the tensor's
- *     chunk signatures mod 2^64)).
+ *     fmix64(0x4333534947540001 ^ (sum of the tensor's chunk signatures
+ *     mod 2^64)).
  *
  *   records  device [R][C] as written by c3_signature (tensor ids must be
  *            non-decreasing along each replica's row, as c3_signature

@@ -334,11 +334,11 @@ int c3o_signature(const uint8_t *const *ptrs, const int32_t *dtypes,
 
 /* ------------------------------------------------------------------ */
 /* Per-tensor signature (Sec. 5.2 evidence at the paper's granularity,  */
-/* one value per tensor): fmix64 of a tagged header carrying the        */
-/* tensor's chunk count, xor the wrapping sum of its chunk signatures,  */
-/* finalized once more.  Each chunk signature already covers dtype,     */
-/* shape, chunk position, length and bytes, so the sum keeps position   */
-/* sensitivity while allowing any reduction order.                      */
+/* one value per tensor): the wrapping sum of the tensor's chunk        */
+/* signatures, xor a domain tag, through fmix64.  Each chunk signature  */
+/* already covers dtype, shape, chunk position, length and bytes, so    */
+/* the sum keeps position sensitivity while allowing any reduction      */
+/* order.                                                               */
 /* sig and tensor_id are [R][C]; out is [R][T].                         */
 /* ------------------------------------------------------------------ */
 #define O_TAG_TENSOR 0x4333534947540001ULL
@@ -350,14 +350,11 @@ int c3o_tensor_signature(const uint64_t *sig, const uint32_t *tensor_id, int R, 
     int64_t c;
     for (r = 0; r < R; r++) {
         for (t = 0; t < T; t++) {
-            uint64_t sum = 0, n = 0;
-            for (c = 0; c < C; c++) {
-                if (tensor_id[(int64_t)r * C + c] == (uint32_t)t) {
+            uint64_t sum = 0;
+            for (c = 0; c < C; c++)
+                if (tensor_id[(int64_t)r * C + c] == (uint32_t)t)
                     sum += sig[(int64_t)r * C + c];
-                    n++;
-                }
-            }
-            out[(int64_t)r * T + t] = c3o_fmix64(c3o_fmix64(O_TAG_TENSOR ^ n) ^ sum);
+            out[(int64_t)r * T + t] = c3o_fmix64(O_TAG_TENSOR ^ sum);
         }
     }
     return 0;

@@ -1,7 +1,7 @@
 // Per-tensor signature of C3 for gfx950: one 64-bit value per (replica,
 // tensor), the paper's own evidence granularity (Sec. 5.2), combined from
 // the tensor's chunk signatures:
-//     fmix64(fmix64(tag ^ n_chunks) ^ sum of chunk signatures mod 2^64).
+//     fmix64(tag ^ (sum of the tensor's chunk signatures mod 2^64)).
 // Chunk signatures already cover dtype, shape, chunk position, length and
 // bytes, so an order-free sum keeps position sensitivity.
 //
@@ -40,7 +40,7 @@ __global__ void __launch_bounds__(256) tensor_signature_kernel(
     for (int64_t c = lo + lane; c < hi; c += 64) sum += row[c].sig;
 #pragma unroll
     for (int m = 32; m >= 1; m >>= 1) sum += shfl_xor_u64(sum, m);
-    if (lane == 0) out[wid] = fmix64(fmix64(kTagTensor ^ (uint64_t)(hi - lo)) ^ sum);
+    if (lane == 0) out[wid] = fmix64(kTagTensor ^ sum);
 }
 
 hipError_t launch_tensor_signature(const c3_chunk_record_t* records, int R, int64_t C, int T,

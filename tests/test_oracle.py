@@ -111,12 +111,21 @@ def test_nh_empty_is_zero_and_padding_counts():
     assert oracle.nh(z15) == oracle.nh(z16)
     assert oracle.chunk_signature(z15, oracle.RAW, [15], 0)["sig"] != \
         oracle.chunk_signature(z16, oracle.RAW, [16], 0)["sig"]
+    # same dtype, shape and chunk index, lengths 1033 and 1040 (the chunk plan
+    # of a 1040-byte tensor under two chunk sizes): equal folds, the length
+    # alone must separate the signatures (the evidence covers the bytes)
+    z1033, z1040 = np.zeros(1033, np.uint8), np.zeros(1040, np.uint8)
+    assert oracle.nh(z1033) == oracle.nh(z1040)
+    assert oracle.chunk_signature(z1033, oracle.RAW, [1040], 0)["sig"] != \
+        oracle.chunk_signature(z1040, oracle.RAW, [1040], 0)["sig"]
 
 
 def test_signature_is_sensitive_to_metadata():
     d = np.arange(64, dtype=np.float32).view(np.uint8)
     s = oracle.chunk_signature(d, oracle.F32, [64], 0)["sig"]
     assert s != oracle.chunk_signature(d, oracle.F32, [8, 8], 0)["sig"]   # shape
+    assert oracle.chunk_signature(d, oracle.F32, [8, 8], 0)["sig"] != \
+        oracle.chunk_signature(d, oracle.F32, [4, 16], 0)["sig"]          # dims, same rank
     assert s != oracle.chunk_signature(d, oracle.RAW, [64], 0)["sig"]     # dtype
     assert s != oracle.chunk_signature(d, oracle.F32, [64], 1)["sig"]     # position
     # same bytes, same metadata -> same signature (determinism)
@@ -203,7 +212,7 @@ def _values(dtype, raw_u8):
 
 
 @pytest.mark.parametrize("dtype", [oracle.F32, oracle.BF16, oracle.F16])
-@pytest.mark.parametrize("case", ["normal", "specials", "tiny", "huge", "cancel"])
+@pytest.mark.parametrize("case", ["normal", "specials", "tiny", "huge", "cancel", "absorb"])
 def test_stats_match_numpy_and_fsum(dtype, case):
     rng = np.random.default_rng(hash((dtype, case)) % 2 ** 32)
     n = 5000
@@ -216,6 +225,12 @@ def test_stats_match_numpy_and_fsum(dtype, case):
     elif case == "cancel":
         x = np.concatenate([rng.standard_normal(n // 2) * 1e3, [0.0]])
         x = np.concatenate([x, -x])
+    elif case == "absorb":
+        # a huge value absorbs many small ones in a plain fp64 sum; the exact
+        # sum is the small ones (a compensated sum recovers them)
+        big = 2.0 ** 60 if dtype != oracle.F16 else 2.0 ** 15
+        small = 1.0 if dtype != oracle.F16 else 2.0 ** -10
+        x = np.concatenate([[big], np.full(1000, small), [-big]])
     else:
         x = rng.standard_normal(n)
     if dtype == oracle.F32:
@@ -364,6 +379,20 @@ def test_tensor_vote_equals_whole_tensor_byte_vote(k):
     assert s1[0].max() > 0                                # some tensor is not unanimous
 
 
+def test_tensor_signature_moves_only_with_its_own_bytes():
+    rng = np.random.default_rng(23)
+    metas = [(oracle.F32, (700,)), (oracle.BF16, (1500,)), (oracle.RAW, (2500,))]
+    base = [rng.integers(0, 256, 2800, dtype=np.uint8), rng.integers(0, 256, 3000, dtype=np.uint8),
+            rng.integers(0, 256, 2500, dtype=np.uint8)]
+    ref = oracle.tensor_signature(oracle.signature([base, base], metas, 1024), 3)[0]
+    for t, a in enumerate(base):
+        for pos in list(range(0, a.size, 1024)) + [a.size - 1]:
+            mod = [b.copy() for b in base]
+            mod[t][pos] ^= 0x40
+            got = oracle.tensor_signature(oracle.signature([mod, base], metas, 1024), 3)[0]
+            assert [got[i] != ref[i] for i in range(3)] == [i == t for i in range(3)], (t, pos)
+
+
 def test_tensor_signature_sees_shape_and_chunk_count():
     d = np.arange(512, dtype=np.float32).view(np.uint8)
     r1 = oracle.signature([[d], [d.copy()]], [(oracle.F32, (512,))], 1024)
@@ -486,6 +515,28 @@ def test_confirm_brute_force(T, W):
             consec = bool(np.any(slow[1:] & slow[:-1])) if T > 1 else False
             want = (1 if hit.size else 0) | (2 if div.any() else 0) | (4 if consec else 0)
             assert out["flags"][rank] == want
+
+
+def test_confirm_needs_more_than_half_of_a_window():
+    # reading: a confirmed straggler is flagged in a strict majority of some
+    # window (the strict-majority principle applied over time)
+    T, W = 16, 16
+    for flagged, want in ((8, 0), (9, 1)):
+        tmb = np.zeros((T, 1), np.uint64)
+        tmb[:flagged, 0] = 1
+        out = oracle.confirm(np.zeros((T, 1), np.uint64), tmb, 1, W)
+        assert int(out["flags"][0] & 1) == want and out["max_window"][0] == flagged
+
+
+def test_empty_tensor_is_one_empty_chunk():
+    # reading: an empty tensor keeps one chunk so its dtype and shape are compared
+    assert oracle.num_chunks([(oracle.F32, (0,))], 1024) == 1
+    assert oracle.num_chunks([(oracle.F32, (0,)), (oracle.BF16, (5, 0, 3))], 1024) == 2
+    e = np.zeros(0, np.uint8)
+    r1 = oracle.signature([[e], [e]], [(oracle.F32, (0,))], 1024)
+    r2 = oracle.signature([[e], [e]], [(oracle.F32, (0, 4))], 1024)
+    assert r1["sig"].shape == (2, 1) and r1["sig"][0, 0] != r2["sig"][0, 0]
+    assert r1["n_elems"][0, 0] == 0
 
 
 def test_confirm_rank_layout_matches_paper_peer_groups():
