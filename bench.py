@@ -96,7 +96,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", type=int, default=3, choices=[1, 2, 3, 4])
+    ap.add_argument("--config", type=int, default=3, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--copy-calibration", action="store_true")
@@ -114,6 +114,8 @@ def main():
 
     dev = "cuda:0"
     torch.cuda.set_device(0)
+    if args.config == 5:
+        return bench_timing(args, torch, workloads, c3, dev)
     log(f"[bench] generating config {args.config}")
     w = workloads.make(args.config, device=dev, scale="full")
     torch.cuda.synchronize()
@@ -219,6 +221,98 @@ def main():
         "wall_s_timed": round(wall, 3),
         "ms_per_step_plan_reused": round(ms_staged, 4),
         "value_plan_reused": round(total / (ms_staged * 1e-3) / 1e9, 2),
+    }
+    print(json.dumps(out), flush=True)
+
+
+def _kernel_ms(torch, fn, reps):
+    """Mean duration of a call that enqueues one kernel, by events around it."""
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(reps)]
+    torch.cuda.synchronize()
+    for a, b in evs:
+        a.record()
+        fn()
+        b.record()
+    torch.cuda.synchronize()
+    return sum(a.elapsed_time(b) for a, b in evs) / reps
+
+
+def bench_timing(args, torch, workloads, c3, dev):
+    """Progress/timing consensus: exact vote on fingerprints, statistical vote
+    on step times, temporal confirmation, one step per pass over all records."""
+    log("[bench] generating config 5")
+    w = workloads.make(5, device=dev, scale="full")
+    T, G, R = w.T, w.G, w.R
+    U = T * G
+    total = w.total_bytes
+    out_f = (torch.empty(U, dtype=torch.uint8, device=dev), torch.empty(U, dtype=torch.int64, device=dev),
+             torch.empty(U, dtype=torch.int32, device=dev))
+    out_t = (torch.empty(U, dtype=torch.uint8, device=dev), torch.empty(U, dtype=torch.int64, device=dev),
+             torch.empty(U, dtype=torch.int32, device=dev))
+    ver = torch.empty((R * G, 24), dtype=torch.uint8, device=dev)
+    cws = torch.empty(c3.confirm_workspace_size(R, G, T), dtype=torch.uint8, device=dev)
+
+    def vote_fp():
+        c3.consensus(w.fingerprints, c3.EXACT, out=out_f)
+
+    def vote_time():
+        c3.consensus(w.times, c3.STATISTICAL, out=out_t)
+
+    def confirm():
+        c3.confirm(out_f[1].view(T, G), out_t[1].view(T, G), R, 16, out=ver, workspace=cws)
+
+    def step():
+        vote_fp()
+        vote_time()
+        confirm()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    v = c3.verdicts_numpy(ver)
+    strag = int(((v["flags"] & c3.RANK_STRAGGLER) != 0).sum())
+    proto = int(((v["flags"] & c3.RANK_PROTOCOL) != 0).sum())
+    log(f"[bench] stragglers={strag} protocol_outliers={proto}")
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(args.steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    k_time = _kernel_ms(torch, vote_time, args.steps)
+    k_fp = _kernel_ms(torch, vote_fp, args.steps)
+    k_conf = _kernel_ms(torch, confirm, args.steps)
+    time_bytes = U * R * 4 + U * 13          # read the timings, write status, bitmap, index
+    fp_bytes = U * R * 8 + U * 13
+    conf_bytes = 2 * U * 8 + R * G * 24       # both bitmaps read, one verdict per rank
+    out = {
+        "metric": "timing+fingerprint records GB/s voted+confirmed",
+        "value": round(total / (ms * 1e-3) / 1e9, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u64+f64",
+        "data": "synthetic",
+        "config": {"workload": w.name, "ranks": R * G, "group": R, "iterations": T,
+                   "record_bytes_total": total, "stragglers_found": strag,
+                   "protocol_outliers_found": proto},
+        "kernels": {
+            "statistical_vote": {"ms": round(k_time, 4), "algorithmic_bytes": time_bytes,
+                                 "GBps": round(time_bytes / (k_time * 1e-3) / 1e9, 1)},
+            "exact_vote": {"ms": round(k_fp, 4), "algorithmic_bytes": fp_bytes,
+                           "GBps": round(fp_bytes / (k_fp * 1e-3) / 1e9, 1)},
+            "confirm": {"ms": round(k_conf, 4), "algorithmic_bytes": conf_bytes,
+                        "GBps": round(conf_bytes / (k_conf * 1e-3) / 1e9, 1)},
+        },
     }
     print(json.dumps(out), flush=True)
 

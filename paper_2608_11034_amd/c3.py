@@ -312,15 +312,24 @@ def localize_workspace_size(n_units: int) -> int:
     return int(lib().c3_localize_workspace_size(n_units))
 
 
-def confirm(fp_bitmap, time_bitmap, R: int, window: int = 16, stream=None):
+def confirm_workspace_size(R: int, G: int, T: int) -> int:
+    return int(lib().c3_confirm_workspace_size(R, G, T))
+
+
+def confirm(fp_bitmap, time_bitmap, R: int, window: int = 16, stream=None, out=None,
+            workspace=None):
     """Per-rank verdicts [R * G, 24] (uint8) from [T, G] bitmaps; rank = r * G + g."""
     _dev_tensor(fp_bitmap, "fp_bitmap")
     _dev_tensor(time_bitmap, "time_bitmap")
     T, G = fp_bitmap.shape
     dev = fp_bitmap.device
-    out = _empty((R * G, 24), torch.uint8, dev)
-    ws_bytes = int(lib().c3_confirm_workspace_size(R, G, T))
-    ws = _empty((max(ws_bytes, 256),), torch.uint8, dev)
+    if out is None:
+        out = _empty((R * G, 24), torch.uint8, dev)
+    ws_bytes = confirm_workspace_size(R, G, T)
+    ws = _empty((max(ws_bytes, 256),), torch.uint8, dev) if workspace is None else workspace
+    if ws.numel() < ws_bytes:
+        raise C3Error("confirm workspace too small")
+    ws_bytes = ws.numel()
     rc = lib().c3_confirm(_ptr(fp_bitmap), _ptr(time_bitmap), R, G, T, window, _ptr(out), _ptr(ws),
                           ws_bytes, _stream(stream))
     _check(rc, "c3_confirm")

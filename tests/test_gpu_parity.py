@@ -343,11 +343,13 @@ def test_localize_matches_oracle(U):
         assert und.cpu().numpy()[:n_u].tolist() == loc["undecided"].tolist()
 
 
-@pytest.mark.parametrize("T,W", [(200, 16), (64, 16), (65, 16), (10, 16), (1, 1), (130, 7)])
-def test_confirm_matches_oracle(T, W):
-    _print_case("confirm", T, W)
-    rng = np.random.default_rng(T * 31 + W)
-    R, G = 8, 37
+@pytest.mark.parametrize("R", [3, 8, 13, 20])
+@pytest.mark.parametrize("T,W", [(200, 16), (64, 16), (65, 16), (10, 16), (1, 1), (130, 7),
+                                 (200, 64), (200, 65), (90, 100), (300, 63)])
+def test_confirm_matches_oracle(T, W, R):
+    _print_case("confirm", T, W, R)
+    rng = np.random.default_rng(T * 31 + W + 1000 * R)
+    G = 37
     fpb = (rng.random((T, G, R)) < 0.02)
     tmb = (rng.random((T, G, R)) < np.where((np.arange(R)[None, None, :] + np.arange(G)[None, :, None]) % 11 == 0, 0.7, 0.05))
     pack = lambda b: (b.astype(np.uint64) << np.arange(R, dtype=np.uint64)).sum(-1).astype(np.uint64)
