@@ -244,33 +244,25 @@ hipError_t launch_confirm(const uint64_t* fp_bitmap, const uint64_t* time_bitmap
                           hipStream_t stream) {
     const int64_t n_ranks = (int64_t)R * G;
     if (n_ranks == 0) return hipSuccess;
-    const int64_t n_seg = T > 0 ? (T + kSeg - 1) / kSeg : 1;
     const int64_t Wt = (int64_t)window < T ? (int64_t)window : T;
     SegVerdict* seg = static_cast<SegVerdict*>(ws);
-    if (R <= 16 && Wt <= 64) {
-        const int64_t n_gseg = T > 0 ? (T + kGroupSeg - 1) / kGroupSeg : 1;
-        const int64_t threads1 = G * n_gseg;
-        const int64_t blocks1 = (threads1 + kConfThreads - 1) / kConfThreads;
-        if (blocks1 > 0x7FFFFFFF) return hipErrorInvalidValue;
-        if (R <= 8)
-            hipLaunchKernelGGL((confirm_group_kernel<8, kGroupSeg>), dim3((unsigned)blocks1),
-                               dim3(kConfThreads), 0, stream, fp_bitmap, time_bitmap, R, G, T, Wt,
-                               n_gseg, seg);
-        else
-            hipLaunchKernelGGL((confirm_group_kernel<16, kGroupSeg>), dim3((unsigned)blocks1),
-                               dim3(kConfThreads), 0, stream, fp_bitmap, time_bitmap, R, G, T, Wt,
-                               n_gseg, seg);
-        const int64_t blocks2 = (n_ranks + kConfThreads - 1) / kConfThreads;
-        hipLaunchKernelGGL(confirm_combine_kernel, dim3((unsigned)blocks2), dim3(kConfThreads), 0,
-                           stream, seg, R, G, n_ranks, n_gseg, verdicts);
-        return hipGetLastError();
-    } else {
-        const int64_t threads1 = n_ranks * n_seg;
-        const int64_t blocks1 = (threads1 + kConfThreads - 1) / kConfThreads;
-        if (blocks1 > 0x7FFFFFFF) return hipErrorInvalidValue;
+    const bool by_group = R <= 16 && Wt <= 64;
+    const int64_t seg_len = by_group ? kGroupSeg : kSeg;
+    const int64_t n_seg = T > 0 ? (T + seg_len - 1) / seg_len : 1;
+    const int64_t threads1 = (by_group ? G : n_ranks) * n_seg;
+    const int64_t blocks1 = (threads1 + kConfThreads - 1) / kConfThreads;
+    if (blocks1 > 0x7FFFFFFF) return hipErrorInvalidValue;
+    if (by_group && R <= 8)
+        hipLaunchKernelGGL((confirm_group_kernel<8, kGroupSeg>), dim3((unsigned)blocks1),
+                           dim3(kConfThreads), 0, stream, fp_bitmap, time_bitmap, R, G, T, Wt, n_seg,
+                           seg);
+    else if (by_group)
+        hipLaunchKernelGGL((confirm_group_kernel<16, kGroupSeg>), dim3((unsigned)blocks1),
+                           dim3(kConfThreads), 0, stream, fp_bitmap, time_bitmap, R, G, T, Wt, n_seg,
+                           seg);
+    else
         hipLaunchKernelGGL(confirm_segment_kernel, dim3((unsigned)blocks1), dim3(kConfThreads), 0,
                            stream, fp_bitmap, time_bitmap, R, G, T, Wt, n_seg, seg);
-    }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int64_t blocks2 = (n_ranks + kConfThreads - 1) / kConfThreads;

@@ -301,9 +301,9 @@ __device__ inline void write_record(c3_chunk_record_t* rec, const TensorInfo* ti
 // over that order (gtile[]); this launch covers group positions [gk0, gk1)
 // of every replica.
 template <int DT, int U>
-__global__ void __launch_bounds__(kSigThreads, C3_SIG_WAVES_PER_EU) signature_kernel(const SigPlan* __restrict__ plan,
-                                                                c3_chunk_record_t* __restrict__ records,
-                                                                int gk0, int gk1, int64_t gtiles) {
+__global__ void __launch_bounds__(kSigThreads, C3_SIG_WAVES_PER_EU)
+    signature_kernel(const SigPlan* __restrict__ plan, c3_chunk_record_t* __restrict__ records,
+                     int gk0, int gk1, int64_t gtiles) {
     __shared__ TilePartial lds[kSigThreads / 64];
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
