@@ -309,6 +309,74 @@ int c3_confirm(const uint64_t *fp_bitmap, const uint64_t *time_bitmap, int R, in
                int64_t T, int window, c3_rank_verdict_t *verdicts, void *ws, size_t ws_bytes,
                c3_stream_t stream);
 
+/* ---------------------------------------------------------------------- */
+/* Checkpoint certification (Sec. 8, Algorithm 3).  Host-only calls; no   */
+/* GPU work.  Checkpoint identifiers are caller-chosen non-negative       */
+/* integers (e.g. the training step); -1 means none.                      */
+/* ---------------------------------------------------------------------- */
+
+/* Job-wide outcome of one replay boundary. */
+typedef enum {
+    C3_OUTCOME_OK = 0,        /* every comparison agreed                        */
+    C3_OUTCOME_STRAGGLER = 1, /* a confirmed straggler, numbers agree           */
+    C3_OUTCOME_SDC = 2,       /* some comparison group's evidence disagreed     */
+    C3_OUTCOME_HANG = 3       /* a hang or protocol divergence was reported     */
+} c3_outcome_t;
+
+/* State of Algorithm 3: recipe catalog size K, accepted recipes q in the
+ * current cycle, and the latest, candidate and verified checkpoints. */
+typedef struct {
+    int32_t K;
+    int32_t q;
+    int64_t latest;
+    int64_t candidate;
+    int64_t verified;
+} c3_ckpt_state_t;
+
+/* What one c3_ckpt_save call asks the checkpoint system to do.
+ *   captured      the new in-memory checkpoint becomes latest
+ *   persisted_id  persist this checkpoint as the new candidate (-1: none)
+ *   promoted      the previous candidate became verified
+ *   retrieve      recovery must restart from retrieve_id (-1: no verified
+ *                 checkpoint exists yet) */
+typedef struct {
+    int32_t captured;
+    int32_t promoted;
+    int32_t retrieve;
+    int32_t reserved;
+    int64_t persisted_id;
+    int64_t retrieve_id;
+} c3_ckpt_action_t;
+
+/* Combines one boundary's evidence into an outcome, most severe first:
+ * sdc_units > 0 (attributed or undecided chunks: peers disagree) -> SDC;
+ * hang_signals > 0 (hang or protocol-outlier reports) -> HANG;
+ * stragglers > 0 -> STRAGGLER; else OK.  Negative counts: C3_E_INVAL. */
+int c3_job_outcome(int64_t sdc_units, int64_t hang_signals, int64_t stragglers);
+
+/* Starts a checkpoint cycle for a catalog of K >= 1 recipes (q = 0, no
+ * checkpoints). */
+int c3_ckpt_init(c3_ckpt_state_t *st, int K);
+
+/* CheckpointSave of Algorithm 3 at one replay boundary.
+ *   OK or STRAGGLER: checkpoint_id becomes latest and q advances; when q
+ *     reaches K, q resets, the previous candidate (if any) is promoted to
+ *     verified and checkpoint_id is persisted as the new candidate.
+ *   SDC or HANG: nothing is captured; act->retrieve_id is the checkpoint
+ *     CheckpointRetrieval selects (see c3_ckpt_retrieve).  The state is left
+ *     as it was; after recovery the caller starts a new cycle.
+ * machines_accessible and full_catalog_sdc are the retrieval inputs: whether
+ * every machine's latest shard is reachable, and whether a full-catalog
+ * replay (run by the caller) found SDC. */
+int c3_ckpt_save(c3_ckpt_state_t *st, int outcome, int64_t checkpoint_id, int machines_accessible,
+                 int full_catalog_sdc, c3_ckpt_action_t *act);
+
+/* CheckpointRetrieval of Algorithm 3: SDC or an unreachable machine ->
+ * verified; STRAGGLER -> latest; otherwise latest unless the full-catalog
+ * replay found SDC, then verified. */
+int c3_ckpt_retrieve(const c3_ckpt_state_t *st, int outcome, int machines_accessible,
+                     int full_catalog_sdc, int64_t *checkpoint_id);
+
 /* Static description of a status code. */
 const char *c3_status_string(int code);
 

@@ -32,6 +32,7 @@ EV_U64, EV_U32, EV_F32, EV_F64 = 0, 1, 2, 3
 AGREE, ATTRIBUTED, INCONCLUSIVE = 0, 1, 2
 KAPPA_DEFAULT = 3.5 / 0.6745
 RANK_STRAGGLER, RANK_PROTOCOL, RANK_CONSEC2 = 1, 2, 4
+OUTCOME_OK, OUTCOME_STRAGGLER, OUTCOME_SDC, OUTCOME_HANG = 0, 1, 2, 3
 OPT_PLAN_STAGED = 1
 
 RECORD_DTYPE = np.dtype([("sig", "<u8"), ("n_elems", "<u8"), ("nan_count", "<u4"),
@@ -50,6 +51,17 @@ _TORCH_CODE = {torch.float32: F32, torch.bfloat16: BF16, torch.float16: F16, tor
 
 class C3Error(RuntimeError):
     pass
+
+
+class CkptState(ctypes.Structure):
+    _fields_ = [("K", ctypes.c_int32), ("q", ctypes.c_int32), ("latest", ctypes.c_int64),
+                ("candidate", ctypes.c_int64), ("verified", ctypes.c_int64)]
+
+
+class CkptAction(ctypes.Structure):
+    _fields_ = [("captured", ctypes.c_int32), ("promoted", ctypes.c_int32),
+                ("retrieve", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("persisted_id", ctypes.c_int64), ("retrieve_id", ctypes.c_int64)]
 
 
 class TensorMeta(ctypes.Structure):
@@ -103,6 +115,14 @@ def lib():
         L.c3_confirm_workspace_size.argtypes = [i32, i64, i64]
         L.c3_confirm.restype = i32
         L.c3_confirm.argtypes = [vp, vp, i32, i64, i64, i32, vp, vp, sz, vp]
+        L.c3_job_outcome.restype = i32
+        L.c3_job_outcome.argtypes = [i64, i64, i64]
+        L.c3_ckpt_init.restype = i32
+        L.c3_ckpt_init.argtypes = [vp, i32]
+        L.c3_ckpt_save.restype = i32
+        L.c3_ckpt_save.argtypes = [vp, i32, i64, i32, i32, vp]
+        L.c3_ckpt_retrieve.restype = i32
+        L.c3_ckpt_retrieve.argtypes = [vp, i32, i32, i32, vp]
         if L.c3_abi_version() != 1:
             raise C3Error("libc3.so ABI version mismatch")
         _lib = L
@@ -334,6 +354,39 @@ def confirm(fp_bitmap, time_bitmap, R: int, window: int = 16, stream=None, out=N
                           ws_bytes, _stream(stream))
     _check(rc, "c3_confirm")
     return out
+
+
+# ---------------------------------------------------------------------------
+# checkpoint certification (host-only)
+# ---------------------------------------------------------------------------
+def job_outcome(sdc_units: int, hang_signals: int, stragglers: int) -> int:
+    rc = lib().c3_job_outcome(sdc_units, hang_signals, stragglers)
+    if rc < 0:
+        _check(rc, "c3_job_outcome")
+    return rc
+
+
+class CheckpointGate:
+    """Algorithm 3 state (latest / candidate / verified) held by libc3."""
+
+    def __init__(self, K: int):
+        self.state = CkptState()
+        _check(lib().c3_ckpt_init(ctypes.byref(self.state), K), "c3_ckpt_init")
+
+    def save(self, outcome: int, checkpoint_id: int, machines_accessible=True,
+             full_catalog_sdc=False) -> CkptAction:
+        act = CkptAction()
+        _check(lib().c3_ckpt_save(ctypes.byref(self.state), outcome, checkpoint_id,
+                                  int(bool(machines_accessible)), int(bool(full_catalog_sdc)),
+                                  ctypes.byref(act)), "c3_ckpt_save")
+        return act
+
+    def retrieve(self, outcome: int, machines_accessible=True, full_catalog_sdc=False) -> int:
+        out = ctypes.c_int64(-1)
+        _check(lib().c3_ckpt_retrieve(ctypes.byref(self.state), outcome,
+                                      int(bool(machines_accessible)), int(bool(full_catalog_sdc)),
+                                      ctypes.byref(out)), "c3_ckpt_retrieve")
+        return out.value
 
 
 # ---------------------------------------------------------------------------

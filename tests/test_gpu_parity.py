@@ -448,3 +448,30 @@ def test_full_config5_timing_consensus():
              for r in np.nonzero(ver["flags"] & c3.RANK_PROTOCOL)[0]}
     assert strag == set(w.stragglers)
     assert proto == w.divergent
+
+
+# ---------------------------------------------------------------------------
+# checkpoint certification fed by GPU verdicts (Sec. 8, Algorithm 3)
+# ---------------------------------------------------------------------------
+def test_checkpoint_gate_fed_by_gpu_verdicts():
+    """The paper's two-recipe scenario driven by real verdicts on Adam-shard
+    state: steps 1-4 clean, SDC at step 5 -> recover the step-2 checkpoint."""
+    _print_case("checkpoint gate")
+    w = workloads.make(4, device=DEV, scale="small")
+    clean_src = next(r for r in range(w.R) if all(f.replica != r for f in w.faults))
+    clean = [[t.clone() for t in w.replicas[clean_src]] for _ in range(w.R)]
+    gate = c3.CheckpointGate(K=2)
+    for step in range(1, 6):
+        reps = w.replicas if step == 5 else clean
+        rec = c3.signature(reps, w.chunk_bytes)
+        st, bm, mj = c3.consensus(rec, c3.EXACT)
+        _, _, cnt = c3.localize(st, bm, mj, rec)
+        torch.cuda.synchronize()
+        counts = cnt.cpu().tolist()
+        outcome = c3.job_outcome(counts[1] + counts[2], 0, 0)
+        act = gate.save(outcome, step)
+        if step < 5:
+            assert outcome == c3.OUTCOME_OK and act.captured == 1
+        else:
+            assert outcome == c3.OUTCOME_SDC and act.retrieve == 1 and act.retrieve_id == 2
+    assert (gate.state.candidate, gate.state.verified) == (4, 2)
