@@ -22,6 +22,9 @@ function cites the paper passage it follows:
                        which peers disagree.
 * ``confirm``          Sec. 10 protocol: stragglers are confirmed across
                        repeated timing rounds.
+* ``adamw``            Sec. 9 optimizer boundary: the replayed AdamW step on a
+                       rotating slice and the check built on it (module
+                       ``oracle.adamw``).
 
 Parity: the hash bits of C3SIG-1 are not fixed by the paper ("parity
 unpinned" for the exact bit pattern); they are pinned indirectly (see the

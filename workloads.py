@@ -15,7 +15,7 @@ is a deterministic three-block Transformer and names no public dataset):
   k))``, applied through integer views so NaN payloads survive;
 * replicas: R copies of one clean replica, faults applied afterwards.
 
-Configs (k = 1..5), ``scale="full"`` is the benchmark size, ``"small"`` keeps
+Configs (k = 1..6), ``scale="full"`` is the benchmark size, ``"small"`` keeps
 the structure (dtypes, fault kinds, ragged tails, several chunks per tensor)
 at a size the oracle finishes in well under a second.
 """
@@ -288,7 +288,70 @@ def config5(device="cuda", scale="full") -> TimingWorkload:
                           else "ranks512_g8_iters64", R, G, T, fp, tau, divergent, stragglers)
 
 
-CONFIGS = {1: config1, 2: config2, 3: config3, 4: config4, 5: config5}
+# --------------------------------------------------------------------------
+# config 6: optimizer-boundary check, R=8 data-parallel replicas of an AdamW
+# state of 134,217,728 fp32 parameters (param ~N(0,0.02), grad ~N(0,1e-3),
+# exp_avg ~N(0,1e-4), exp_avg_sq ~|N(0,1e-6)|); 64K-element rotating slices;
+# lr 3e-4, betas (0.9, 0.95), eps 1e-8, weight decay 0.1, step 1000.
+# Faults, all in slice s1 except the last: an exponent-bit flip in one
+# replica's gradient, a sign flip in another replica's exp_avg_sq (the
+# replayed square root turns it into NaN) and, in slice s2, a low mantissa
+# bit of a third replica's parameter.  The small scale keeps a ragged last
+# slice.
+# --------------------------------------------------------------------------
+@dataclass
+class OptimizerWorkload:
+    name: str
+    R: int
+    numel: int
+    state: list                      # [4][R] device fp32 tensors: param, grad, exp_avg, exp_avg_sq
+    hparams: dict
+    faults: list
+    fault_slices: list               # slice indices (k) that hold the planted faults
+    slice_elems: int = 65536
+
+    @property
+    def bytes_per_check(self) -> int:
+        """Bytes the replay reads and writes per check (16 in, 12 out per element)."""
+        return self.R * min(self.slice_elems, self.numel) * 28
+
+
+OPT_TENSORS = ("param", "grad", "exp_avg", "exp_avg_sq")
+
+
+def config6(device="cuda", scale="full") -> OptimizerWorkload:
+    S = 65536
+    numel = 134_217_728 if scale == "full" else 3 * S + 1000
+    R = 8
+    rng = np.random.Generator(np.random.PCG64(106))
+    metas = [(F32, (numel,))] * 4
+    clean = _clean_replica(metas, [0.02, 1e-3, 1e-4, 1e-6], 6, device,
+                           absolute=[False, False, False, True])
+    reps = _replicate(clean, R)
+    n_slices = -(-numel // S)
+    s1 = int(rng.integers(0, n_slices))
+    s2 = (s1 + 1 + int(rng.integers(0, n_slices - 1))) % n_slices
+    ra, rb, rc = (int(x) for x in rng.choice(R, size=3, replace=False))
+
+    def elem_in(slice_k):
+        lo = slice_k * S
+        return lo + int(rng.integers(0, min(S, numel - lo)))
+
+    e1, e2, e3 = elem_in(s1), elem_in(s1), elem_in(s2)
+    b1 = int(rng.integers(23, 30))
+    _xor_bit(reps[ra][1], F32, e1, b1)
+    _xor_bit(reps[rb][3], F32, e2, 31)
+    b3 = int(rng.integers(0, 4))
+    _xor_bit(reps[rc][0], F32, e3, b3)
+    faults = [Fault(ra, 1, 4 * e1, 4, f"bitflip{b1}"), Fault(rb, 3, 4 * e2, 4, "signflip"),
+              Fault(rc, 0, 4 * e3, 4, f"bitflip{b3}")]
+    state = [[reps[r][t] for r in range(R)] for t in range(4)]
+    hp = dict(lr=3e-4, betas=(0.9, 0.95), eps=1e-8, weight_decay=0.1, step=1000)
+    name = "r8_adamw_134m_fp32_slice64kel" if scale == "full" else "r8_adamw_small_ragged"
+    return OptimizerWorkload(name, R, numel, state, hp, faults, [s1, s1, s2], S)
+
+
+CONFIGS = {1: config1, 2: config2, 3: config3, 4: config4, 5: config5, 6: config6}
 
 
 def make(k: int, device="cuda", scale="full"):
