@@ -12,8 +12,10 @@ Prints ONE JSON line on stdout (progress goes to stderr):
   cpu_baseline  the CPU oracle (single thread) on a bounded sample
 
 Flags: --gpus N (only 1: the path runs on one GPU), --steps K, --warmup W,
---no-cpu-baseline, --copy-calibration (adds a 1 GiB device copy used to scale
-rocprofv3 FETCH_SIZE / WRITE_SIZE counters).
+--config 1..6 (5: timing consensus of 32,768 ranks; 6: optimizer-boundary
+check on 8 replicas of a 134M-parameter AdamW state), --no-cpu-baseline,
+--copy-calibration (adds a 1 GiB device copy used to scale rocprofv3
+FETCH_SIZE / WRITE_SIZE counters).
 """
 import argparse
 import hashlib
@@ -96,7 +98,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", type=int, default=3, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--config", type=int, default=3, choices=[1, 2, 3, 4, 5, 6])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--copy-calibration", action="store_true")
@@ -116,6 +118,8 @@ def main():
     torch.cuda.set_device(0)
     if args.config == 5:
         return bench_timing(args, torch, workloads, c3, dev)
+    if args.config == 6:
+        return bench_optimizer(args, torch, workloads, c3, dev)
     log(f"[bench] generating config {args.config}")
     w = workloads.make(args.config, device=dev, scale="full")
     torch.cuda.synchronize()
@@ -315,6 +319,130 @@ def bench_timing(args, torch, workloads, c3, dev):
         },
     }
     print(json.dumps(out), flush=True)
+
+
+def bench_optimizer(args, torch, workloads, c3, dev):
+    """Optimizer-boundary check: one step = one scheduled check on the next
+    rotating 64K-element slice (AdamW replay on R replicas, signatures of the
+    4 input and 3 output slices per replica, exact vote, localize)."""
+    log("[bench] generating config 6")
+    w = workloads.make(6, device=dev, scale="full")
+    torch.cuda.synchronize()
+    chk = c3.OptimizerBoundaryCheck(*w.state, slice_elems=w.slice_elems, tile_bytes=args.tile)
+    tile = chk.st.tile_bytes or 65536
+    hp = c3.adamw_hparams(w.hparams["lr"], w.hparams["betas"], w.hparams["eps"],
+                          w.hparams["weight_decay"], w.hparams["step"])
+    n_slices = -(-w.numel // w.slice_elems)
+    k0 = w.fault_slices[0]
+    found = {}
+    for k in sorted(set(w.fault_slices)):
+        res = chk.run(k, hp)
+        torch.cuda.synchronize()
+        o = c3.outliers_numpy(res[4], res[6])
+        found[k] = sorted({(chk.UNITS[int(u)], int(r)) for u, r in zip(o["chunk"], o["replica"])})
+    log(f"[bench] outliers at the faulted slices: {found}")
+    for i in range(args.warmup):
+        chk.run(k0 + i, hp)
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    e0.record()
+    for i in range(args.steps):
+        chk.run(k0 + i, hp)
+    e1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = e0.elapsed_time(e1) / args.steps
+    n = w.slice_elems
+    R = w.R
+    # Per-kernel durations in the check's launch configuration (slice k0, row
+    # stride S, the same signature tile).  These kernels last microseconds:
+    # a per-launch event pair would add several microseconds of its own, and
+    # the host needs about as long to enqueue one call as the GPU to run it.
+    # So a 4 GiB device copy is queued first, a run of back-to-back launches
+    # is enqueued behind it between one pair of HIP events on the launch
+    # stream, and the interval is divided by the run's length.
+    head_src = torch.empty(1 << 32, dtype=torch.uint8, device=dev)
+    head_dst = torch.empty_like(head_src)
+    batch = 64
+
+    def batch_ms(fn):
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        fn(0, None, None)
+        torch.cuda.synchronize()
+        head_dst.copy_(head_src)
+        a.record()
+        for i in range(batch):
+            fn(i, a if i == 0 else None, b if i == batch - 1 else None)
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / batch
+
+    k_adamw = batch_ms(lambda i, x, y: c3.adamw_slice(*w.state, k0 * n, n, hp, out=chk.updated,
+                                                       out_stride=n, _tables=chk.tables))
+    views = [[x[r][k0 * n:(k0 + 1) * n] for x in w.state] + [chk.updated[r, j] for j in range(3)]
+             for r in range(R)]
+    plan = c3.SignaturePlan(views, n * 4, tile)
+    rec = plan.new_records()
+    sws = plan.new_workspace()
+    plan.run(rec, sws)
+    # the staged plan is reused (no fetch kernel); the library records the
+    # first event right before the first signature kernel and the last one
+    # after the last partial combine
+    k_sig = batch_ms(lambda i, a, b: plan.run(rec, sws, plan_staged=True, ev_begin=a, ev_end=b))
+    del head_src, head_dst
+    adamw_bytes = R * n * 28                 # read p, g, m, v; write p', m', v'
+    sig_bytes = R * 7 * n * 4                # the seven signed slices per replica
+    kern = {"adamw_slice_vec4_kernel": (k_adamw, adamw_bytes),
+            "signature_kernel+finalize_kernel": (k_sig, sig_bytes)}
+    dom = max(kern, key=lambda k: kern[k][0])
+    d_ms, d_bytes = kern[dom]
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("[bench] CPU oracle baseline on a bounded sample of checks")
+        from oracle import adamw as oadamw
+        n_host = 8
+        host = [[t[(k0 % n_slices) * n:(k0 % n_slices + n_host) * n].cpu().numpy() for t in x]
+                for x in w.state]
+        t1 = time.perf_counter()
+        done = 0
+        while done < 1 or time.perf_counter() - t1 < args.cpu_budget:
+            oadamw.boundary_check(host, done % n_host, w.hparams, n)
+            done += 1
+        dt = time.perf_counter() - t1
+        cpu = {"value": round(done / dt, 3), "unit": "checks/s", "cores": 1, "kind": "oracle",
+               "sample": f"{done} checks over {n_host} resident 64K-element slices of all {R} "
+                         f"replicas (AdamW replay, 56 slice signatures, vote, localize), {dt:.1f} s"}
+    res = {
+        "metric": "optimizer-boundary checks/s (64K-element AdamW slice, 8 replicas)",
+        "value": round(1e3 / ms, 1),
+        "unit": "checks/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32+u64",
+        "data": "synthetic",
+        "config": {"workload": w.name, "R": R, "params_per_replica": w.numel,
+                   "slice_elems": n, "slices": n_slices, "tile_bytes": tile,
+                   "outliers_at_fault_slices": {str(k): v for k, v in found.items()}},
+        "roofline": {"bound": "hbm", "achieved": round(d_bytes / (d_ms * 1e-3) / 1e9, 2),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(d_bytes / (d_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                     "traffic": None, "kernel": dom, "kernel_ms": round(d_ms, 4),
+                     "algorithmic_bytes_per_launch": d_bytes},
+        "kernels": {k: {"ms": round(v[0], 4), "algorithmic_bytes": v[1],
+                        "GBps": round(v[1] / (v[0] * 1e-3) / 1e9, 1)} for k, v in kern.items()},
+        "cpu_baseline": cpu,
+        "wall_s_timed": round(wall, 3),
+    }
+    print(json.dumps(res), flush=True)
 
 
 if __name__ == "__main__":

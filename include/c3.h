@@ -150,8 +150,10 @@ typedef struct {
 
 /* Optional launch controls for c3_signature_ex.
  *   ev_kernel_begin / ev_kernel_end: if non-NULL, recorded on the stream
- *     immediately before and after the streaming signature kernel (for
- *     timing that kernel alone).
+ *     immediately before the streaming signature kernel (after the plan is
+ *     staged) and after the pass ends: the streaming kernel, plus the combine
+ *     of tile partials when a chunk spans several tiles.  Either may be
+ *     given alone, so a run of calls can be timed as a whole.
  *   grid_blocks: workgroups of the streaming kernel; 0 chooses one per tile.
  *     Results do not depend on it.
  *   flags: C3_OPT_PLAN_STAGED -- the workspace still holds the plan that a
@@ -231,6 +233,98 @@ int c3_signature_ex(const void *const *ptrs, const c3_tensor_meta_t *metas, int 
  */
 int c3_tensor_signature(const c3_chunk_record_t *records, int R, int64_t C, int T, uint64_t *out,
                         c3_stream_t stream);
+
+/* AdamW hyperparameters of the optimizer step being replayed (fp64 on the
+ * host; step t >= 1 is the step count after this update). */
+typedef struct {
+    double lr, beta1, beta2, eps, weight_decay;
+    int64_t step;
+} c3_adamw_hparams_t;
+
+/*
+ * c3_adamw_slice -- optimizer-boundary replay (Sec. 9, optimizer boundary;
+ * Sec. 6.2, optimizer recipe): one AdamW step (decoupled weight decay,
+ * PyTorch's single-tensor operation order, amsgrad off) re-applied to
+ * elements [offset, offset + n) of R replicas' fp32 tensors, which are only
+ * read.  Per element, each fp32 operation rounded once, no contraction:
+ *     p1 = p * fp32(1 - lr wd)
+ *     m1 = m + w (g - m)  if |w| < 1/2,  else  g - (g - m)(1 - w);  w = fp32(1 - b1)
+ *     v1 = v * fp32(b2) + (fp32(1 - b2) g) g
+ *     p2 = p1 + fp32(-lr / (1 - b1^t)) * (m1 / (sqrt(v1) / fp32(sqrt(1 - b2^t)) + fp32(eps)))
+ * with the scalar factors formed in fp64.  A NaN result is stored as the
+ * quiet NaN 0x7FC00000.
+ *
+ *   param, grad, exp_avg, exp_avg_sq  host arrays [R] of device pointers to
+ *            each replica's tensor of `numel` fp32 elements (4-byte aligned;
+ *            16-byte aligned bases with offset, n and out_stride multiples
+ *            of 4 take the 128-bit path).
+ *   out      device fp32, caller-owned: row (replica r, j) at out + (3 r + j)
+ *            out_stride holds the n updated values of the parameter (j = 0),
+ *            first moment (1) and second moment (2) -- three tensors of n
+ *            elements per replica for c3_signature.  out_stride >= n; 0
+ *            means n (packed [R][3][n]).
+ *   R in 1..64; 0 <= offset, offset + n <= numel; lr >= 0, 0 <= b1, b2 < 1,
+ *   eps > 0, wd >= 0, step >= 1, else C3_E_INVAL; misaligned pointers
+ *   C3_E_ALIGN; a failed launch C3_E_HIP.  n = 0 does nothing.  Asynchronous
+ *   on `stream`.
+ */
+int c3_adamw_slice(const float *const *param, const float *const *grad,
+                   const float *const *exp_avg, const float *const *exp_avg_sq, int R,
+                   int64_t numel, int64_t offset, int64_t n, const c3_adamw_hparams_t *hp,
+                   float *out, int64_t out_stride, c3_stream_t stream);
+
+/* One optimizer-boundary check over R replicas' AdamW state (Sec. 9). */
+typedef struct {
+    const float *const *param;       /* host arrays [R] of device pointers, */
+    const float *const *grad;        /* numel fp32 elements each, 16-byte   */
+    const float *const *exp_avg;     /* aligned                              */
+    const float *const *exp_avg_sq;
+    int32_t R;                       /* 2..64 */
+    int32_t reserved;
+    int64_t numel;
+    int64_t slice_elems;             /* S: multiple of 256 (65536 in Sec. 9) */
+    uint64_t tile_bytes;             /* signature tile: a power of two >= 1024,
+                                        lowered until it divides 4 S; 0 = 64 KiB */
+} c3_optimizer_state_t;
+
+/* Device outputs of c3_optimizer_check, all caller-owned.  Unit u of the
+ * vote is tensor u of each replica: 0 param, 1 grad, 2 exp_avg, 3
+ * exp_avg_sq (the input slices), 4 param, 5 exp_avg, 6 exp_avg_sq (the
+ * replayed updates). */
+typedef struct {
+    float *updated;                  /* [R][3][S], 16-byte aligned */
+    c3_chunk_record_t *records;      /* [R][7] */
+    uint8_t *status;                 /* [7] */
+    uint64_t *bitmap;                /* [7] */
+    int32_t *majority_idx;           /* [7] */
+    c3_outlier_t *outliers;          /* [7 R] */
+    int64_t *undecided;              /* [7] */
+    int64_t *counts;                 /* [3], as c3_localize */
+} c3_optimizer_check_out_t;
+
+/* Workspace bytes for c3_optimizer_check with this state; 0 if invalid. */
+size_t c3_optimizer_check_workspace_size(const c3_optimizer_state_t *st);
+
+/*
+ * c3_optimizer_check -- scheduled check k at the optimizer boundary (Sec. 9;
+ * Sec. 6.2 optimizer recipe; exact C3 of Algorithm 1 on the slices).  Takes
+ * the rotating slice [off, off + n): off = (k mod ceil(numel / S)) S, n =
+ * min(S, numel - off).  Enqueues on `stream`:
+ *   1. c3_adamw_slice on that slice into `updated` (row stride S);
+ *   2. c3_signature of seven tensors of n fp32 elements per replica (the
+ *      four input slices, read in place, and the three updated slices),
+ *      one chunk each;
+ *   3. c3_consensus (exact) over the seven units; 4. c3_localize.
+ * Healthy data-parallel replicas agree on all seven units; an outlier on an
+ * input unit names replicas whose state diverged before the step, one on an
+ * output unit only names replicas whose replayed update differs.
+ * k >= 0; errors as the four calls (C3_E_INVAL, C3_E_ALIGN, C3_E_WORKSPACE,
+ * C3_E_HIP); workspace 256-byte aligned, at least
+ * c3_optimizer_check_workspace_size bytes, not used concurrently.
+ */
+int c3_optimizer_check(const c3_optimizer_state_t *st, int64_t k, const c3_adamw_hparams_t *hp,
+                       const c3_optimizer_check_out_t *out, void *ws, size_t ws_bytes,
+                       c3_stream_t stream);
 
 /*
  * c3_consensus -- the decision of Algorithm 1 for n_units independent units

@@ -1,9 +1,10 @@
 """Builds libc3.so, the gfx950 HIP library behind include/c3.h.
 
 hipcc compiles every source of csrc/ for gfx950 only:
-  -O3, no floating-point contraction (the statistical vote must round like
-  its plain definition; sums use explicit fma), fp32/fp16 denormals kept,
-  packed-fp32 instructions disabled.
+  -O3, no floating-point contraction (the statistical vote and the AdamW
+  replay must round like their plain definitions; sums use explicit fma),
+  correctly rounded fp32 division and square root, fp32/fp16 denormals
+  kept, packed-fp32 instructions disabled.
 """
 import glob
 import os
@@ -17,6 +18,7 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
     "-ffp-contract=off", "-fno-gpu-flush-denormals-to-zero",
+    "-fhip-fp32-correctly-rounded-divide-sqrt",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wall", "-Wno-unused-function",
 ]

@@ -11,6 +11,10 @@ Entry points (same names as the C ABI):
 * ``consensus(evidence, mode, ...)``     -> status, bitmap, majority index
 * ``localize(status, bitmap, majority_idx, records, R)`` -> lists + counts
 * ``confirm(fp_bitmap, time_bitmap, R, window)`` -> per-rank verdicts
+* ``adamw_slice(params, grads, exp_avgs, exp_avg_sqs, offset, n, hp)``
+                                         -> updated slices [R, 3, n] fp32
+* ``OptimizerBoundaryCheck``             replay + signature + vote + localize
+                                         on a rotating optimizer-state slice
 
 Records, outliers and verdicts are returned as raw device tensors
 (``torch.uint8`` rows); ``records_numpy`` & co. view host copies as numpy
@@ -68,6 +72,25 @@ class TensorMeta(ctypes.Structure):
     _fields_ = [("dtype", ctypes.c_int32), ("ndim", ctypes.c_int32), ("shape", ctypes.c_int64 * 8)]
 
 
+class AdamwHparams(ctypes.Structure):
+    _fields_ = [("lr", ctypes.c_double), ("beta1", ctypes.c_double), ("beta2", ctypes.c_double),
+                ("eps", ctypes.c_double), ("weight_decay", ctypes.c_double),
+                ("step", ctypes.c_int64)]
+
+
+class OptimizerState(ctypes.Structure):
+    _fields_ = [("param", ctypes.c_void_p), ("grad", ctypes.c_void_p), ("exp_avg", ctypes.c_void_p),
+                ("exp_avg_sq", ctypes.c_void_p), ("R", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("numel", ctypes.c_int64), ("slice_elems", ctypes.c_int64),
+                ("tile_bytes", ctypes.c_uint64)]
+
+
+class OptimizerCheckOut(ctypes.Structure):
+    _fields_ = [(name, ctypes.c_void_p) for name in ("updated", "records", "status", "bitmap",
+                                                      "majority_idx", "outliers", "undecided",
+                                                      "counts")]
+
+
 class LaunchOpts(ctypes.Structure):
     _fields_ = [("ev_kernel_begin", ctypes.c_void_p), ("ev_kernel_end", ctypes.c_void_p),
                 ("grid_blocks", ctypes.c_int32), ("flags", ctypes.c_int32),
@@ -115,6 +138,12 @@ def lib():
         L.c3_confirm_workspace_size.argtypes = [i32, i64, i64]
         L.c3_confirm.restype = i32
         L.c3_confirm.argtypes = [vp, vp, i32, i64, i64, i32, vp, vp, sz, vp]
+        L.c3_adamw_slice.restype = i32
+        L.c3_adamw_slice.argtypes = [vp, vp, vp, vp, i32, i64, i64, i64, vp, vp, i64, vp]
+        L.c3_optimizer_check_workspace_size.restype = sz
+        L.c3_optimizer_check_workspace_size.argtypes = [vp]
+        L.c3_optimizer_check.restype = i32
+        L.c3_optimizer_check.argtypes = [vp, i64, vp, vp, vp, sz, vp]
         L.c3_job_outcome.restype = i32
         L.c3_job_outcome.argtypes = [i64, i64, i64]
         L.c3_ckpt_init.restype = i32
@@ -354,6 +383,126 @@ def confirm(fp_bitmap, time_bitmap, R: int, window: int = 16, stream=None, out=N
                           ws_bytes, _stream(stream))
     _check(rc, "c3_confirm")
     return out
+
+
+# ---------------------------------------------------------------------------
+# optimizer-boundary check
+# ---------------------------------------------------------------------------
+SLICE_ELEMS = 65536
+
+
+def adamw_hparams(lr=1e-3, betas=(0.9, 0.999), eps=1e-8, weight_decay=1e-2, step=1) -> AdamwHparams:
+    return AdamwHparams(float(lr), float(betas[0]), float(betas[1]), float(eps),
+                        float(weight_decay), int(step))
+
+
+def _ptr_table(tensors, name, numel, dev):
+    for i, t in enumerate(tensors):
+        _dev_tensor(t, f"{name}[{i}]")
+        if t.dtype != torch.float32 or t.numel() != numel or t.device != dev:
+            raise C3Error(f"{name}[{i}] must be fp32 with {numel} elements on {dev}")
+    return (ctypes.c_void_p * len(tensors))(*[t.data_ptr() for t in tensors])
+
+
+def adamw_slice(params, grads, exp_avgs, exp_avg_sqs, offset: int, n: int, hp: AdamwHparams,
+                out=None, out_stride: int = 0, stream=None, _tables=None):
+    """Replay one AdamW step on elements [offset, offset + n) of R replicas'
+    fp32 tensors.  Returns out: row (r, j) at element (3 r + j) * stride,
+    stride = out_stride or n (by default a new [R, 3, n] tensor) holding the
+    updated param (j = 0), exp_avg (1) and exp_avg_sq (2)."""
+    R = len(params)
+    if not (len(grads) == len(exp_avgs) == len(exp_avg_sqs) == R) or R < 1:
+        raise C3Error("params, grads, exp_avgs and exp_avg_sqs need one tensor per replica")
+    numel, dev = params[0].numel(), params[0].device
+    tables = _tables or [_ptr_table(x, nm, numel, dev) for x, nm in
+                         ((params, "params"), (grads, "grads"), (exp_avgs, "exp_avgs"),
+                          (exp_avg_sqs, "exp_avg_sqs"))]
+    stride = out_stride or n
+    if out is None:
+        out = _empty((R, 3, stride), torch.float32, dev)
+    elif out.dtype != torch.float32 or out.numel() < (3 * R - 1) * stride + n:
+        raise C3Error("out must be fp32 with room for R * 3 rows of the stride")
+    rc = lib().c3_adamw_slice(tables[0], tables[1], tables[2], tables[3], R, numel, int(offset),
+                              int(n), ctypes.byref(hp), _ptr(_dev_tensor(out, "out")), int(out_stride),
+                              _stream(stream))
+    _check(rc, "c3_adamw_slice")
+    return out
+
+
+def optimizer_slice(k: int, numel: int, slice_elems: int = SLICE_ELEMS):
+    """(offset, n) of rotating check k: the (k mod S)-th window of slice_elems
+    elements among the S = ceil(numel / slice_elems) windows of the tensor."""
+    if numel <= 0:
+        return 0, 0
+    n_slices = -(-numel // slice_elems)
+    off = (k % n_slices) * slice_elems
+    return off, min(slice_elems, numel - off)
+
+
+class OptimizerBoundaryCheck:
+    """Scheduled optimizer-boundary checks over R replicas' AdamW state
+    (c3_optimizer_check).
+
+    Check k takes the rotating slice ``optimizer_slice(k, numel)`` and signs
+    seven tensors per replica: the four pre-update input slices (param, grad,
+    exp_avg, exp_avg_sq; whether the replicas start from identical values)
+    and the three updated slices of the replayed step (param, exp_avg,
+    exp_avg_sq).  Each is one chunk, so unit u of the vote is tensor u in
+    ``UNITS`` order.  Exact C3 votes per unit and localize lists the outliers.
+    All buffers are allocated here once; ``run`` enqueues one check.
+    """
+
+    UNITS = ("param", "grad", "exp_avg", "exp_avg_sq", "param_new", "exp_avg_new",
+             "exp_avg_sq_new")
+
+    def __init__(self, params, grads, exp_avgs, exp_avg_sqs, slice_elems: int = SLICE_ELEMS,
+                 tile_bytes: int = 0):
+        self.R = len(params)
+        if self.R < 2:
+            raise C3Error("need at least two replicas")
+        self.numel, self.device = params[0].numel(), params[0].device
+        self.state = (list(params), list(grads), list(exp_avgs), list(exp_avg_sqs))
+        self.tables = [_ptr_table(x, nm, self.numel, self.device) for x, nm in
+                       zip(self.state, ("params", "grads", "exp_avgs", "exp_avg_sqs"))]
+        self.slice_elems = int(slice_elems)
+        self.st = OptimizerState(ctypes.cast(self.tables[0], ctypes.c_void_p),
+                                 ctypes.cast(self.tables[1], ctypes.c_void_p),
+                                 ctypes.cast(self.tables[2], ctypes.c_void_p),
+                                 ctypes.cast(self.tables[3], ctypes.c_void_p),
+                                 self.R, 0, self.numel, self.slice_elems, int(tile_bytes))
+        ws_bytes = int(lib().c3_optimizer_check_workspace_size(ctypes.byref(self.st)))
+        if ws_bytes == 0:
+            raise C3Error("invalid optimizer-check configuration")
+        R, dev, U = self.R, self.device, len(self.UNITS)
+        self.updated = _empty((R, 3, self.slice_elems), torch.float32, dev)
+        self.records = _empty((R, U, 64), torch.uint8, dev)
+        self.status = _empty((U,), torch.uint8, dev)
+        self.bitmap = _empty((U,), torch.int64, dev)
+        self.majority = _empty((U,), torch.int32, dev)
+        self.outliers = _empty((U * R, 80), torch.uint8, dev)
+        self.undecided = _empty((U,), torch.int64, dev)
+        self.counts = _empty((3,), torch.int64, dev)
+        self.workspace = _empty((ws_bytes,), torch.uint8, dev)
+        self.out = OptimizerCheckOut(*[t.data_ptr() for t in (
+            self.updated, self.records, self.status, self.bitmap, self.majority, self.outliers,
+            self.undecided, self.counts)])
+
+    def slice(self, k: int):
+        return optimizer_slice(k, self.numel, self.slice_elems)
+
+    def updated_slices(self, k: int):
+        """[R, 3, n] view of the replayed values of check k (after it ran)."""
+        return self.updated[:, :, : self.slice(k)[1]]
+
+    def run(self, k: int, hp: AdamwHparams, stream=None):
+        """Enqueue check k; returns (records, status, bitmap, majority, outliers,
+        undecided, counts), device tensors owned by this object."""
+        rc = lib().c3_optimizer_check(ctypes.byref(self.st), int(k), ctypes.byref(hp),
+                                      ctypes.byref(self.out), _ptr(self.workspace),
+                                      self.workspace.numel(), _stream(stream))
+        _check(rc, "c3_optimizer_check")
+        return (self.records, self.status, self.bitmap, self.majority, self.outliers,
+                self.undecided, self.counts)
 
 
 # ---------------------------------------------------------------------------

@@ -2,6 +2,7 @@
 // tile plan, descriptor staging into the caller's workspace, and launches.
 // Nothing here computes evidence or verdicts; all of that runs in the HIP
 // kernels.
+#include <math.h>
 #include <string.h>
 
 #include <mutex>
@@ -253,10 +254,13 @@ int c3_signature_ex(const void* const* ptrs, const c3_tensor_meta_t* metas, int 
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     const bool staged = opts != nullptr && (opts->flags & C3_OPT_PLAN_STAGED) != 0;
     if (!staged && stage_to_device(ws, buf.data(), buf.size(), s) != hipSuccess) return C3_E_HIP;
-    const hipError_t e = c3::launch_signature(
+    // the end event follows the whole pass: the streaming kernels and, for
+    // tiled plans, the combine of their partials
+    hipError_t e = c3::launch_signature(
         static_cast<const SigPlan*>(ws), p.h, p.groups, records, opts ? opts->grid_blocks : 0, s,
-        opts ? reinterpret_cast<hipEvent_t>(opts->ev_kernel_begin) : nullptr,
-        opts ? reinterpret_cast<hipEvent_t>(opts->ev_kernel_end) : nullptr);
+        opts ? reinterpret_cast<hipEvent_t>(opts->ev_kernel_begin) : nullptr, nullptr);
+    if (e == hipSuccess && opts != nullptr && opts->ev_kernel_end != nullptr)
+        e = hipEventRecord(reinterpret_cast<hipEvent_t>(opts->ev_kernel_end), s);
     return e == hipSuccess ? C3_OK : C3_E_HIP;
 }
 
@@ -274,6 +278,57 @@ int c3_tensor_signature(const c3_chunk_record_t* records, int R, int64_t C, int 
     if (!aligned(records, 8) || !aligned(out, 8)) return C3_E_ALIGN;
     const hipError_t e = c3::launch_tensor_signature(records, R, C, T, out,
                                                      reinterpret_cast<hipStream_t>(stream));
+    return e == hipSuccess ? C3_OK : C3_E_HIP;
+}
+
+int c3_adamw_slice(const float* const* param, const float* const* grad, const float* const* exp_avg,
+                   const float* const* exp_avg_sq, int R, int64_t numel, int64_t offset, int64_t n,
+                   const c3_adamw_hparams_t* hp, float* out, int64_t out_stride,
+                   c3_stream_t stream) {
+    if (param == nullptr || grad == nullptr || exp_avg == nullptr || exp_avg_sq == nullptr ||
+        hp == nullptr || R < 1 || R > C3_MAX_REPLICAS || numel < 0 || offset < 0 || n < 0 ||
+        offset > numel || n > numel - offset || hp->step < 1)
+        return C3_E_INVAL;
+    if (out_stride == 0) out_stride = n;
+    if (out_stride < n) return C3_E_INVAL;
+    if (!(hp->lr >= 0.0) || !(hp->beta1 >= 0.0 && hp->beta1 < 1.0) ||
+        !(hp->beta2 >= 0.0 && hp->beta2 < 1.0) || !(hp->eps > 0.0) || !(hp->weight_decay >= 0.0))
+        return C3_E_INVAL;
+    if (n == 0) return C3_OK;
+    if (out == nullptr) return C3_E_INVAL;
+    if (!aligned(out, 4)) return C3_E_ALIGN;
+    c3::AdamwPtrs ptrs;
+    memset(&ptrs, 0, sizeof(ptrs));
+    for (int r = 0; r < R; ++r) {
+        if (param[r] == nullptr || grad[r] == nullptr || exp_avg[r] == nullptr ||
+            exp_avg_sq[r] == nullptr)
+            return C3_E_INVAL;
+        if (!aligned(param[r], 4) || !aligned(grad[r], 4) || !aligned(exp_avg[r], 4) ||
+            !aligned(exp_avg_sq[r], 4))
+            return C3_E_ALIGN;
+        ptrs.param[r] = param[r];
+        ptrs.grad[r] = grad[r];
+        ptrs.exp_avg[r] = exp_avg[r];
+        ptrs.exp_avg_sq[r] = exp_avg_sq[r];
+    }
+    // scalar factors in fp64, rounded once to fp32
+    c3::AdamwConst c;
+    const double t = (double)hp->step;
+    c.decay = (float)(1.0 - hp->lr * hp->weight_decay);
+    c.w = (float)(1.0 - hp->beta1);
+    c.one_minus_w = 1.0f - c.w;
+    c.lerp_small = fabsf(c.w) < 0.5f;
+    c.beta2 = (float)hp->beta2;
+    c.c2 = (float)(1.0 - hp->beta2);
+    c.s2 = (float)sqrt(1.0 - pow(hp->beta2, t));
+    c.eps = (float)hp->eps;
+    c.neg_step = -(float)(hp->lr / (1.0 - pow(hp->beta1, t)));
+    bool vec4 = offset % 4 == 0 && n % 4 == 0 && out_stride % 4 == 0 && aligned(out, 16);
+    for (int r = 0; r < R && vec4; ++r)
+        vec4 = aligned(param[r], 16) && aligned(grad[r], 16) && aligned(exp_avg[r], 16) &&
+               aligned(exp_avg_sq[r], 16);
+    const hipError_t e = c3::launch_adamw_slice(ptrs, c, R, vec4, offset, n, out, out_stride,
+                                                reinterpret_cast<hipStream_t>(stream));
     return e == hipSuccess ? C3_OK : C3_E_HIP;
 }
 
@@ -329,6 +384,97 @@ int c3_localize(const uint8_t* status, const uint64_t* bitmap, const int32_t* ma
                                              outliers, out_cap, undecided, und_cap, counts, ws,
                                              reinterpret_cast<hipStream_t>(stream));
     return e == hipSuccess ? C3_OK : C3_E_HIP;
+}
+
+// ---------------------------------------------------------------------------
+// Optimizer-boundary check: replay, signatures of the seven slices per
+// replica, exact vote and localization, enqueued by one host call.
+// ---------------------------------------------------------------------------
+static int optimizer_plan(const c3_optimizer_state_t* st, int64_t n, c3_tensor_meta_t metas[7],
+                          uint64_t* chunk, uint64_t* tile) {
+    if (st == nullptr || st->R < 2 || st->R > C3_MAX_REPLICAS || st->numel < 1 ||
+        st->slice_elems < 256 || st->slice_elems % 256 != 0 || st->slice_elems > (1ll << 30))
+        return C3_E_INVAL;
+    *chunk = (uint64_t)st->slice_elems * 4;
+    uint64_t t = st->tile_bytes ? st->tile_bytes : 65536;
+    if (t < 1024 || (t & (t - 1)) != 0) return C3_E_INVAL;
+    while (*chunk % t != 0) t /= 2;  // chunk is a multiple of 1024
+    *tile = t;
+    for (int i = 0; i < 7; ++i) {
+        memset(&metas[i], 0, sizeof(metas[i]));
+        metas[i].dtype = C3_F32;
+        metas[i].ndim = 1;
+        metas[i].shape[0] = n;
+    }
+    return C3_OK;
+}
+
+static uint64_t optimizer_sig_ws(const c3_optimizer_state_t* st, const c3_tensor_meta_t* metas,
+                                 uint64_t chunk, uint64_t tile) {
+    Plan p;
+    if (make_plan(metas, 7, st->R, chunk, tile, p) != C3_OK) return 0;
+    return p.h.total_bytes;
+}
+
+size_t c3_optimizer_check_workspace_size(const c3_optimizer_state_t* st) {
+    c3_tensor_meta_t metas[7];
+    uint64_t chunk, tile;
+    if (optimizer_plan(st, st ? st->slice_elems : 0, metas, &chunk, &tile) != C3_OK) return 0;
+    const uint64_t sig = optimizer_sig_ws(st, metas, chunk, tile);
+    if (sig == 0) return 0;
+    return (size_t)(align_up(sig, 256) + align_up(c3::localize_ws_bytes(7), 256));
+}
+
+int c3_optimizer_check(const c3_optimizer_state_t* st, int64_t k, const c3_adamw_hparams_t* hp,
+                       const c3_optimizer_check_out_t* out, void* ws, size_t ws_bytes,
+                       c3_stream_t stream) {
+    c3_tensor_meta_t metas[7];
+    uint64_t chunk, tile;
+    int rc = optimizer_plan(st, 0, metas, &chunk, &tile);
+    if (rc != C3_OK) return rc;
+    if (k < 0 || out == nullptr || out->updated == nullptr || out->records == nullptr ||
+        out->status == nullptr || out->bitmap == nullptr || out->majority_idx == nullptr ||
+        out->outliers == nullptr || out->undecided == nullptr || out->counts == nullptr)
+        return C3_E_INVAL;
+    if (st->param == nullptr || st->grad == nullptr || st->exp_avg == nullptr ||
+        st->exp_avg_sq == nullptr)
+        return C3_E_INVAL;
+    const size_t need = c3_optimizer_check_workspace_size(st);
+    if (need == 0) return C3_E_INVAL;
+    if (ws == nullptr || !aligned(ws, 256) || ws_bytes < need) return C3_E_WORKSPACE;
+    if (!aligned(out->updated, 16)) return C3_E_ALIGN;
+    const int R = st->R;
+    const int64_t S = st->slice_elems;
+    const int64_t n_slices = (st->numel + S - 1) / S;
+    const int64_t off = (k % n_slices) * S;
+    const int64_t n = st->numel - off < S ? st->numel - off : S;
+    for (int i = 0; i < 7; ++i) metas[i].shape[0] = n;
+    // the replay writes row (r, j) at updated + (3 r + j) S
+    rc = c3_adamw_slice(st->param, st->grad, st->exp_avg, st->exp_avg_sq, R, st->numel, off, n,
+                        hp, out->updated, S, stream);
+    if (rc != C3_OK) return rc;
+    const void* ptrs[7 * C3_MAX_REPLICAS];
+    for (int r = 0; r < R; ++r) {
+        const void** row = ptrs + 7 * r;
+        row[0] = st->param[r] + off;
+        row[1] = st->grad[r] + off;
+        row[2] = st->exp_avg[r] + off;
+        row[3] = st->exp_avg_sq[r] + off;
+        for (int j = 0; j < 3; ++j) row[4 + j] = out->updated + (3 * (int64_t)r + j) * S;
+    }
+    c3_launch_opts_t opts;
+    memset(&opts, 0, sizeof(opts));
+    opts.tile_bytes = tile;
+    const uint64_t sig_ws = align_up(optimizer_sig_ws(st, metas, chunk, tile), 256);
+    rc = c3_signature_ex(ptrs, metas, 7, R, chunk, out->records, ws, sig_ws, stream, &opts);
+    if (rc != C3_OK) return rc;
+    rc = c3_consensus(out->records, C3_EV_U64, 7 * (int64_t)sizeof(c3_chunk_record_t),
+                      (int64_t)sizeof(c3_chunk_record_t), R, 7, C3_EXACT, C3_KAPPA_DEFAULT,
+                      out->status, out->bitmap, out->majority_idx, stream);
+    if (rc != C3_OK) return rc;
+    return c3_localize(out->status, out->bitmap, out->majority_idx, out->records, R, 7,
+                       out->outliers, 7 * (int64_t)R, out->undecided, 7, out->counts,
+                       static_cast<unsigned char*>(ws) + sig_ws, ws_bytes - sig_ws, stream);
 }
 
 size_t c3_confirm_workspace_size(int R, int64_t G, int64_t T) {

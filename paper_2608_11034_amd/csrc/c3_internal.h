@@ -24,6 +24,21 @@ hipError_t launch_plan_fetch(const void* host_src, void* dst, size_t bytes, hipS
 hipError_t launch_tensor_signature(const c3_chunk_record_t* records, int R, int64_t C, int T,
                                    uint64_t* out, hipStream_t stream);
 
+// Optimizer-boundary replay: per-replica tensor bases and fp32 factors.
+struct AdamwPtrs {
+    const float* param[C3_MAX_REPLICAS];
+    const float* grad[C3_MAX_REPLICAS];
+    const float* exp_avg[C3_MAX_REPLICAS];
+    const float* exp_avg_sq[C3_MAX_REPLICAS];
+};
+struct AdamwConst {
+    float decay, w, one_minus_w, beta2, c2, s2, eps, neg_step;
+    int lerp_small;
+};
+hipError_t launch_adamw_slice(const AdamwPtrs& ptrs, const AdamwConst& c, int R, bool vec4,
+                              int64_t offset, int64_t n, float* out, int64_t stride,
+                              hipStream_t stream);
+
 hipError_t launch_consensus(const void* evidence, int kind, int64_t rstride, int64_t ustride, int R,
                             int64_t n_units, int mode, double kappa, uint8_t* status,
                             uint64_t* bitmap, int32_t* majority_idx, hipStream_t stream);

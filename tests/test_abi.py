@@ -30,7 +30,8 @@ def test_header_declares_the_boundary():
     for n in ("c3_signature", "c3_signature_ex", "c3_consensus", "c3_localize", "c3_confirm",
               "c3_tensor_signature", "c3_num_chunks", "c3_signature_workspace_size",
               "c3_localize_workspace_size", "c3_confirm_workspace_size", "c3_status_string",
-              "c3_abi_version"):
+              "c3_abi_version", "c3_adamw_slice", "c3_optimizer_check",
+              "c3_optimizer_check_workspace_size"):
         assert n in names, n
 
 
@@ -44,6 +45,9 @@ def test_library_exports_every_declared_symbol():
 def test_struct_sizes_match_the_header():
     assert ctypes.sizeof(c3.TensorMeta) == 72
     assert ctypes.sizeof(c3.LaunchOpts) == 32
+    assert ctypes.sizeof(c3.AdamwHparams) == 48
+    assert ctypes.sizeof(c3.OptimizerState) == 64
+    assert ctypes.sizeof(c3.OptimizerCheckOut) == 64
     assert c3.RECORD_DTYPE.itemsize == 64
     assert c3.OUTLIER_DTYPE.itemsize == 80
     assert c3.VERDICT_DTYPE.itemsize == 24
@@ -119,3 +123,70 @@ def test_binding_has_no_cpu_fallback():
     x = torch.zeros(1024)
     with pytest.raises(c3.C3Error):
         c3.signature([[x], [x]], 1024)
+
+
+def test_adamw_slice_argument_errors_return_before_gpu_work():
+    L = c3.lib()
+    ptrs = (ctypes.c_void_p * 2)(256, 512)
+    out = ctypes.c_void_p(1024)
+    null = ctypes.c_void_p(0)
+    hp = c3.adamw_hparams(lr=1e-3, betas=(0.9, 0.999), eps=1e-8, weight_decay=0.1, step=1)
+
+    def call(R=2, numel=1000, off=0, n=100, h=hp, o=out, p=ptrs, stride=0):
+        return L.c3_adamw_slice(p, p, p, p, R, numel, off, n, ctypes.byref(h), o, stride, null)
+
+    assert call(R=0) == -1 and call(R=65) == -1
+    assert call(off=950, n=100) == -1                    # past the end
+    assert call(off=-1) == -1 and call(n=-1) == -1
+    assert call(o=null) == -1
+    assert call(o=ctypes.c_void_p(1026)) == -2           # fp32 alignment
+    assert call(p=(ctypes.c_void_p * 2)(256, 514)) == -2
+    assert call(p=(ctypes.c_void_p * 2)(256, 0)) == -1
+    for bad in (dict(step=0), dict(betas=(1.0, 0.9)), dict(betas=(0.9, -0.1)), dict(eps=0.0),
+                dict(lr=-1.0), dict(weight_decay=-0.5)):
+        kw = dict(lr=1e-3, betas=(0.9, 0.999), eps=1e-8, weight_decay=0.1, step=1)
+        kw.update(bad)
+        assert call(h=c3.adamw_hparams(**kw)) == -1, bad
+    assert call(stride=99) == -1                         # rows overlap
+    assert call(n=0, o=null) == 0                        # nothing to do
+
+
+def test_optimizer_check_argument_errors_return_before_gpu_work():
+    L = c3.lib()
+    ptrs = (ctypes.c_void_p * 2)(256, 512)
+    null = ctypes.c_void_p(0)
+    hp = c3.adamw_hparams(step=1)
+    addr = [4096 * (i + 1) for i in range(8)]
+    out = c3.OptimizerCheckOut(*addr)
+
+    def state(R=2, numel=10000, S=1024, tile=0):
+        p = ctypes.cast(ptrs, ctypes.c_void_p)
+        return c3.OptimizerState(p, p, p, p, R, 0, numel, S, tile)
+
+    def ws_size(**kw):
+        return L.c3_optimizer_check_workspace_size(ctypes.byref(state(**kw)))
+
+    assert ws_size() > 0 and ws_size(S=768) > 0 and ws_size(tile=1 << 20) > 0
+    assert ws_size(R=1) == 0 and ws_size(R=65) == 0 and ws_size(S=100) == 0
+    assert ws_size(numel=0) == 0 and ws_size(tile=3000) == 0 and ws_size(tile=512) == 0
+    assert L.c3_optimizer_check_workspace_size(null) == 0
+    need = ws_size()
+
+    def call(st=None, k=0, o=out, ws=ctypes.c_void_p(1 << 20), nbytes=need):
+        st = st or state()
+        return L.c3_optimizer_check(ctypes.byref(st), k, ctypes.byref(hp), ctypes.byref(o), ws,
+                                    nbytes, null)
+
+    assert call(k=-1) == -1
+    assert call(st=state(R=1)) == -1
+    assert call(o=c3.OptimizerCheckOut(*(addr[:7] + [0]))) == -1
+    assert call(ws=null) == -4 and call(nbytes=need - 1) == -4
+    assert call(ws=ctypes.c_void_p((1 << 20) + 8)) == -4
+    assert call(o=c3.OptimizerCheckOut(*([4104] + addr[1:]))) == -2
+
+
+@pytest.mark.parametrize("numel,S", [(10, 4), (12, 4), (3, 4), (65536 * 3 + 1000, 65536), (0, 8)])
+def test_rotating_slice_matches_oracle(numel, S):
+    from oracle import adamw
+    for k in range(-(-numel // S) * 2 + 1):
+        assert c3.optimizer_slice(k, numel, S) == adamw.slice_bounds(k, numel, S)
