@@ -12,8 +12,9 @@ Prints ONE JSON line on stdout (progress goes to stderr):
   cpu_baseline  the CPU oracle (single thread) on a bounded sample
 
 Flags: --gpus N (only 1: the path runs on one GPU), --steps K, --warmup W,
---config 1..6 (5: timing consensus of 32,768 ranks; 6: optimizer-boundary
-check on 8 replicas of a 134M-parameter AdamW state), --no-cpu-baseline,
+--config 1..7 (5: timing consensus of 32,768 ranks; 6: optimizer-boundary
+check on 8 replicas of a 134M-parameter AdamW state; 7: out-of-band hang
+localization, CPU only), --no-cpu-baseline,
 --copy-calibration (adds a 1 GiB device copy used to scale rocprofv3
 FETCH_SIZE / WRITE_SIZE counters).
 """
@@ -98,7 +99,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", type=int, default=3, choices=[1, 2, 3, 4, 5, 6])
+    ap.add_argument("--config", type=int, default=3, choices=[1, 2, 3, 4, 5, 6, 7])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--copy-calibration", action="store_true")
@@ -109,6 +110,9 @@ def main():
         print("bench.py: this hot path runs on one GPU (R replicas resident in one GPU's HBM); "
               "--gpus N > 1 is not supported", file=sys.stderr)
         sys.exit(2)
+
+    if args.config == 7:
+        return bench_hang(args)
 
     import torch
     import workloads
@@ -443,6 +447,52 @@ def bench_optimizer(args, torch, workloads, c3, dev):
         "wall_s_timed": round(wall, 3),
     }
     print(json.dumps(res), flush=True)
+
+
+def bench_hang(args):
+    """Out-of-band hang localization on the host CPU: the native cost of the
+    progress path, and the time from a frozen rank to every observer's
+    verdict in a 4-rank Gloo drill (one step per drill)."""
+    import statistics
+    import subprocess
+
+    from paper_2608_11034_amd import build as pbuild
+    from paper_2608_11034_amd import oob_drill
+    log("[bench] native progress path")
+    native = json.loads(subprocess.run([pbuild.OOB_BENCH, "2000000"], check=True,
+                                       capture_output=True, text=True, timeout=300).stdout)
+    native.pop("sink", None)
+    silence = 0.5
+    runs = max(1, min(args.steps, 5))
+    lat, classes = [], []
+    for i in range(runs):
+        log(f"[bench] freeze drill {i + 1}/{runs}")
+        res = oob_drill.run_drill("freeze", world=4, at_step=5, silence_s=silence)
+        lat += list(res["latency_s"].values())
+        classes += [(v or {}).get("class") for v in res["verdicts"].values()]
+    over = [t - silence for t in lat]
+    out = {
+        "metric": "hang localization latency beyond the silence threshold (frozen rank -> verdict)",
+        "value": round(statistics.median(over), 4) if over else None,
+        "unit": "s",
+        "n_gpus": 0,
+        "steps": runs,
+        "warmup": 0,
+        "ms_per_step": None,
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u64",
+        "data": "synthetic",
+        "config": {"workload": "gloo_drill_4ranks_freeze", "ranks": 4, "silence_threshold_s": silence,
+                   "poll_s": 0.005, "verdicts": classes},
+        "latency_s": {"min": round(min(lat), 4), "median": round(statistics.median(lat), 4),
+                      "max": round(max(lat), 4)} if lat else None,
+        "native": native,
+        "roofline": None,
+        "cpu_baseline": None,
+    }
+    print(json.dumps(out), flush=True)
 
 
 if __name__ == "__main__":
