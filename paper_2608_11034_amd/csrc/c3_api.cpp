@@ -442,7 +442,25 @@ int c3_optimizer_check(const c3_optimizer_state_t* st, int64_t k, const c3_adamw
     const size_t need = c3_optimizer_check_workspace_size(st);
     if (need == 0) return C3_E_INVAL;
     if (ws == nullptr || !aligned(ws, 256) || ws_bytes < need) return C3_E_WORKSPACE;
-    if (!aligned(out->updated, 16)) return C3_E_ALIGN;
+    if (!aligned(out->updated, 16) || !aligned(out->records, 8) || !aligned(out->bitmap, 8) ||
+        !aligned(out->majority_idx, 4) || !aligned(out->outliers, 8) ||
+        !aligned(out->undecided, 8) || !aligned(out->counts, 8))
+        return C3_E_ALIGN;
+    // every check that a later step would make is made here, before the
+    // first launch: the slices are signed in place, so the bases must meet
+    // the signature's 16-byte alignment
+    for (int r = 0; r < st->R; ++r) {
+        if (st->param[r] == nullptr || st->grad[r] == nullptr || st->exp_avg[r] == nullptr ||
+            st->exp_avg_sq[r] == nullptr)
+            return C3_E_INVAL;
+        if (!aligned(st->param[r], 16) || !aligned(st->grad[r], 16) ||
+            !aligned(st->exp_avg[r], 16) || !aligned(st->exp_avg_sq[r], 16))
+            return C3_E_ALIGN;
+    }
+    if (hp == nullptr || hp->step < 1 || !(hp->lr >= 0.0) ||
+        !(hp->beta1 >= 0.0 && hp->beta1 < 1.0) || !(hp->beta2 >= 0.0 && hp->beta2 < 1.0) ||
+        !(hp->eps > 0.0) || !(hp->weight_decay >= 0.0))
+        return C3_E_INVAL;
     const int R = st->R;
     const int64_t S = st->slice_elems;
     const int64_t n_slices = (st->numel + S - 1) / S;

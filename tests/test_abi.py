@@ -183,6 +183,19 @@ def test_optimizer_check_argument_errors_return_before_gpu_work():
     assert call(ws=null) == -4 and call(nbytes=need - 1) == -4
     assert call(ws=ctypes.c_void_p((1 << 20) + 8)) == -4
     assert call(o=c3.OptimizerCheckOut(*([4104] + addr[1:]))) == -2
+    assert call(o=c3.OptimizerCheckOut(*(addr[:1] + [4100] + addr[2:]))) == -2     # records
+    # state bases must be 16-byte aligned and the hyperparameters valid before
+    # anything is launched
+    bad = (ctypes.c_void_p * 2)(256, 520)
+    p = ctypes.cast(bad, ctypes.c_void_p)
+    assert call(st=c3.OptimizerState(p, p, p, p, 2, 0, 10000, 1024, 0)) == -2
+    zero = (ctypes.c_void_p * 2)(256, 0)
+    z = ctypes.cast(zero, ctypes.c_void_p)
+    assert call(st=c3.OptimizerState(z, z, z, z, 2, 0, 10000, 1024, 0)) == -1
+    for kw in (dict(step=0), dict(betas=(1.0, 0.9)), dict(eps=0.0), dict(lr=-1.0)):
+        h = c3.adamw_hparams(**kw)
+        assert L.c3_optimizer_check(ctypes.byref(state()), 0, ctypes.byref(h), ctypes.byref(out),
+                                    ctypes.c_void_p(1 << 20), need, null) == -1, kw
 
 
 @pytest.mark.parametrize("numel,S", [(10, 4), (12, 4), (3, 4), (65536 * 3 + 1000, 65536), (0, 8)])
