@@ -11,7 +11,10 @@ Prints ONE JSON line on stdout (progress goes to stderr):
              with HIP events the library records around that kernel
   cpu_baseline  the CPU oracle (single thread) on a bounded sample
 
-Flags: --gpus N (only 1: the path runs on one GPU), --steps K, --warmup W,
+Flags: --gpus N (only 1: the path runs on one GPU), --steps K, --warmup W
+(default: untimed steps until at least 0.25 s and 10 steps have run, which
+takes the GPU past the clock and power transient of its first launches;
+the JSON reports the count), 
 --config 1..7 (5: timing consensus of 32,768 ranks; 6: optimizer-boundary
 check on 8 replicas of a 134M-parameter AdamW state; 7: out-of-band hang
 localization, CPU only), --no-cpu-baseline,
@@ -98,7 +101,7 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=None)
     ap.add_argument("--config", type=int, default=3, choices=[1, 2, 3, 4, 5, 6, 7])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
@@ -157,10 +160,8 @@ def main():
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / args.steps, time.perf_counter() - t0
 
-    log(f"[bench] warmup {args.warmup}")
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
+    args.warmup = warm_up(torch, step, args.warmup)
+    log(f"[bench] warmup {args.warmup} steps")
     counts = cnt.cpu().tolist()
     log(f"[bench] outliers={counts[0]} undecided={counts[1]} attributed_chunks={counts[2]}")
 
@@ -233,6 +234,22 @@ def main():
     print(json.dumps(out), flush=True)
 
 
+def warm_up(torch, step, warmup, min_s=0.25, min_steps=10):
+    """Runs `warmup` untimed steps, or with None steps until min_s seconds and
+    min_steps steps have passed; returns the count."""
+    if warmup is not None:
+        for _ in range(warmup):
+            step()
+        torch.cuda.synchronize()
+        return warmup
+    n, t0 = 0, time.perf_counter()
+    while n < min_steps or time.perf_counter() - t0 < min_s:
+        step()
+        torch.cuda.synchronize()
+        n += 1
+    return n
+
+
 def _kernel_ms(torch, fn, reps):
     """Mean duration of a call that enqueues one kernel, by events around it."""
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
@@ -275,9 +292,7 @@ def bench_timing(args, torch, workloads, c3, dev):
         vote_time()
         confirm()
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
+    args.warmup = warm_up(torch, step, args.warmup)
     v = c3.verdicts_numpy(ver)
     strag = int(((v["flags"] & c3.RANK_STRAGGLER) != 0).sum())
     proto = int(((v["flags"] & c3.RANK_PROTOCOL) != 0).sum())
@@ -345,9 +360,12 @@ def bench_optimizer(args, torch, workloads, c3, dev):
         o = c3.outliers_numpy(res[4], res[6])
         found[k] = sorted({(chk.UNITS[int(u)], int(r)) for u, r in zip(o["chunk"], o["replica"])})
     log(f"[bench] outliers at the faulted slices: {found}")
-    for i in range(args.warmup):
-        chk.run(k0 + i, hp)
-    torch.cuda.synchronize()
+    wk = [0]
+
+    def warm_step():
+        chk.run(k0 + wk[0], hp)
+        wk[0] += 1
+    args.warmup = warm_up(torch, warm_step, args.warmup)
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
