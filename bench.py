@@ -265,53 +265,64 @@ def _kernel_ms(torch, fn, reps):
 
 def bench_timing(args, torch, workloads, c3, dev):
     """Progress/timing consensus: exact vote on fingerprints, statistical vote
-    on step times, temporal confirmation, one step per pass over all records."""
+    on step times and temporal confirmation (c3_timing_consensus, fused
+    kernels), one step per pass over all records; per-unit results are
+    written."""
     log("[bench] generating config 5")
     w = workloads.make(5, device=dev, scale="full")
     T, G, R = w.T, w.G, w.R
     U = T * G
     total = w.total_bytes
-    out_f = (torch.empty(U, dtype=torch.uint8, device=dev), torch.empty(U, dtype=torch.int64, device=dev),
-             torch.empty(U, dtype=torch.int32, device=dev))
-    out_t = (torch.empty(U, dtype=torch.uint8, device=dev), torch.empty(U, dtype=torch.int64, device=dev),
+    fp_out = (torch.empty(U, dtype=torch.uint8, device=dev), torch.empty(U, dtype=torch.int64, device=dev),
+              torch.empty(U, dtype=torch.int32, device=dev))
+    t_out = (torch.empty(U, dtype=torch.uint8, device=dev), torch.empty(U, dtype=torch.int64, device=dev),
              torch.empty(U, dtype=torch.int32, device=dev))
     ver = torch.empty((R * G, 24), dtype=torch.uint8, device=dev)
-    cws = torch.empty(c3.confirm_workspace_size(R, G, T), dtype=torch.uint8, device=dev)
-
-    def vote_fp():
-        c3.consensus(w.fingerprints, c3.EXACT, out=out_f)
-
-    def vote_time():
-        c3.consensus(w.times, c3.STATISTICAL, out=out_t)
-
-    def confirm():
-        c3.confirm(out_f[1].view(T, G), out_t[1].view(T, G), R, 16, out=ver, workspace=cws)
+    ws = torch.empty(c3.timing_consensus_workspace_size(R, G, T, 16), dtype=torch.uint8, device=dev)
 
     def step():
-        vote_fp()
-        vote_time()
-        confirm()
+        c3.timing_consensus(w.fingerprints, w.times, window=16, out=(ver, fp_out, t_out),
+                            workspace=ws)
+
+    def step_verdicts_only():
+        c3.timing_consensus(w.fingerprints, w.times, window=16, out=(ver, None, None),
+                            workspace=ws)
 
     args.warmup = warm_up(torch, step, args.warmup)
     v = c3.verdicts_numpy(ver)
     strag = int(((v["flags"] & c3.RANK_STRAGGLER) != 0).sum())
     proto = int(((v["flags"] & c3.RANK_PROTOCOL) != 0).sum())
     log(f"[bench] stragglers={strag} protocol_outliers={proto}")
-    e0 = torch.cuda.Event(enable_timing=True)
-    e1 = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    e0.record()
-    for _ in range(args.steps):
-        step()
-    e1.record()
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / args.steps
-    k_time = _kernel_ms(torch, vote_time, args.steps)
-    k_fp = _kernel_ms(torch, vote_fp, args.steps)
-    k_conf = _kernel_ms(torch, confirm, args.steps)
-    time_bytes = U * R * 4 + U * 13          # read the timings, write status, bitmap, index
-    fp_bytes = U * R * 8 + U * 13
-    conf_bytes = 2 * U * 8 + R * G * 24       # both bitmaps read, one verdict per rank
+
+    def timed(fn):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(args.steps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / args.steps
+
+    t0 = time.perf_counter()
+    ms = timed(step)
+    wall = time.perf_counter() - t0
+    ms_verdicts = timed(step_verdicts_only)
+    # the three separate calls, for comparison
+    sep_f = (torch.empty_like(fp_out[0]), torch.empty_like(fp_out[1]), torch.empty_like(fp_out[2]))
+    sep_t = (torch.empty_like(t_out[0]), torch.empty_like(t_out[1]), torch.empty_like(t_out[2]))
+    cws = torch.empty(max(c3.confirm_workspace_size(R, G, T), 256), dtype=torch.uint8, device=dev)
+
+    def separate():
+        c3.consensus(w.fingerprints, c3.EXACT, out=sep_f)
+        c3.consensus(w.times, c3.STATISTICAL, out=sep_t)
+        c3.confirm(sep_f[1].view(T, G), sep_t[1].view(T, G), R, 16, out=ver, workspace=cws)
+    ms_sep = timed(separate)
+    iters = 16 if R <= 8 else 8
+    n_seg = -(-T // iters)
+    masks = 2 * 2 * n_seg * R * G
+    pass_bytes = U * R * (8 + 4) + 2 * U * 13 + masks + masks + R * G * 24
     out = {
         "metric": "timing+fingerprint records GB/s voted+confirmed",
         "value": round(total / (ms * 1e-3) / 1e9, 2),
@@ -328,14 +339,14 @@ def bench_timing(args, torch, workloads, c3, dev):
         "config": {"workload": w.name, "ranks": R * G, "group": R, "iterations": T,
                    "record_bytes_total": total, "stragglers_found": strag,
                    "protocol_outliers_found": proto},
-        "kernels": {
-            "statistical_vote": {"ms": round(k_time, 4), "algorithmic_bytes": time_bytes,
-                                 "GBps": round(time_bytes / (k_time * 1e-3) / 1e9, 1)},
-            "exact_vote": {"ms": round(k_fp, 4), "algorithmic_bytes": fp_bytes,
-                           "GBps": round(fp_bytes / (k_fp * 1e-3) / 1e9, 1)},
-            "confirm": {"ms": round(k_conf, 4), "algorithmic_bytes": conf_bytes,
-                        "GBps": round(conf_bytes / (k_conf * 1e-3) / 1e9, 1)},
-        },
+        "roofline": {"bound": "hbm", "achieved": round(pass_bytes / (ms * 1e-3) / 1e9, 2),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(pass_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                     "traffic": None, "kernel": "timing_vote_kernel+timing_confirm_kernel",
+                     "kernel_ms": round(ms, 4), "algorithmic_bytes_per_launch": pass_bytes},
+        "ms_per_step_verdicts_only": round(ms_verdicts, 4),
+        "ms_per_step_separate_calls": round(ms_sep, 4),
+        "wall_s_timed": round(wall, 3),
     }
     print(json.dumps(out), flush=True)
 

@@ -381,6 +381,40 @@ int c3_localize(const uint8_t *status, const uint64_t *bitmap, const int32_t *ma
                 int64_t out_cap, int64_t *undecided, int64_t und_cap, int64_t *counts, void *ws,
                 size_t ws_bytes, c3_stream_t stream);
 
+/* Device workspace bytes c3_timing_consensus needs (256 at least; 0 if the
+ * sizes are invalid). */
+size_t c3_timing_consensus_workspace_size(int R, int64_t G, int64_t T, int window);
+
+/*
+ * c3_timing_consensus -- the whole timing path in one call: per (iteration
+ * t, group g) exact C3 on the ranks' collective fingerprints (Sec. 5.3; a
+ * minority fingerprint is a protocol outlier, Sec. 7) and statistical C3 on
+ * their step times (Sec. 5.4), then per-rank temporal confirmation (Sec. 10
+ * protocol).  The results equal c3_consensus(fingerprints, EXACT) and
+ * c3_consensus(times, STATISTICAL) per unit and c3_confirm on their bitmaps.
+ *
+ *   fingerprints  device [T][G][R] u64, ranks innermost (8-byte aligned).
+ *   times         device [T][G][R] fp32 (C3_EV_F32) or fp64 (C3_EV_F64).
+ *   kappa         statistical threshold (> 0); window W >= 1 as c3_confirm.
+ *   fp_status/fp_bitmap/fp_majority, t_status/t_bitmap/t_majority
+ *                 device [T*G] per-unit results (unit t*G + g), or all
+ *                 three NULL for a kind whose per-unit results are not
+ *                 wanted (then only the verdicts are produced for it).
+ *   verdicts      device [R*G], rank = r*G + g, as c3_confirm.
+ * For R <= 16 and W <= 64 two fused kernels run: the votes of 16 (8 for
+ * R > 8) iterations x 64 groups per workgroup, packing each rank's outlier
+ * bits through LDS into the workspace, then one thread per rank confirms
+ * from those bits.  Otherwise the three separate steps run, with the
+ * per-unit results kept in the workspace when not requested.
+ * Errors: C3_E_INVAL (sizes, kinds, kappa, outputs half given),
+ * C3_E_WORKSPACE, C3_E_ALIGN, C3_E_HIP.  R * G == 0 does nothing.
+ */
+int c3_timing_consensus(const uint64_t *fingerprints, const void *times, int time_kind, int R,
+                        int64_t G, int64_t T, double kappa, int window, uint8_t *fp_status,
+                        uint64_t *fp_bitmap, int32_t *fp_majority, uint8_t *t_status,
+                        uint64_t *t_bitmap, int32_t *t_majority, c3_rank_verdict_t *verdicts,
+                        void *ws, size_t ws_bytes, c3_stream_t stream);
+
 /* Device workspace bytes c3_confirm needs. */
 size_t c3_confirm_workspace_size(int R, int64_t G, int64_t T);
 

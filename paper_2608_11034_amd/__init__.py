@@ -5,4 +5,5 @@ The work runs in libc3.so (HIP kernels behind the C ABI of include/c3.h);
 """
 from . import c3  # noqa: F401
 from .c3 import (signature, tensor_signature, consensus, localize, confirm, num_chunks,  # noqa: F401
-                 adamw_slice, OptimizerBoundaryCheck, SignaturePlan, C3Error)
+                 adamw_slice, OptimizerBoundaryCheck, timing_consensus, SignaturePlan,
+                 C3Error)

@@ -11,6 +11,8 @@ Entry points (same names as the C ABI):
 * ``consensus(evidence, mode, ...)``     -> status, bitmap, majority index
 * ``localize(status, bitmap, majority_idx, records, R)`` -> lists + counts
 * ``confirm(fp_bitmap, time_bitmap, R, window)`` -> per-rank verdicts
+* ``timing_consensus(fingerprints, times, window)`` -> verdicts (and per-unit
+                                         results): both votes + confirmation
 * ``adamw_slice(params, grads, exp_avgs, exp_avg_sqs, offset, n, hp)``
                                          -> updated slices [R, 3, n] fp32
 * ``OptimizerBoundaryCheck``             replay + signature + vote + localize
@@ -144,6 +146,11 @@ def lib():
         L.c3_optimizer_check_workspace_size.argtypes = [vp]
         L.c3_optimizer_check.restype = i32
         L.c3_optimizer_check.argtypes = [vp, i64, vp, vp, vp, sz, vp]
+        L.c3_timing_consensus_workspace_size.restype = sz
+        L.c3_timing_consensus_workspace_size.argtypes = [i32, i64, i64, i32]
+        L.c3_timing_consensus.restype = i32
+        L.c3_timing_consensus.argtypes = [vp, vp, i32, i32, i64, i64, dbl, i32, vp, vp, vp, vp, vp,
+                                          vp, vp, vp, sz, vp]
         L.c3_job_outcome.restype = i32
         L.c3_job_outcome.argtypes = [i64, i64, i64]
         L.c3_ckpt_init.restype = i32
@@ -383,6 +390,53 @@ def confirm(fp_bitmap, time_bitmap, R: int, window: int = 16, stream=None, out=N
                           ws_bytes, _stream(stream))
     _check(rc, "c3_confirm")
     return out
+
+
+def timing_consensus_workspace_size(R: int, G: int, T: int, window: int = 16) -> int:
+    return int(lib().c3_timing_consensus_workspace_size(R, G, T, window))
+
+
+def timing_consensus(fingerprints, times, window: int = 16, kappa: float = KAPPA_DEFAULT,
+                     per_unit: bool = True, stream=None, out=None, workspace=None):
+    """Exact vote on fingerprints [T, G, R] (int64 bit patterns), statistical
+    vote on times [T, G, R] (float32/float64) and temporal confirmation.
+    Returns (verdicts [R * G, 24] uint8, fp (status, bitmap, majority) or
+    None, time (status, bitmap, majority) or None)."""
+    _dev_tensor(fingerprints, "fingerprints")
+    _dev_tensor(times, "times")
+    if fingerprints.dtype != torch.int64 or fingerprints.dim() != 3:
+        raise C3Error("fingerprints must be int64 [T, G, R]")
+    if times.shape != fingerprints.shape:
+        raise C3Error("times must have the fingerprints' shape [T, G, R]")
+    kind = {torch.float32: EV_F32, torch.float64: EV_F64}.get(times.dtype)
+    if kind is None:
+        raise C3Error("times must be float32 or float64")
+    T, G, R = fingerprints.shape
+    dev = fingerprints.device
+    if out is not None:
+        verdicts, fp_out, t_out = out
+    else:
+        verdicts = _empty((R * G, 24), torch.uint8, dev)
+        fp_out = t_out = None
+        if per_unit:
+            fp_out = (_empty((T * G,), torch.uint8, dev), _empty((T * G,), torch.int64, dev),
+                      _empty((T * G,), torch.int32, dev))
+            t_out = (_empty((T * G,), torch.uint8, dev), _empty((T * G,), torch.int64, dev),
+                     _empty((T * G,), torch.int32, dev))
+    need = timing_consensus_workspace_size(R, G, T, window)
+    if need == 0:
+        raise C3Error("invalid timing-consensus sizes")
+    ws = _empty((need,), torch.uint8, dev) if workspace is None else workspace
+    if ws.numel() < need:
+        raise C3Error("timing-consensus workspace too small")
+    fo = fp_out if fp_out is not None else (None, None, None)
+    to = t_out if t_out is not None else (None, None, None)
+    rc = lib().c3_timing_consensus(_ptr(fingerprints), _ptr(times), kind, R, G, T, float(kappa),
+                                   int(window), _ptr(fo[0]), _ptr(fo[1]), _ptr(fo[2]), _ptr(to[0]),
+                                   _ptr(to[1]), _ptr(to[2]), _ptr(verdicts), _ptr(ws), ws.numel(),
+                                   _stream(stream))
+    _check(rc, "c3_timing_consensus")
+    return verdicts, fp_out, t_out
 
 
 # ---------------------------------------------------------------------------

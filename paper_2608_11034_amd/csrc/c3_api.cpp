@@ -495,6 +495,93 @@ int c3_optimizer_check(const c3_optimizer_state_t* st, int64_t k, const c3_adamw
                        static_cast<unsigned char*>(ws) + sig_ws, ws_bytes - sig_ws, stream);
 }
 
+// ---------------------------------------------------------------------------
+// Timing consensus: exact vote on fingerprints, statistical vote on times and
+// temporal confirmation in one call; fused kernels for R <= 16 and
+// window <= 64, the three separate steps otherwise.
+// ---------------------------------------------------------------------------
+static bool timing_fused(int R, int window) { return R <= 16 && window <= 64; }
+
+static uint64_t timing_fallback_bytes(int R, int64_t G, int64_t T) {
+    const uint64_t n = (uint64_t)T * (uint64_t)G;
+    const uint64_t one = align_up(n, 256) + align_up(8 * n, 256) + align_up(4 * n, 256);
+    return 2 * one + align_up(c3::confirm_ws_bytes(R, G, T), 256);
+}
+
+size_t c3_timing_consensus_workspace_size(int R, int64_t G, int64_t T, int window) {
+    if (R < 1 || R > C3_MAX_REPLICAS || G < 0 || T < 0 || window < 1) return 0;
+    if (T > 0x7FFFFFFF || G > ((int64_t)1 << 40) / (T > 0 ? T : 1)) return 0;
+    const uint64_t b = timing_fused(R, window) ? (uint64_t)c3::timing_masks_bytes(R, G, T)
+                                               : timing_fallback_bytes(R, G, T);
+    return (size_t)(b < 256 ? 256 : b);
+}
+
+int c3_timing_consensus(const uint64_t* fingerprints, const void* times, int time_kind, int R,
+                        int64_t G, int64_t T, double kappa, int window, uint8_t* fp_status,
+                        uint64_t* fp_bitmap, int32_t* fp_majority, uint8_t* t_status,
+                        uint64_t* t_bitmap, int32_t* t_majority, c3_rank_verdict_t* verdicts,
+                        void* ws, size_t ws_bytes, c3_stream_t stream) {
+    if (R < 1 || R > C3_MAX_REPLICAS || G < 0 || T < 0 || window < 1) return C3_E_INVAL;
+    if (time_kind != C3_EV_F32 && time_kind != C3_EV_F64) return C3_E_INVAL;
+    if (!(kappa > 0.0) || kappa > 1e300) return C3_E_INVAL;
+    if (T > 0x7FFFFFFF || (int64_t)R * G > 0x7FFFFFFF) return C3_E_INVAL;
+    const bool fp_out = fp_status != nullptr, t_out = t_status != nullptr;
+    if (fp_out != (fp_bitmap != nullptr) || fp_out != (fp_majority != nullptr) ||
+        t_out != (t_bitmap != nullptr) || t_out != (t_majority != nullptr))
+        return C3_E_INVAL;  // each kind's three outputs are all given or all NULL
+    if ((int64_t)R * G == 0) return C3_OK;
+    if (verdicts == nullptr || (T > 0 && (fingerprints == nullptr || times == nullptr)))
+        return C3_E_INVAL;
+    const size_t need = c3_timing_consensus_workspace_size(R, G, T, window);
+    if (need == 0) return C3_E_INVAL;
+    if (ws == nullptr || !aligned(ws, 256) || ws_bytes < need) return C3_E_WORKSPACE;
+    const int tsize = time_kind == C3_EV_F64 ? 8 : 4;
+    if (!aligned(fingerprints, 8) || !aligned(times, tsize) || !aligned(verdicts, 4) ||
+        !aligned(fp_bitmap, 8) || !aligned(t_bitmap, 8) || !aligned(fp_majority, 4) ||
+        !aligned(t_majority, 4))
+        return C3_E_ALIGN;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    if (timing_fused(R, window)) {
+        const hipError_t e = c3::launch_timing_consensus(fingerprints, times, time_kind, R, G, T,
+                                                         kappa, window, fp_status, fp_bitmap,
+                                                         fp_majority, t_status, t_bitmap, t_majority,
+                                                         verdicts, ws, s);
+        return e == hipSuccess ? C3_OK : C3_E_HIP;
+    }
+    // separate steps; outputs not requested live in the workspace
+    const uint64_t n = (uint64_t)T * (uint64_t)G;
+    unsigned char* w = static_cast<unsigned char*>(ws);
+    auto carve = [&](uint64_t bytes) {
+        unsigned char* p = w;
+        w += align_up(bytes, 256);
+        return p;
+    };
+    uint8_t* fs = reinterpret_cast<uint8_t*>(carve(n));
+    uint64_t* fb = reinterpret_cast<uint64_t*>(carve(8 * n));
+    int32_t* fm = reinterpret_cast<int32_t*>(carve(4 * n));
+    uint8_t* ts = reinterpret_cast<uint8_t*>(carve(n));
+    uint64_t* tb = reinterpret_cast<uint64_t*>(carve(8 * n));
+    int32_t* tm = reinterpret_cast<int32_t*>(carve(4 * n));
+    void* cws = carve(0);
+    if (fp_out) {
+        fs = fp_status;
+        fb = fp_bitmap;
+        fm = fp_majority;
+    }
+    if (t_out) {
+        ts = t_status;
+        tb = t_bitmap;
+        tm = t_majority;
+    }
+    hipError_t e = c3::launch_consensus(fingerprints, C3_EV_U64, 8, 8 * (int64_t)R, R,
+                                        (int64_t)n, C3_EXACT, kappa, fs, fb, fm, s);
+    if (e == hipSuccess)
+        e = c3::launch_consensus(times, time_kind, tsize, (int64_t)tsize * R, R, (int64_t)n,
+                                 C3_STATISTICAL, kappa, ts, tb, tm, s);
+    if (e == hipSuccess) e = c3::launch_confirm(fb, tb, R, G, T, window, verdicts, cws, s);
+    return e == hipSuccess ? C3_OK : C3_E_HIP;
+}
+
 size_t c3_confirm_workspace_size(int R, int64_t G, int64_t T) {
     if (R < 1 || R > C3_MAX_REPLICAS || G < 0 || T < 0) return 0;
     return c3::confirm_ws_bytes(R, G, T);

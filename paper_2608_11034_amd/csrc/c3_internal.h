@@ -39,6 +39,16 @@ hipError_t launch_adamw_slice(const AdamwPtrs& ptrs, const AdamwConst& c, int R,
                               int64_t offset, int64_t n, float* out, int64_t stride,
                               hipStream_t stream);
 
+// Fused timing consensus (R <= 16, window <= 64): vote both evidence kinds
+// per (iteration, group), pack per-rank bits, confirm per rank.  The
+// workspace holds the packed masks (timing_masks_bytes).
+int64_t timing_masks_bytes(int R, int64_t G, int64_t T);
+hipError_t launch_timing_consensus(const uint64_t* fp, const void* times, int time_kind, int R,
+                                   int64_t G, int64_t T, double kappa, int window,
+                                   uint8_t* fp_status, uint64_t* fp_bitmap, int32_t* fp_majority,
+                                   uint8_t* t_status, uint64_t* t_bitmap, int32_t* t_majority,
+                                   c3_rank_verdict_t* verdicts, void* ws, hipStream_t stream);
+
 hipError_t launch_consensus(const void* evidence, int kind, int64_t rstride, int64_t ustride, int R,
                             int64_t n_units, int mode, double kappa, uint8_t* status,
                             uint64_t* bitmap, int32_t* majority_idx, hipStream_t stream);

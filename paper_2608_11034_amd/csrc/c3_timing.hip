@@ -1,0 +1,273 @@
+// Timing consensus of C3 for gfx950: per (iteration, peer group) an exact
+// vote on the ranks' collective fingerprints (Sec. 7: a minority fingerprint
+// is a protocol outlier) and a statistical vote on their step times
+// (Sec. 5.4), then the per-rank temporal confirmation (Sec. 10: a straggler
+// must recur).  The votes are the per-unit decisions of c3_vote_row.h, as in
+// c3_consensus; besides the optional per-unit results they OR each outlier
+// bit into a per-rank mask (one 32-bit word per rank, kind and 32
+// iterations), so the confirmation reads 8 bytes per rank and 32 iterations
+// instead of the per-unit bitmaps, and walks them a word at a time.
+#include "c3_device.h"
+#include "c3_internal.h"
+#include "c3_vote_row.h"
+
+namespace c3 {
+
+constexpr int kVoteThreads = 256;
+constexpr int kSegIters = 32;      // iterations per mask segment (one u32 per rank and kind)
+constexpr int kConfirmThreads = 256;
+constexpr int kConfirmLanes = 8;   // lanes per rank in the confirmation
+constexpr int kPrefetch = 8;       // mask segments fetched at once per lane
+
+// One evidence kind per launch, one thread per unit u = t * G + g (a wave
+// reads 64 consecutive rows, fully coalesced), deciding with the per-unit
+// functions of c3_vote_row.h.  Outlier bits also go to the per-rank masks
+// [segment][r][g] (bit t mod 32 of word t / 32) by atomic OR; they are
+// sparse, so the atomics cost little, and the masks must start zeroed.
+template <int NMAX, int MODE>
+__global__ void __launch_bounds__(kVoteThreads) timing_vote_kernel(
+    const char* __restrict__ ev, int kind, int R, int64_t G, int64_t n_units, double kappa,
+    bool dense, uint8_t* __restrict__ status, uint64_t* __restrict__ bitmap,
+    int32_t* __restrict__ majority, uint32_t* __restrict__ masks) {
+    const int64_t u = (int64_t)blockIdx.x * kVoteThreads + threadIdx.x;
+    if (u >= n_units) return;
+    const int64_t vsize = (kind == C3_EV_U64 || kind == C3_EV_F64) ? 8 : 4;
+    uint64_t e[NMAX];
+    load_row_bits<NMAX>(ev + u * R * vsize, kind, vsize, R, dense, e);
+    const UnitVote v = MODE == C3_EXACT ? exact_vote_row<NMAX>(e, R)
+                                        : statistical_vote_row<NMAX>(e, kind, R, kappa);
+    if (status != nullptr) {
+        status[u] = v.status;
+        bitmap[u] = v.bitmap;
+        majority[u] = v.majority;
+    }
+    if (v.bitmap != 0ull) {
+        // 32-bit division when the unit count allows it (uniform per launch)
+        const int64_t t = n_units <= 0xFFFFFFFFll ? (int64_t)((uint32_t)u / (uint32_t)G) : u / G;
+        const int64_t g = u - t * G;
+        const uint32_t bit = 1u << (t & (kSegIters - 1));
+        uint32_t* m = masks + (t / kSegIters) * R * G + g;
+        for (uint64_t b = v.bitmap; b != 0ull; b &= b - 1ull)
+            atomicOr(m + (int64_t)__builtin_ctzll(b) * G, bit);
+    }
+}
+
+// Clears n16 16-byte words (the mask area is a multiple of 256 bytes).
+__global__ void __launch_bounds__(256) timing_zero_kernel(uint4* __restrict__ p, int64_t n16) {
+    const int64_t step = (int64_t)gridDim.x * 256;
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n16; i += step)
+        p[i] = make_uint4(0u, 0u, 0u, 0u);
+}
+
+// Confirmation: kConfirmLanes adjacent lanes per rank, each over a
+// contiguous run of whole segments; a lane also reads up to W - 1 timing
+// bits past its run so it sees every window that starts in it.  Lanes
+// combine with shuffles.  Positions q = t - t_lo (32 bits): iteration t
+// counts if q < len, closes this lane's pair (t - 1, t) if 1 <= q <= len,
+// and ends window [t - Wt + 1, t], this lane's if Wt - 1 <= q < len + Wt - 1.
+// With Wt <= 32 the window ending at bit i of a segment is a 32-bit field
+// of the 64 bits (segment : previous segment); longer windows keep a 64-bit
+// shift register.  Segments whose window bits are all zero are skipped.
+template <bool SHORT>
+__global__ void __launch_bounds__(kConfirmThreads) timing_confirm_kernel(
+    const uint32_t* __restrict__ fp_masks, const uint32_t* __restrict__ t_masks, int R, int64_t G,
+    int64_t T, int Wt, c3_rank_verdict_t* __restrict__ verdicts) {
+    const int64_t idx = (int64_t)blockIdx.x * kConfirmThreads + threadIdx.x;
+    const int64_t rank = idx / kConfirmLanes;
+    const int part = (int)(idx % kConfirmLanes);
+    const bool live = rank < (int64_t)R * G;    // dead lanes still join the shuffles
+    const int64_t r = live ? rank / G : 0, g = live ? rank - r * G : 0;
+    const int64_t n_seg = (T + kSegIters - 1) / kSegIters;
+    const int64_t per = (n_seg + kConfirmLanes - 1) / kConfirmLanes;   // segments per lane
+    const int64_t s_lo = part * per;
+    const int64_t t_lo = s_lo * kSegIters;
+    int64_t t_hi = t_lo + per * kSegIters;
+    if (t_hi > T) t_hi = T;
+    int64_t t_end = t_hi + Wt - 1;            // last window starting before t_hi ends here
+    if (t_end > T) t_end = T;
+    uint32_t flags = 0, dc = 0, sc = 0, mw = 0;
+    int32_t fd = -1, fw = -1;
+    if (live && t_lo < t_hi) {
+        const int64_t stride = (int64_t)R * G;
+        const uint32_t* fpm = fp_masks + r * G + g;
+        const uint32_t* tpm = t_masks + r * G + g;
+        const uint32_t len = (uint32_t)(t_hi - t_lo);
+        const uint32_t wlo = (uint32_t)(Wt - 1);
+        const uint64_t wmask = Wt >= 64 ? ~0ull : ((1ull << Wt) - 1ull);
+        uint32_t prev = 0;                      // the previous segment's bits
+        uint64_t hist = 0;                      // (long windows) bit k: iteration t - k
+        for (int64_t s0 = s_lo; s0 * kSegIters < t_end; s0 += kPrefetch) {
+            // both kinds' masks of the next kPrefetch segments in one batch
+            uint32_t tmv[kPrefetch], fmv[kPrefetch];
+#pragma unroll
+            for (int j = 0; j < kPrefetch; ++j) {
+                tmv[j] = (s0 + j) * kSegIters < t_end ? tpm[(s0 + j) * stride] : 0u;
+                fmv[j] = (s0 + j) * kSegIters < t_hi ? fpm[(s0 + j) * stride] : 0u;
+            }
+#pragma unroll
+            for (int j = 0; j < kPrefetch; ++j) {
+                // fingerprint bits: counts and the first attributed iteration
+                // (bits past T were never set)
+                if (fmv[j] != 0u && fd < 0)
+                    fd = (int32_t)((s0 + j) * kSegIters + __builtin_ctz(fmv[j]));
+                dc += (uint32_t)__builtin_popcount(fmv[j]);
+                const int64_t left = t_end - (s0 + j) * kSegIters;
+                const uint32_t n = left <= 0 ? 0u : left < kSegIters ? (uint32_t)left : kSegIters;
+                if (n == 0u) break;
+                const uint32_t q0 = (uint32_t)((s0 + j - s_lo) * kSegIters);
+                const uint32_t tm = n < 32u ? tmv[j] & ((1u << n) - 1u) : tmv[j];
+                // counts at positions q0 + i < len
+                const uint32_t cn = len > q0 ? (len - q0 < n ? len - q0 : n) : 0u;
+                sc += (uint32_t)__builtin_popcount(cn < 32u ? tm & ((1u << cn) - 1u) : tm);
+                // pairs ending at q0 + i with 1 <= q0 + i <= len
+                const uint32_t pairs = tm & ((tm << 1) | (prev >> 31));
+                const uint32_t p_hi = len + 1u > q0 ? (len + 1u - q0 < n ? len + 1u - q0 : n) : 0u;
+                const uint32_t p_mask = (p_hi < 32u ? (1u << p_hi) - 1u : ~0u) & (q0 == 0u ? ~1u : ~0u);
+                if (pairs & p_mask) flags |= C3_RANK_CONSEC2;
+                // windows ending at positions i in [lo_i, hi_i) of this segment
+                const uint32_t lo_i = wlo > q0 ? wlo - q0 : 0u;
+                const uint32_t hi_q = wlo + len - q0;       // exclusive, may exceed n
+                const uint32_t hi_i = wlo + len > q0 ? (hi_q < n ? hi_q : n) : 0u;
+                // No window here can raise the maximum or pass the threshold
+                // when all set bits of (segment : previous) could not.
+                const uint32_t ybits = (uint32_t)__builtin_popcount(tm) + __builtin_popcount(prev);
+                if (SHORT) {
+                    if ((ybits > mw || (2u * ybits > (uint32_t)Wt && fw < 0)) && lo_i < hi_i) {
+                        const uint64_t y = ((uint64_t)tm << 32) | prev;
+                        const uint32_t wm = (uint32_t)wmask;
+                        uint32_t over = 0, smax = 0;
+#pragma unroll 4
+                        for (uint32_t i = 0; i < (uint32_t)kSegIters; ++i) {
+                            const uint32_t c = (uint32_t)__builtin_popcount(
+                                (uint32_t)(y >> (33u + i - (uint32_t)Wt)) & wm);
+                            const bool ok = i >= lo_i && i < hi_i;
+                            smax = ok && c > smax ? c : smax;
+                            over |= (ok && 2u * c > (uint32_t)Wt) ? (1u << i) : 0u;
+                        }
+                        mw = smax > mw ? smax : mw;
+                        if (over != 0u && fw < 0)
+                            fw = (int32_t)(t_lo + (int64_t)(q0 + __builtin_ctz(over) - wlo));
+                    }
+                } else {
+                    if ((tm != 0u || hist != 0ull)) {
+                        for (uint32_t i = 0; i < n; ++i) {
+                            hist = (hist << 1) | ((tm >> i) & 1u);
+                            if (i >= lo_i && i < hi_i) {
+                                const uint32_t c = (uint32_t)__builtin_popcountll(hist & wmask);
+                                mw = c > mw ? c : mw;
+                                if (2u * c > (uint32_t)Wt && fw < 0)
+                                    fw = (int32_t)(t_lo + (int64_t)(q0 + i - wlo));
+                            }
+                        }
+                    }
+                }
+                prev = tm;
+            }
+        }
+    }
+    // combine the lanes of one rank: sums, maxima, first (smallest >= 0) positions
+#pragma unroll
+    for (int o = 1; o < kConfirmLanes; o <<= 1) {
+        flags |= (uint32_t)__shfl_xor((int)flags, o, kConfirmLanes);
+        dc += (uint32_t)__shfl_xor((int)dc, o, kConfirmLanes);
+        sc += (uint32_t)__shfl_xor((int)sc, o, kConfirmLanes);
+        const uint32_t m2 = (uint32_t)__shfl_xor((int)mw, o, kConfirmLanes);
+        mw = m2 > mw ? m2 : mw;
+        const int32_t f2 = __shfl_xor(fd, o, kConfirmLanes);
+        fd = (fd < 0 || (f2 >= 0 && f2 < fd)) ? f2 : fd;
+        const int32_t w2 = __shfl_xor(fw, o, kConfirmLanes);
+        fw = (fw < 0 || (w2 >= 0 && w2 < fw)) ? w2 : fw;
+    }
+    if (!live || part != 0) return;
+    if (fw >= 0) flags |= C3_RANK_STRAGGLER;
+    if (fd >= 0) flags |= C3_RANK_PROTOCOL;
+    c3_rank_verdict_t v;
+    v.flags = flags;
+    v.first_divergent_iter = fd;
+    v.divergent_count = dc;
+    v.slow_count = sc;
+    v.max_window_slow = mw;
+    v.first_straggler_window = fw;
+    verdicts[rank] = v;
+}
+
+int64_t timing_masks_bytes(int R, int64_t G, int64_t T) {
+    const int64_t n_seg = (T + kSegIters - 1) / kSegIters;
+    return 2 * ((n_seg * R * G * 4 + 255) / 256 * 256);
+}
+
+template <int NMAX, int MODE>
+static hipError_t launch_vote(const char* ev, int kind, int R, int64_t G, int64_t n_units,
+                              double kappa, uint8_t* status, uint64_t* bitmap, int32_t* majority,
+                              uint32_t* masks, hipStream_t stream) {
+    const int64_t blocks = (n_units + kVoteThreads - 1) / kVoteThreads;
+    const int64_t vsize = (kind == C3_EV_U64 || kind == C3_EV_F64) ? 8 : 4;
+    const bool dense = (R * vsize) % 16 == 0 && ((uintptr_t)ev & 15) == 0;
+    if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
+    if (blocks == 0) return hipSuccess;
+    hipLaunchKernelGGL((timing_vote_kernel<NMAX, MODE>), dim3((unsigned)blocks), dim3(kVoteThreads),
+                       0, stream, ev, kind, R, G, n_units, kappa, dense, status, bitmap, majority,
+                       masks);
+    return hipGetLastError();
+}
+
+template <int NMAX>
+static hipError_t launch_votes(const uint64_t* fp, const char* tp, int time_kind, int R, int64_t G,
+                               int64_t n_units, double kappa, uint8_t* fs, uint64_t* fb,
+                               int32_t* fmj, uint8_t* ts, uint64_t* tb, int32_t* tmj,
+                               uint32_t* fm, uint32_t* tm, hipStream_t stream) {
+    hipError_t e = launch_vote<NMAX, C3_EXACT>(reinterpret_cast<const char*>(fp), C3_EV_U64, R, G,
+                                               n_units, kappa, fs, fb, fmj, fm, stream);
+    if (e != hipSuccess) return e;
+    return launch_vote<NMAX, C3_STATISTICAL>(tp, time_kind, R, G, n_units, kappa, ts, tb, tmj, tm,
+                                             stream);
+}
+
+hipError_t launch_timing_consensus(const uint64_t* fp, const void* times, int time_kind, int R,
+                                   int64_t G, int64_t T, double kappa, int window,
+                                   uint8_t* fp_status, uint64_t* fp_bitmap, int32_t* fp_majority,
+                                   uint8_t* t_status, uint64_t* t_bitmap, int32_t* t_majority,
+                                   c3_rank_verdict_t* verdicts, void* ws, hipStream_t stream) {
+    const int64_t ranks = (int64_t)R * G;
+    if ((ranks * kConfirmLanes + kConfirmThreads - 1) / kConfirmThreads > 0x7FFFFFFF)
+        return hipErrorInvalidValue;
+    if (ranks == 0) return hipSuccess;
+    const int64_t half = timing_masks_bytes(R, G, T) / 2;
+    uint32_t* fm = static_cast<uint32_t*>(ws);
+    uint32_t* tm = reinterpret_cast<uint32_t*>(static_cast<char*>(ws) + half);
+    // the masks collect bits by atomic OR: clear them with a kernel (a memset
+    // node would not survive graph capture reliably)
+    const int64_t n16 = 2 * half / 16;
+    if (n16 > 0) {
+        const int64_t blocks = (n16 + 255) / 256 < 4096 ? (n16 + 255) / 256 : 4096;
+        hipLaunchKernelGGL(timing_zero_kernel, dim3((unsigned)blocks), dim3(256), 0, stream,
+                           reinterpret_cast<uint4*>(fm), n16);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    const char* tp = static_cast<const char*>(times);
+    const int64_t n_units = T * G;
+    hipError_t e;
+    if (R <= 4)
+        e = launch_votes<4>(fp, tp, time_kind, R, G, n_units, kappa, fp_status, fp_bitmap,
+                            fp_majority, t_status, t_bitmap, t_majority, fm, tm, stream);
+    else if (R <= 8)
+        e = launch_votes<8>(fp, tp, time_kind, R, G, n_units, kappa, fp_status, fp_bitmap,
+                            fp_majority, t_status, t_bitmap, t_majority, fm, tm, stream);
+    else
+        e = launch_votes<16>(fp, tp, time_kind, R, G, n_units, kappa, fp_status, fp_bitmap,
+                             fp_majority, t_status, t_bitmap, t_majority, fm, tm, stream);
+    if (e != hipSuccess) return e;
+    const int Wt = (int64_t)window < T ? window : (int)T;
+    const int64_t threads = ranks * kConfirmLanes;
+    const dim3 grid((unsigned)((threads + kConfirmThreads - 1) / kConfirmThreads));
+    if (Wt <= 32)
+        hipLaunchKernelGGL(timing_confirm_kernel<true>, grid, dim3(kConfirmThreads), 0, stream, fm,
+                           tm, R, G, T, Wt, verdicts);
+    else
+        hipLaunchKernelGGL(timing_confirm_kernel<false>, grid, dim3(kConfirmThreads), 0, stream, fm,
+                           tm, R, G, T, Wt, verdicts);
+    return hipGetLastError();
+}
+
+}  // namespace c3

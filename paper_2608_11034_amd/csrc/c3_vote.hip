@@ -1,9 +1,8 @@
 // Consensus kernels of C3 for gfx950: the decision step of Algorithm 1.
 //
 // Groups of up to 16 replicas: one thread per unit, the R values in
-// registers (128-bit row loads when replicas are adjacent), order
-// statistics from min/max bitonic sorting networks, and the lower-median
-// replica from counts in the stable (value, replica) order.  Larger groups:
+// registers (128-bit row loads when replicas are adjacent), deciding with
+// the per-unit functions of c3_vote_row.h.  Larger groups:
 //
 // Layout: one lane per (unit, replica).  A unit's R values sit in a group of
 // W = next_pow2(R) consecutive lanes of one wave64 (64 / W units per wave),
@@ -27,15 +26,11 @@
 // plain definition does.
 #include "c3_device.h"
 #include "c3_internal.h"
+#include "c3_vote_row.h"
 
 namespace c3 {
 
 constexpr int kVoteThreads = 256;
-
-__device__ inline uint64_t load_ev_bits(const char* p, int kind) {
-    if (kind == C3_EV_U64 || kind == C3_EV_F64) return *reinterpret_cast<const uint64_t*>(p);
-    return *reinterpret_cast<const uint32_t*>(p);
-}
 
 __device__ inline double load_ev_f64(const char* p, int kind) {
     if (kind == C3_EV_F32) return (double)*reinterpret_cast<const float*>(p);
@@ -177,40 +172,6 @@ __global__ void __launch_bounds__(kVoteThreads) statistical_vote_kernel(
 // here the whole decision is register arithmetic.  NMAX is R rounded up to
 // a power of two; slots past R are padding that never takes part.
 // ---------------------------------------------------------------------------
-typedef uint32_t vu32x4 __attribute__((ext_vector_type(4)));
-
-// Raw bits of the R values of one unit (4-byte kinds zero-extended).  With
-// `dense` the replicas are adjacent and the row is 16-byte aligned and a
-// whole number of 16-byte words, so it is read with 128-bit loads.
-template <int NMAX>
-__device__ __forceinline__ void load_row_bits(const char* base, int kind, int64_t rstride, int R,
-                                              bool dense, uint64_t (&e)[NMAX]) {
-    const bool wide = kind == C3_EV_U64 || kind == C3_EV_F64;
-    if (dense && wide) {
-#pragma unroll
-        for (int j = 0; j < NMAX / 2; ++j) {
-            vu32x4 v = {0u, 0u, 0u, 0u};
-            if (2 * j < R) v = *reinterpret_cast<const vu32x4*>(base + 16 * j);
-            e[2 * j] = ((uint64_t)v.y << 32) | v.x;
-            e[2 * j + 1] = ((uint64_t)v.w << 32) | v.z;
-        }
-    } else if (dense && NMAX >= 4) {
-#pragma unroll
-        for (int j = 0; j < NMAX / 4; ++j) {
-            vu32x4 v = {0u, 0u, 0u, 0u};
-            if (4 * j < R) v = *reinterpret_cast<const vu32x4*>(base + 16 * j);
-            e[4 * j] = v.x;
-            e[4 * j + 1] = v.y;
-            e[4 * j + 2] = v.z;
-            e[4 * j + 3] = v.w;
-        }
-    } else {
-#pragma unroll
-        for (int r = 0; r < NMAX; ++r)
-            e[r] = r < R ? load_ev_bits(base + (int64_t)r * rstride, kind) : 0ull;
-    }
-}
-
 template <int NMAX>
 __global__ void __launch_bounds__(kVoteThreads) exact_vote_small_kernel(
     const char* __restrict__ ev, int kind, int64_t rstride, int64_t ustride, int R, int64_t n_units,
@@ -220,82 +181,10 @@ __global__ void __launch_bounds__(kVoteThreads) exact_vote_small_kernel(
     if (u >= n_units) return;
     uint64_t e[NMAX];
     load_row_bits<NMAX>(ev + u * ustride, kind, rstride, R, dense, e);
-    uint64_t maj = 0, other = 0;
-#pragma unroll
-    for (int r = 0; r < NMAX; ++r) {
-        int cnt = 0;
-#pragma unroll
-        for (int j = 0; j < NMAX; ++j) cnt += (j < R && e[j] == e[r]) ? 1 : 0;
-        if (r < R) {
-            if (2 * cnt > R) maj |= 1ull << r; else other |= 1ull << r;
-        }
-    }
-    if (maj == 0) {
-        status[u] = C3_INCONCLUSIVE;
-        bitmap[u] = 0;
-        majority_idx[u] = -1;
-    } else {
-        status[u] = other ? C3_ATTRIBUTED : C3_AGREE;
-        bitmap[u] = other;
-        majority_idx[u] = __builtin_ctzll(maj);
-    }
-}
-
-// Bitonic sorting network over N register slots (N a power of two, values
-// without NaN): each comparator is one min and one max.
-template <int N>
-__device__ __forceinline__ void bitonic_sort(double (&v)[N]) {
-    constexpr int LOG = N == 2 ? 1 : N == 4 ? 2 : N == 8 ? 3 : 4;
-    static_assert((1 << LOG) == N, "power of two up to 16");
-#pragma unroll
-    for (int kk = 1; kk <= LOG; ++kk) {
-#pragma unroll
-        for (int jj = kk - 1; jj >= 0; --jj) {
-#pragma unroll
-            for (int i = 0; i < N; ++i) {
-                const int l = i ^ (1 << jj);
-                if (l > i) {
-                    const double lo = fmin(v[i], v[l]), hi = fmax(v[i], v[l]);
-                    const bool up = (i & (1 << kk)) == 0;
-                    v[i] = up ? lo : hi;
-                    v[l] = up ? hi : lo;
-                }
-            }
-        }
-    }
-}
-
-// v[k] for a run-time k, as an OR of masked slots.  A select chain would be
-// turned back into an indexed load, which puts the array in scratch memory.
-template <int N>
-__device__ __forceinline__ double pick(const double (&v)[N], int k) {
-    uint64_t out = 0;
-#pragma unroll
-    for (int i = 0; i < N; ++i) {
-        const uint64_t m = 0ull - (uint64_t)(i == k);
-        out |= m & (uint64_t)__double_as_longlong(v[i]);
-    }
-    return __longlong_as_double((long long)out);
-}
-
-template <int N>
-__device__ __forceinline__ double median_sorted(const double (&s)[N], int n) {
-    if (n & 1) return pick<N>(s, (n - 1) / 2);
-    return (pick<N>(s, n / 2 - 1) + pick<N>(s, n / 2)) * 0.5;
-}
-
-template <int N>
-__device__ __forceinline__ double quantile7_sorted(const double (&s)[N], int n, double p) {
-    const double h = (double)(n - 1) * p;
-    const double fl = floor(h);
-    const int lo = (int)fl;
-    const double frac = h - fl;
-    if (lo + 1 >= n) return pick<N>(s, n - 1);
-    const double a = pick<N>(s, lo);
-    const double b = pick<N>(s, lo + 1);
-    const double diff = b - a;
-    const double prod = frac * diff;
-    return a + prod;
+    const UnitVote v = exact_vote_row<NMAX>(e, R);
+    status[u] = v.status;
+    bitmap[u] = v.bitmap;
+    majority_idx[u] = v.majority;
 }
 
 template <int NMAX>
@@ -305,67 +194,12 @@ __global__ void __launch_bounds__(kVoteThreads) statistical_vote_small_kernel(
     int32_t* __restrict__ majority_idx) {
     const int64_t u = (int64_t)blockIdx.x * kVoteThreads + threadIdx.x;
     if (u >= n_units) return;
-    const double inf = __builtin_huge_val();
     uint64_t bits[NMAX];
     load_row_bits<NMAX>(ev + u * ustride, kind, rstride, R, dense, bits);
-    double x[NMAX], s[NMAX];
-    uint64_t fin = 0;
-#pragma unroll
-    for (int r = 0; r < NMAX; ++r) {
-        x[r] = kind == C3_EV_F32 ? (double)__uint_as_float((uint32_t)bits[r])
-                                 : __longlong_as_double((long long)bits[r]);
-        const bool f = r < R && __builtin_isfinite(x[r]);
-        fin |= (uint64_t)f << r;
-        s[r] = f ? x[r] : inf;      // excluded values sort after every finite one
-    }
-    const uint64_t valid = R == 64 ? ~0ull : ((1ull << R) - 1);
-    const uint64_t nonfin = valid & ~fin;
-    const int nf = __builtin_popcountll(fin);
-    if (2 * nf <= R) {
-        status[u] = C3_INCONCLUSIVE;
-        bitmap[u] = 0;
-        majority_idx[u] = -1;
-        return;
-    }
-    bitonic_sort<NMAX>(s);
-    const double m = median_sorted<NMAX>(s, nf);
-    double dev[NMAX], ds[NMAX];
-#pragma unroll
-    for (int r = 0; r < NMAX; ++r) {
-        dev[r] = ((fin >> r) & 1ull) ? fabs(x[r] - m) : inf;
-        ds[r] = dev[r];
-    }
-    bitonic_sort<NMAX>(ds);
-    double d = median_sorted<NMAX>(ds, nf);
-    if (d == 0.0) {
-        const double q3 = quantile7_sorted<NMAX>(s, nf, 0.75);
-        const double q1 = quantile7_sorted<NMAX>(s, nf, 0.25);
-        d = (q3 - q1) * 0.5;
-    }
-    if (d == 0.0) d = (pick<NMAX>(s, nf - 1) - s[0]) / (double)nf;
-    uint64_t B = nonfin;
-    if (d != 0.0) {
-        const double thr = kappa * d;
-#pragma unroll
-        for (int r = 0; r < NMAX; ++r)
-            if (((fin >> r) & 1ull) && dev[r] > thr) B |= 1ull << r;
-    }
-    // lower-median replica: stable position (nf - 1) / 2 in (value, replica) order
-    const double target = pick<NMAX>(s, (nf - 1) / 2);
-    int want = (nf - 1) / 2;
-#pragma unroll
-    for (int r = 0; r < NMAX; ++r) want -= (((fin >> r) & 1ull) && x[r] < target) ? 1 : 0;
-    int med = -1;
-#pragma unroll
-    for (int r = 0; r < NMAX; ++r) {
-        if (((fin >> r) & 1ull) && x[r] == target) {
-            if (want == 0 && med < 0) med = r;
-            --want;
-        }
-    }
-    status[u] = B ? C3_ATTRIBUTED : C3_AGREE;
-    bitmap[u] = B;
-    majority_idx[u] = med;
+    const UnitVote v = statistical_vote_row<NMAX>(bits, kind, R, kappa);
+    status[u] = v.status;
+    bitmap[u] = v.bitmap;
+    majority_idx[u] = v.majority;
 }
 
 template <int NMAX>

@@ -1,0 +1,218 @@
+// Per-unit decisions of Algorithm 1 for groups of up to 16 replicas, one
+// thread per unit with the R values in registers.  Used by the consensus
+// kernels (c3_vote.hip) and the fused timing-consensus kernel
+// (c3_timing.hip), so both decide every unit with the same code.
+//
+// EXACT (Sec. 5.3): each replica counts the peers equal to it; a strict
+// majority exists iff some count c satisfies 2c > R, the majority replicas
+// are exactly those, the bitmap marks the others and the majority index is
+// the lowest majority replica.
+//
+// STATISTICAL (Sec. 5.4), in fp64: order statistics from min/max bitonic
+// sorting networks over the finite values (non-finite ones sort last and are
+// outliers), RobustScale in the order MAD -> IQR / 2 (type-7 quartiles) ->
+// range / n_finite, strict |x - m| > kappa d, and the lower-median replica in
+// the stable (value, replica) order.  Files including this header are
+// compiled without floating-point contraction, so the decision rounds
+// exactly as the plain definition does.
+#pragma once
+
+#include "c3_device.h"
+
+namespace c3 {
+
+typedef uint32_t vu32x4 __attribute__((ext_vector_type(4)));
+
+struct UnitVote {
+    uint64_t bitmap;
+    int32_t majority;
+    uint8_t status;
+};
+
+__device__ inline uint64_t load_ev_bits(const char* p, int kind) {
+    if (kind == C3_EV_U64 || kind == C3_EV_F64) return *reinterpret_cast<const uint64_t*>(p);
+    return *reinterpret_cast<const uint32_t*>(p);
+}
+
+// Raw bits of the R values of one unit (4-byte kinds zero-extended).  With
+// `dense` the replicas are adjacent and the row is 16-byte aligned and a
+// whole number of 16-byte words, so it is read with 128-bit loads.
+template <int NMAX>
+__device__ __forceinline__ void load_row_bits(const char* base, int kind, int64_t rstride, int R,
+                                              bool dense, uint64_t (&e)[NMAX]) {
+    const bool wide = kind == C3_EV_U64 || kind == C3_EV_F64;
+    if (dense && wide) {
+#pragma unroll
+        for (int j = 0; j < NMAX / 2; ++j) {
+            vu32x4 v = {0u, 0u, 0u, 0u};
+            if (2 * j < R) v = *reinterpret_cast<const vu32x4*>(base + 16 * j);
+            e[2 * j] = ((uint64_t)v.y << 32) | v.x;
+            e[2 * j + 1] = ((uint64_t)v.w << 32) | v.z;
+        }
+    } else if (dense && NMAX >= 4) {
+#pragma unroll
+        for (int j = 0; j < NMAX / 4; ++j) {
+            vu32x4 v = {0u, 0u, 0u, 0u};
+            if (4 * j < R) v = *reinterpret_cast<const vu32x4*>(base + 16 * j);
+            e[4 * j] = v.x;
+            e[4 * j + 1] = v.y;
+            e[4 * j + 2] = v.z;
+            e[4 * j + 3] = v.w;
+        }
+    } else {
+#pragma unroll
+        for (int r = 0; r < NMAX; ++r)
+            e[r] = r < R ? load_ev_bits(base + (int64_t)r * rstride, kind) : 0ull;
+    }
+}
+
+template <int NMAX>
+__device__ __forceinline__ UnitVote exact_vote_row(const uint64_t (&e)[NMAX], int R) {
+    uint64_t maj = 0, other = 0;
+#pragma unroll
+    for (int r = 0; r < NMAX; ++r) {
+        int cnt = 0;
+#pragma unroll
+        for (int j = 0; j < NMAX; ++j) cnt += (j < R && e[j] == e[r]) ? 1 : 0;
+        if (r < R) {
+            if (2 * cnt > R) maj |= 1ull << r; else other |= 1ull << r;
+        }
+    }
+    UnitVote v;
+    if (maj == 0) {
+        v.status = C3_INCONCLUSIVE;
+        v.bitmap = 0;
+        v.majority = -1;
+    } else {
+        v.status = other ? C3_ATTRIBUTED : C3_AGREE;
+        v.bitmap = other;
+        v.majority = __builtin_ctzll(maj);
+    }
+    return v;
+}
+
+// Bitonic sorting network over N register slots (N a power of two, values
+// without NaN): each comparator is one min and one max.
+template <int N>
+__device__ __forceinline__ void bitonic_sort(double (&v)[N]) {
+    constexpr int LOG = N == 2 ? 1 : N == 4 ? 2 : N == 8 ? 3 : 4;
+    static_assert((1 << LOG) == N, "power of two up to 16");
+#pragma unroll
+    for (int kk = 1; kk <= LOG; ++kk) {
+#pragma unroll
+        for (int jj = kk - 1; jj >= 0; --jj) {
+#pragma unroll
+            for (int i = 0; i < N; ++i) {
+                const int l = i ^ (1 << jj);
+                if (l > i) {
+                    const double lo = fmin(v[i], v[l]), hi = fmax(v[i], v[l]);
+                    const bool up = (i & (1 << kk)) == 0;
+                    v[i] = up ? lo : hi;
+                    v[l] = up ? hi : lo;
+                }
+            }
+        }
+    }
+}
+
+// v[k] for a run-time k, as an OR of masked slots.  A select chain would be
+// turned back into an indexed load, which puts the array in scratch memory.
+template <int N>
+__device__ __forceinline__ double pick(const double (&v)[N], int k) {
+    uint64_t out = 0;
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+        const uint64_t m = 0ull - (uint64_t)(i == k);
+        out |= m & (uint64_t)__double_as_longlong(v[i]);
+    }
+    return __longlong_as_double((long long)out);
+}
+
+template <int N>
+__device__ __forceinline__ double median_sorted(const double (&s)[N], int n) {
+    if (n & 1) return pick<N>(s, (n - 1) / 2);
+    return (pick<N>(s, n / 2 - 1) + pick<N>(s, n / 2)) * 0.5;
+}
+
+template <int N>
+__device__ __forceinline__ double quantile7_sorted(const double (&s)[N], int n, double p) {
+    const double h = (double)(n - 1) * p;
+    const double fl = floor(h);
+    const int lo = (int)fl;
+    const double frac = h - fl;
+    if (lo + 1 >= n) return pick<N>(s, n - 1);
+    const double a = pick<N>(s, lo);
+    const double b = pick<N>(s, lo + 1);
+    const double diff = b - a;
+    const double prod = frac * diff;
+    return a + prod;
+}
+
+// `bits` hold fp32 (kind C3_EV_F32, zero-extended) or fp64 patterns.
+template <int NMAX>
+__device__ __forceinline__ UnitVote statistical_vote_row(const uint64_t (&bits)[NMAX], int kind,
+                                                         int R, double kappa) {
+    const double inf = __builtin_huge_val();
+    double x[NMAX], s[NMAX];
+    uint64_t fin = 0;
+#pragma unroll
+    for (int r = 0; r < NMAX; ++r) {
+        x[r] = kind == C3_EV_F32 ? (double)__uint_as_float((uint32_t)bits[r])
+                                 : __longlong_as_double((long long)bits[r]);
+        const bool f = r < R && __builtin_isfinite(x[r]);
+        fin |= (uint64_t)f << r;
+        s[r] = f ? x[r] : inf;      // excluded values sort after every finite one
+    }
+    const uint64_t valid = R == 64 ? ~0ull : ((1ull << R) - 1);
+    const uint64_t nonfin = valid & ~fin;
+    const int nf = __builtin_popcountll(fin);
+    UnitVote v;
+    if (2 * nf <= R) {
+        v.status = C3_INCONCLUSIVE;
+        v.bitmap = 0;
+        v.majority = -1;
+        return v;
+    }
+    bitonic_sort<NMAX>(s);
+    const double m = median_sorted<NMAX>(s, nf);
+    double dev[NMAX], ds[NMAX];
+#pragma unroll
+    for (int r = 0; r < NMAX; ++r) {
+        dev[r] = ((fin >> r) & 1ull) ? fabs(x[r] - m) : inf;
+        ds[r] = dev[r];
+    }
+    bitonic_sort<NMAX>(ds);
+    double d = median_sorted<NMAX>(ds, nf);
+    if (d == 0.0) {
+        const double q3 = quantile7_sorted<NMAX>(s, nf, 0.75);
+        const double q1 = quantile7_sorted<NMAX>(s, nf, 0.25);
+        d = (q3 - q1) * 0.5;
+    }
+    if (d == 0.0) d = (pick<NMAX>(s, nf - 1) - s[0]) / (double)nf;
+    uint64_t B = nonfin;
+    if (d != 0.0) {
+        const double thr = kappa * d;
+#pragma unroll
+        for (int r = 0; r < NMAX; ++r)
+            if (((fin >> r) & 1ull) && dev[r] > thr) B |= 1ull << r;
+    }
+    // lower-median replica: stable position (nf - 1) / 2 in (value, replica) order
+    const double target = pick<NMAX>(s, (nf - 1) / 2);
+    int want = (nf - 1) / 2;
+#pragma unroll
+    for (int r = 0; r < NMAX; ++r) want -= (((fin >> r) & 1ull) && x[r] < target) ? 1 : 0;
+    int med = -1;
+#pragma unroll
+    for (int r = 0; r < NMAX; ++r) {
+        if (((fin >> r) & 1ull) && x[r] == target) {
+            if (want == 0 && med < 0) med = r;
+            --want;
+        }
+    }
+    v.status = B ? C3_ATTRIBUTED : C3_AGREE;
+    v.bitmap = B;
+    v.majority = med;
+    return v;
+}
+
+}  // namespace c3
