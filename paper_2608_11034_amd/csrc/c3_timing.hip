@@ -24,7 +24,7 @@ constexpr int kPrefetch = 8;       // mask segments fetched at once per lane
 // functions of c3_vote_row.h.  Outlier bits also go to the per-rank masks
 // [segment][r][g] (bit t mod 32 of word t / 32) by atomic OR; they are
 // sparse, so the atomics cost little, and the masks must start zeroed.
-template <int NMAX, int MODE>
+template <int NMAX, int MODE, int KIND>
 __global__ void __launch_bounds__(kVoteThreads) timing_vote_kernel(
     const char* __restrict__ ev, int kind, int R, int64_t G, int64_t n_units, double kappa,
     bool dense, uint8_t* __restrict__ status, uint64_t* __restrict__ bitmap,
@@ -35,7 +35,7 @@ __global__ void __launch_bounds__(kVoteThreads) timing_vote_kernel(
     uint64_t e[NMAX];
     load_row_bits<NMAX>(ev + u * R * vsize, kind, vsize, R, dense, e);
     const UnitVote v = MODE == C3_EXACT ? exact_vote_row<NMAX>(e, R)
-                                        : statistical_vote_row<NMAX>(e, kind, R, kappa);
+                                        : statistical_vote_row<NMAX, KIND>(e, R, kappa);
     if (status != nullptr) {
         status[u] = v.status;
         bitmap[u] = v.bitmap;
@@ -196,7 +196,7 @@ int64_t timing_masks_bytes(int R, int64_t G, int64_t T) {
     return 2 * ((n_seg * R * G * 4 + 255) / 256 * 256);
 }
 
-template <int NMAX, int MODE>
+template <int NMAX, int MODE, int KIND>
 static hipError_t launch_vote(const char* ev, int kind, int R, int64_t G, int64_t n_units,
                               double kappa, uint8_t* status, uint64_t* bitmap, int32_t* majority,
                               uint32_t* masks, hipStream_t stream) {
@@ -205,7 +205,7 @@ static hipError_t launch_vote(const char* ev, int kind, int R, int64_t G, int64_
     const bool dense = (R * vsize) % 16 == 0 && ((uintptr_t)ev & 15) == 0;
     if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
     if (blocks == 0) return hipSuccess;
-    hipLaunchKernelGGL((timing_vote_kernel<NMAX, MODE>), dim3((unsigned)blocks), dim3(kVoteThreads),
+    hipLaunchKernelGGL((timing_vote_kernel<NMAX, MODE, KIND>), dim3((unsigned)blocks), dim3(kVoteThreads),
                        0, stream, ev, kind, R, G, n_units, kappa, dense, status, bitmap, majority,
                        masks);
     return hipGetLastError();
@@ -216,11 +216,15 @@ static hipError_t launch_votes(const uint64_t* fp, const char* tp, int time_kind
                                int64_t n_units, double kappa, uint8_t* fs, uint64_t* fb,
                                int32_t* fmj, uint8_t* ts, uint64_t* tb, int32_t* tmj,
                                uint32_t* fm, uint32_t* tm, hipStream_t stream) {
-    hipError_t e = launch_vote<NMAX, C3_EXACT>(reinterpret_cast<const char*>(fp), C3_EV_U64, R, G,
-                                               n_units, kappa, fs, fb, fmj, fm, stream);
+    hipError_t e = launch_vote<NMAX, C3_EXACT, C3_EV_U64>(reinterpret_cast<const char*>(fp),
+                                                          C3_EV_U64, R, G, n_units, kappa, fs, fb,
+                                                          fmj, fm, stream);
     if (e != hipSuccess) return e;
-    return launch_vote<NMAX, C3_STATISTICAL>(tp, time_kind, R, G, n_units, kappa, ts, tb, tmj, tm,
-                                             stream);
+    if (time_kind == C3_EV_F32)
+        return launch_vote<NMAX, C3_STATISTICAL, C3_EV_F32>(tp, time_kind, R, G, n_units, kappa, ts,
+                                                            tb, tmj, tm, stream);
+    return launch_vote<NMAX, C3_STATISTICAL, C3_EV_F64>(tp, time_kind, R, G, n_units, kappa, ts, tb,
+                                                        tmj, tm, stream);
 }
 
 hipError_t launch_timing_consensus(const uint64_t* fp, const void* times, int time_kind, int R,

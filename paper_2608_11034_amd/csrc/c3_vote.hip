@@ -187,7 +187,7 @@ __global__ void __launch_bounds__(kVoteThreads) exact_vote_small_kernel(
     majority_idx[u] = v.majority;
 }
 
-template <int NMAX>
+template <int NMAX, int KIND>
 __global__ void __launch_bounds__(kVoteThreads) statistical_vote_small_kernel(
     const char* __restrict__ ev, int kind, int64_t rstride, int64_t ustride, int R, int64_t n_units,
     bool dense, double kappa, uint8_t* __restrict__ status, uint64_t* __restrict__ bitmap,
@@ -196,7 +196,7 @@ __global__ void __launch_bounds__(kVoteThreads) statistical_vote_small_kernel(
     if (u >= n_units) return;
     uint64_t bits[NMAX];
     load_row_bits<NMAX>(ev + u * ustride, kind, rstride, R, dense, bits);
-    const UnitVote v = statistical_vote_row<NMAX>(bits, kind, R, kappa);
+    const UnitVote v = statistical_vote_row<NMAX, KIND>(bits, R, kappa);
     status[u] = v.status;
     bitmap[u] = v.bitmap;
     majority_idx[u] = v.majority;
@@ -213,10 +213,14 @@ static void launch_small(const char* ev, int kind, int64_t rstride, int64_t ustr
         hipLaunchKernelGGL(exact_vote_small_kernel<NMAX>, dim3(blocks), dim3(kVoteThreads), 0, stream,
                            ev, kind, rstride, ustride, R, n_units, dense, status, bitmap,
                            majority_idx);
+    else if (kind == C3_EV_F32)
+        hipLaunchKernelGGL((statistical_vote_small_kernel<NMAX, C3_EV_F32>), dim3(blocks),
+                           dim3(kVoteThreads), 0, stream, ev, kind, rstride, ustride, R, n_units,
+                           dense, kappa, status, bitmap, majority_idx);
     else
-        hipLaunchKernelGGL(statistical_vote_small_kernel<NMAX>, dim3(blocks), dim3(kVoteThreads), 0,
-                           stream, ev, kind, rstride, ustride, R, n_units, dense, kappa, status,
-                           bitmap, majority_idx);
+        hipLaunchKernelGGL((statistical_vote_small_kernel<NMAX, C3_EV_F64>), dim3(blocks),
+                           dim3(kVoteThreads), 0, stream, ev, kind, rstride, ustride, R, n_units,
+                           dense, kappa, status, bitmap, majority_idx);
 }
 
 hipError_t launch_consensus(const void* evidence, int kind, int64_t rstride, int64_t ustride, int R,

@@ -17,6 +17,8 @@
 // exactly as the plain definition does.
 #pragma once
 
+#include <type_traits>
+
 #include "c3_device.h"
 
 namespace c3 {
@@ -93,8 +95,13 @@ __device__ __forceinline__ UnitVote exact_vote_row(const uint64_t (&e)[NMAX], in
 
 // Bitonic sorting network over N register slots (N a power of two, values
 // without NaN): each comparator is one min and one max.
-template <int N>
-__device__ __forceinline__ void bitonic_sort(double (&v)[N]) {
+__device__ __forceinline__ float vmin(float a, float b) { return fminf(a, b); }
+__device__ __forceinline__ float vmax(float a, float b) { return fmaxf(a, b); }
+__device__ __forceinline__ double vmin(double a, double b) { return fmin(a, b); }
+__device__ __forceinline__ double vmax(double a, double b) { return fmax(a, b); }
+
+template <int N, typename V>
+__device__ __forceinline__ void bitonic_sort(V (&v)[N]) {
     constexpr int LOG = N == 2 ? 1 : N == 4 ? 2 : N == 8 ? 3 : 4;
     static_assert((1 << LOG) == N, "power of two up to 16");
 #pragma unroll
@@ -105,7 +112,7 @@ __device__ __forceinline__ void bitonic_sort(double (&v)[N]) {
             for (int i = 0; i < N; ++i) {
                 const int l = i ^ (1 << jj);
                 if (l > i) {
-                    const double lo = fmin(v[i], v[l]), hi = fmax(v[i], v[l]);
+                    const V lo = vmin(v[i], v[l]), hi = vmax(v[i], v[l]);
                     const bool up = (i & (1 << kk)) == 0;
                     v[i] = up ? lo : hi;
                     v[l] = up ? hi : lo;
@@ -115,70 +122,61 @@ __device__ __forceinline__ void bitonic_sort(double (&v)[N]) {
     }
 }
 
+__device__ __forceinline__ uint32_t vbits(float x) { return __float_as_uint(x); }
+__device__ __forceinline__ uint64_t vbits(double x) { return (uint64_t)__double_as_longlong(x); }
+__device__ __forceinline__ float vfrom(uint32_t b, float) { return __uint_as_float(b); }
+__device__ __forceinline__ double vfrom(uint64_t b, double) { return __longlong_as_double((long long)b); }
+
 // v[k] for a run-time k, as an OR of masked slots.  A select chain would be
 // turned back into an indexed load, which puts the array in scratch memory.
-template <int N>
-__device__ __forceinline__ double pick(const double (&v)[N], int k) {
-    uint64_t out = 0;
+// With a compile-time k the loop folds to the one slot.
+template <int N, typename V>
+__device__ __forceinline__ V pick(const V (&v)[N], int k) {
+    decltype(vbits(v[0])) out = 0;
 #pragma unroll
     for (int i = 0; i < N; ++i) {
-        const uint64_t m = 0ull - (uint64_t)(i == k);
-        out |= m & (uint64_t)__double_as_longlong(v[i]);
+        const decltype(out) m = (decltype(out))0 - (decltype(out))(i == k);
+        out |= m & vbits(v[i]);
     }
-    return __longlong_as_double((long long)out);
+    return vfrom(out, v[0]);
 }
 
-template <int N>
-__device__ __forceinline__ double median_sorted(const double (&s)[N], int n) {
-    if (n & 1) return pick<N>(s, (n - 1) / 2);
-    return (pick<N>(s, n / 2 - 1) + pick<N>(s, n / 2)) * 0.5;
+// Median of the n smallest slots of s (sorted), in fp64.
+template <int N, typename V>
+__device__ __forceinline__ double median_sorted(const V (&s)[N], int n) {
+    if (n & 1) return (double)pick<N>(s, (n - 1) / 2);
+    return ((double)pick<N>(s, n / 2 - 1) + (double)pick<N>(s, n / 2)) * 0.5;
 }
 
-template <int N>
-__device__ __forceinline__ double quantile7_sorted(const double (&s)[N], int n, double p) {
+// Type-7 quantile p of the n smallest slots of s (sorted), in fp64.
+template <int N, typename V>
+__device__ __forceinline__ double quantile7_sorted(const V (&s)[N], int n, double p) {
     const double h = (double)(n - 1) * p;
     const double fl = floor(h);
     const int lo = (int)fl;
     const double frac = h - fl;
-    if (lo + 1 >= n) return pick<N>(s, n - 1);
-    const double a = pick<N>(s, lo);
-    const double b = pick<N>(s, lo + 1);
+    if (lo + 1 >= n) return (double)pick<N>(s, n - 1);
+    const double a = (double)pick<N>(s, lo);
+    const double b = (double)pick<N>(s, lo + 1);
     const double diff = b - a;
     const double prod = frac * diff;
     return a + prod;
 }
 
-// `bits` hold fp32 (kind C3_EV_F32, zero-extended) or fp64 patterns.
-template <int NMAX>
-__device__ __forceinline__ UnitVote statistical_vote_row(const uint64_t (&bits)[NMAX], int kind,
-                                                         int R, double kappa) {
+// Everything after the first sort.  NC > 0 fixes the finite count at
+// compile time (every value finite and R == NMAX, the usual case), so every
+// order statistic is a plain register.
+template <int NMAX, int NC, typename V>
+__device__ __forceinline__ UnitVote statistical_tail(const V (&x)[NMAX], const V (&s)[NMAX],
+                                                     uint64_t fin, uint64_t nonfin, int nf_rt,
+                                                     double kappa) {
     const double inf = __builtin_huge_val();
-    double x[NMAX], s[NMAX];
-    uint64_t fin = 0;
-#pragma unroll
-    for (int r = 0; r < NMAX; ++r) {
-        x[r] = kind == C3_EV_F32 ? (double)__uint_as_float((uint32_t)bits[r])
-                                 : __longlong_as_double((long long)bits[r]);
-        const bool f = r < R && __builtin_isfinite(x[r]);
-        fin |= (uint64_t)f << r;
-        s[r] = f ? x[r] : inf;      // excluded values sort after every finite one
-    }
-    const uint64_t valid = R == 64 ? ~0ull : ((1ull << R) - 1);
-    const uint64_t nonfin = valid & ~fin;
-    const int nf = __builtin_popcountll(fin);
-    UnitVote v;
-    if (2 * nf <= R) {
-        v.status = C3_INCONCLUSIVE;
-        v.bitmap = 0;
-        v.majority = -1;
-        return v;
-    }
-    bitonic_sort<NMAX>(s);
+    const int nf = NC > 0 ? NC : nf_rt;
     const double m = median_sorted<NMAX>(s, nf);
     double dev[NMAX], ds[NMAX];
 #pragma unroll
     for (int r = 0; r < NMAX; ++r) {
-        dev[r] = ((fin >> r) & 1ull) ? fabs(x[r] - m) : inf;
+        dev[r] = ((fin >> r) & 1ull) ? fabs((double)x[r] - m) : inf;
         ds[r] = dev[r];
     }
     bitonic_sort<NMAX>(ds);
@@ -188,7 +186,7 @@ __device__ __forceinline__ UnitVote statistical_vote_row(const uint64_t (&bits)[
         const double q1 = quantile7_sorted<NMAX>(s, nf, 0.25);
         d = (q3 - q1) * 0.5;
     }
-    if (d == 0.0) d = (pick<NMAX>(s, nf - 1) - s[0]) / (double)nf;
+    if (d == 0.0) d = ((double)pick<NMAX>(s, nf - 1) - (double)s[0]) / (double)nf;
     uint64_t B = nonfin;
     if (d != 0.0) {
         const double thr = kappa * d;
@@ -197,7 +195,7 @@ __device__ __forceinline__ UnitVote statistical_vote_row(const uint64_t (&bits)[
             if (((fin >> r) & 1ull) && dev[r] > thr) B |= 1ull << r;
     }
     // lower-median replica: stable position (nf - 1) / 2 in (value, replica) order
-    const double target = pick<NMAX>(s, (nf - 1) / 2);
+    const V target = pick<NMAX>(s, (nf - 1) / 2);
     int want = (nf - 1) / 2;
 #pragma unroll
     for (int r = 0; r < NMAX; ++r) want -= (((fin >> r) & 1ull) && x[r] < target) ? 1 : 0;
@@ -209,10 +207,43 @@ __device__ __forceinline__ UnitVote statistical_vote_row(const uint64_t (&bits)[
             --want;
         }
     }
+    UnitVote v;
     v.status = B ? C3_ATTRIBUTED : C3_AGREE;
     v.bitmap = B;
     v.majority = med;
     return v;
+}
+
+// `bits` hold the fp32 (KIND == C3_EV_F32, zero-extended) or fp64 patterns.
+// fp32 values are ordered and compared in fp32 (exact: the conversion to
+// fp64 is monotonic and exact); every arithmetic step is fp64.
+template <int NMAX, int KIND>
+__device__ __forceinline__ UnitVote statistical_vote_row(const uint64_t (&bits)[NMAX], int R,
+                                                         double kappa) {
+    using V = typename std::conditional<KIND == C3_EV_F32, float, double>::type;
+    V x[NMAX], s[NMAX];
+    uint64_t fin = 0;
+#pragma unroll
+    for (int r = 0; r < NMAX; ++r) {
+        if constexpr (KIND == C3_EV_F32) x[r] = __uint_as_float((uint32_t)bits[r]);
+        else x[r] = __longlong_as_double((long long)bits[r]);
+        const bool f = r < R && __builtin_isfinite(x[r]);
+        fin |= (uint64_t)f << r;
+        s[r] = f ? x[r] : (V)__builtin_huge_val();   // excluded values sort last
+    }
+    const uint64_t valid = R == 64 ? ~0ull : ((1ull << R) - 1);
+    const uint64_t nonfin = valid & ~fin;
+    const int nf = __builtin_popcountll(fin);
+    if (2 * nf <= R) {
+        UnitVote v;
+        v.status = C3_INCONCLUSIVE;
+        v.bitmap = 0;
+        v.majority = -1;
+        return v;
+    }
+    bitonic_sort<NMAX>(s);
+    if (nf == NMAX) return statistical_tail<NMAX, NMAX>(x, s, fin, nonfin, nf, kappa);
+    return statistical_tail<NMAX, 0>(x, s, fin, nonfin, nf, kappa);
 }
 
 }  // namespace c3
