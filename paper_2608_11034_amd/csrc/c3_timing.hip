@@ -66,8 +66,9 @@ __global__ void __launch_bounds__(256) timing_zero_kernel(uint4* __restrict__ p,
 // counts if q < len, closes this lane's pair (t - 1, t) if 1 <= q <= len,
 // and ends window [t - Wt + 1, t], this lane's if Wt - 1 <= q < len + Wt - 1.
 // With Wt <= 32 the window ending at bit i of a segment is a 32-bit field
-// of the 64 bits (segment : previous segment); longer windows keep a 64-bit
-// shift register.  Segments whose window bits are all zero are skipped.
+// of the 64 bits (segment : previous segment), evaluated only where a set
+// bit enters; longer windows keep a 64-bit shift register.  Segments whose
+// set bits cannot raise the maximum or reach the threshold are skipped.
 template <bool SHORT>
 __global__ void __launch_bounds__(kConfirmThreads) timing_confirm_kernel(
     const uint32_t* __restrict__ fp_masks, const uint32_t* __restrict__ t_masks, int R, int64_t G,
@@ -83,7 +84,9 @@ __global__ void __launch_bounds__(kConfirmThreads) timing_confirm_kernel(
     const int64_t t_lo = s_lo * kSegIters;
     int64_t t_hi = t_lo + per * kSegIters;
     if (t_hi > T) t_hi = T;
-    int64_t t_end = t_hi + Wt - 1;            // last window starting before t_hi ends here
+    // Read on to where the last window starting before t_hi ends, and at
+    // least one iteration past t_hi for the pair (t_hi - 1, t_hi).
+    int64_t t_end = t_hi + (Wt > 1 ? Wt - 1 : 1);
     if (t_end > T) t_end = T;
     uint32_t flags = 0, dc = 0, sc = 0, mw = 0;
     int32_t fd = -1, fw = -1;
@@ -133,20 +136,25 @@ __global__ void __launch_bounds__(kConfirmThreads) timing_confirm_kernel(
                 const uint32_t ybits = (uint32_t)__builtin_popcount(tm) + __builtin_popcount(prev);
                 if (SHORT) {
                     if ((ybits > mw || (2u * ybits > (uint32_t)Wt && fw < 0)) && lo_i < hi_i) {
+                        // A window count only grows when a set bit enters, so
+                        // the maximum and the first window over the threshold
+                        // end at a set bit -- or at the lane's first window
+                        // end, whose count owes nothing to entering bits.
                         const uint64_t y = ((uint64_t)tm << 32) | prev;
                         const uint32_t wm = (uint32_t)wmask;
-                        uint32_t over = 0, smax = 0;
-#pragma unroll 4
-                        for (uint32_t i = 0; i < (uint32_t)kSegIters; ++i) {
+                        const uint32_t range = (hi_i >= 32u ? ~0u : (1u << hi_i) - 1u) &
+                                               ~((1u << lo_i) - 1u);
+                        uint32_t ev = tm & range;
+                        if (wlo >= q0 && wlo - q0 < n) ev |= 1u << (wlo - q0);
+                        while (ev != 0u) {
+                            const uint32_t i = (uint32_t)__builtin_ctz(ev);
+                            ev &= ev - 1u;
                             const uint32_t c = (uint32_t)__builtin_popcount(
                                 (uint32_t)(y >> (33u + i - (uint32_t)Wt)) & wm);
-                            const bool ok = i >= lo_i && i < hi_i;
-                            smax = ok && c > smax ? c : smax;
-                            over |= (ok && 2u * c > (uint32_t)Wt) ? (1u << i) : 0u;
+                            mw = c > mw ? c : mw;
+                            if (2u * c > (uint32_t)Wt && fw < 0)
+                                fw = (int32_t)(t_lo + (int64_t)(q0 + i - wlo));
                         }
-                        mw = smax > mw ? smax : mw;
-                        if (over != 0u && fw < 0)
-                            fw = (int32_t)(t_lo + (int64_t)(q0 + __builtin_ctz(over) - wlo));
                     }
                 } else {
                     if ((tm != 0u || hist != 0ull)) {

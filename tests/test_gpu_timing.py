@@ -93,6 +93,7 @@ CASES = [
     (3, 63, 40, 5, False), (4, 1, 1, 16, False), (1, 7, 33, 3, False), (2, 70, 31, 1, True),
     (5, 64, 64, 64, False), (7, 66, 90, 64, True), (8, 20, 129, 63, False),
     (9, 64, 16, 16, False), (13, 33, 41, 16, True), (16, 64, 24, 8, False), (16, 3, 9, 64, False),
+    (4, 66, 300, 1, False), (6, 9, 700, 2, True),   # several lanes per rank, short windows
     (20, 40, 50, 16, False),                 # R > 16: separate steps
     (8, 50, 120, 80, False),                 # W > 64: separate steps
 ]
@@ -110,6 +111,24 @@ def test_timing_consensus_without_per_unit_outputs(R, G, T, W):
     _case("timing verdicts only", R, G, T, W)
     fp, tau = _inputs(R, G, T, seed=R + G + T)
     _check(fp, tau, W, per_unit=False)
+
+
+@pytest.mark.parametrize("W", [1, 2, 16])
+@pytest.mark.parametrize("t0", [31, 63, 64, 127, 255])
+def test_timing_consensus_pair_across_lane_boundary(W, t0):
+    # T = 300 splits into lanes of 64 iterations: slowness at t0 and t0 + 1
+    # straddles a lane boundary when t0 + 1 is a multiple of 64.
+    _case("timing pair", W, t0)
+    R, G, T = 8, 3, 300
+    rng = np.random.default_rng(t0 * 10 + W)
+    fp = np.repeat(rng.integers(-(2 ** 63), 2 ** 63 - 1, size=(T, G, 1), dtype=np.int64), R,
+                   axis=2)
+    tau = np.exp(rng.normal(0.0, 0.01, size=(T, G, R))).astype(np.float32)
+    tau[t0:t0 + 2, 1, 5] = 4.0
+    v = _check(fp, tau, W)
+    rank = 5 * G + 1
+    assert v["flags"][rank] & c3.RANK_CONSEC2
+    assert v["slow_count"][rank] >= 2
 
 
 def test_timing_consensus_argument_errors():
