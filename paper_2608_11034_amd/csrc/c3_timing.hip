@@ -19,37 +19,64 @@ constexpr int kConfirmThreads = 256;
 constexpr int kConfirmLanes = 8;   // lanes per rank in the confirmation
 constexpr int kPrefetch = 8;       // mask segments fetched at once per lane
 
-// One evidence kind per launch, one thread per unit u = t * G + g (a wave
-// reads 64 consecutive rows, fully coalesced), deciding with the per-unit
-// functions of c3_vote_row.h.  Outlier bits also go to the per-rank masks
-// [segment][r][g] (bit t mod 32 of word t / 32) by atomic OR; they are
-// sparse, so the atomics cost little, and the masks must start zeroed.
+// Per-unit outputs of one evidence kind (status null: none) and its masks.
+struct VoteOut {
+    uint8_t* status;
+    uint64_t* bitmap;
+    int32_t* majority;
+    uint32_t* masks;
+};
+
+// One thread per unit u = t * G + g (a wave reads 64 consecutive rows, fully
+// coalesced), deciding with the per-unit functions of c3_vote_row.h.
+// Outlier bits also go to the per-rank masks [segment][r][g] (bit t mod 32
+// of word t / 32) by atomic OR; they are sparse, so the atomics cost little,
+// and the masks must start zeroed.
 template <int NMAX, int MODE, int KIND>
-__global__ void __launch_bounds__(kVoteThreads) timing_vote_kernel(
-    const char* __restrict__ ev, int kind, int R, int64_t G, int64_t n_units, double kappa,
-    bool dense, uint8_t* __restrict__ status, uint64_t* __restrict__ bitmap,
-    int32_t* __restrict__ majority, uint32_t* __restrict__ masks) {
-    const int64_t u = (int64_t)blockIdx.x * kVoteThreads + threadIdx.x;
-    if (u >= n_units) return;
-    const int64_t vsize = (kind == C3_EV_U64 || kind == C3_EV_F64) ? 8 : 4;
+__device__ __forceinline__ void vote_unit(const char* __restrict__ ev, int R, int64_t G,
+                                          int64_t n_units, double kappa, bool dense,
+                                          const VoteOut& o, int64_t ub) {
+    constexpr int vsize = (KIND == C3_EV_U64 || KIND == C3_EV_F64) ? 8 : 4;
+    const int64_t u = ub * kVoteThreads + threadIdx.x;
+    // the workgroup's rows start at a uniform offset; the lane's offset
+    // within them fits 32 bits
+    const char* row = ev + ub * kVoteThreads * R * vsize + (uint32_t)(threadIdx.x * R * vsize);
     uint64_t e[NMAX];
-    load_row_bits<NMAX>(ev + u * R * vsize, kind, vsize, R, dense, e);
+    load_row_bits<NMAX>(row, KIND, vsize, R, dense, e);
     const UnitVote v = MODE == C3_EXACT ? exact_vote_row<NMAX>(e, R)
                                         : statistical_vote_row<NMAX, KIND>(e, R, kappa);
-    if (status != nullptr) {
-        status[u] = v.status;
-        bitmap[u] = v.bitmap;
-        majority[u] = v.majority;
+    if (o.status != nullptr) {
+        o.status[u] = v.status;
+        o.bitmap[u] = v.bitmap;
+        o.majority[u] = v.majority;
     }
     if (v.bitmap != 0ull) {
         // 32-bit division when the unit count allows it (uniform per launch)
         const int64_t t = n_units <= 0xFFFFFFFFll ? (int64_t)((uint32_t)u / (uint32_t)G) : u / G;
         const int64_t g = u - t * G;
         const uint32_t bit = 1u << (t & (kSegIters - 1));
-        uint32_t* m = masks + (t / kSegIters) * R * G + g;
+        uint32_t* m = o.masks + (t / kSegIters) * R * G + g;
         for (uint64_t b = v.bitmap; b != 0ull; b &= b - 1ull)
             atomicOr(m + (int64_t)__builtin_ctzll(b) * G, bit);
     }
+}
+
+// Both votes in one launch, so every CU overlaps the exact vote (waits on
+// memory) with the statistical one (VALU-bound).  Workgroups go to the 8
+// XCDs round-robin, so the kind alternates every 8 workgroups:
+// b = 16 q + 8 k + x votes kind k (0 fingerprints, 1 step times) on unit
+// block 8 q + x.
+template <int NMAX, int KIND>
+__global__ void __launch_bounds__(kVoteThreads) timing_votes_kernel(
+    const char* __restrict__ fp, const char* __restrict__ tp, int R, int64_t G, int64_t n_units,
+    double kappa, bool fp_dense, bool t_dense, VoteOut fo, VoteOut to) {
+    const uint32_t b = blockIdx.x;
+    const int64_t ub = (int64_t)(((b >> 4) << 3) | (b & 7u));
+    if (ub * kVoteThreads + threadIdx.x >= n_units) return;
+    if ((b & 8u) == 0u)
+        vote_unit<NMAX, C3_EXACT, C3_EV_U64>(fp, R, G, n_units, kappa, fp_dense, fo, ub);
+    else
+        vote_unit<NMAX, C3_STATISTICAL, KIND>(tp, R, G, n_units, kappa, t_dense, to, ub);
 }
 
 // Clears n16 16-byte words (the mask area is a multiple of 256 bytes).
@@ -204,35 +231,29 @@ int64_t timing_masks_bytes(int R, int64_t G, int64_t T) {
     return 2 * ((n_seg * R * G * 4 + 255) / 256 * 256);
 }
 
-template <int NMAX, int MODE, int KIND>
-static hipError_t launch_vote(const char* ev, int kind, int R, int64_t G, int64_t n_units,
-                              double kappa, uint8_t* status, uint64_t* bitmap, int32_t* majority,
-                              uint32_t* masks, hipStream_t stream) {
-    const int64_t blocks = (n_units + kVoteThreads - 1) / kVoteThreads;
-    const int64_t vsize = (kind == C3_EV_U64 || kind == C3_EV_F64) ? 8 : 4;
-    const bool dense = (R * vsize) % 16 == 0 && ((uintptr_t)ev & 15) == 0;
+template <int NMAX, int KIND>
+static hipError_t launch_votes(const uint64_t* fp, const char* tp, int R, int64_t G,
+                               int64_t n_units, double kappa, const VoteOut& fo, const VoteOut& to,
+                               hipStream_t stream) {
+    const int64_t blocks = 2 * (((n_units + kVoteThreads - 1) / kVoteThreads + 7) / 8 * 8);
+    constexpr int64_t tsize = KIND == C3_EV_F64 ? 8 : 4;
+    const bool fp_dense = (R * 8) % 16 == 0 && ((uintptr_t)fp & 15) == 0;
+    const bool t_dense = (R * tsize) % 16 == 0 && ((uintptr_t)tp & 15) == 0;
     if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
     if (blocks == 0) return hipSuccess;
-    hipLaunchKernelGGL((timing_vote_kernel<NMAX, MODE, KIND>), dim3((unsigned)blocks), dim3(kVoteThreads),
-                       0, stream, ev, kind, R, G, n_units, kappa, dense, status, bitmap, majority,
-                       masks);
+    hipLaunchKernelGGL((timing_votes_kernel<NMAX, KIND>), dim3((unsigned)blocks),
+                       dim3(kVoteThreads), 0, stream, reinterpret_cast<const char*>(fp), tp, R, G,
+                       n_units, kappa, fp_dense, t_dense, fo, to);
     return hipGetLastError();
 }
 
 template <int NMAX>
 static hipError_t launch_votes(const uint64_t* fp, const char* tp, int time_kind, int R, int64_t G,
-                               int64_t n_units, double kappa, uint8_t* fs, uint64_t* fb,
-                               int32_t* fmj, uint8_t* ts, uint64_t* tb, int32_t* tmj,
-                               uint32_t* fm, uint32_t* tm, hipStream_t stream) {
-    hipError_t e = launch_vote<NMAX, C3_EXACT, C3_EV_U64>(reinterpret_cast<const char*>(fp),
-                                                          C3_EV_U64, R, G, n_units, kappa, fs, fb,
-                                                          fmj, fm, stream);
-    if (e != hipSuccess) return e;
+                               int64_t n_units, double kappa, const VoteOut& fo, const VoteOut& to,
+                               hipStream_t stream) {
     if (time_kind == C3_EV_F32)
-        return launch_vote<NMAX, C3_STATISTICAL, C3_EV_F32>(tp, time_kind, R, G, n_units, kappa, ts,
-                                                            tb, tmj, tm, stream);
-    return launch_vote<NMAX, C3_STATISTICAL, C3_EV_F64>(tp, time_kind, R, G, n_units, kappa, ts, tb,
-                                                        tmj, tm, stream);
+        return launch_votes<NMAX, C3_EV_F32>(fp, tp, R, G, n_units, kappa, fo, to, stream);
+    return launch_votes<NMAX, C3_EV_F64>(fp, tp, R, G, n_units, kappa, fo, to, stream);
 }
 
 hipError_t launch_timing_consensus(const uint64_t* fp, const void* times, int time_kind, int R,
@@ -259,16 +280,15 @@ hipError_t launch_timing_consensus(const uint64_t* fp, const void* times, int ti
     }
     const char* tp = static_cast<const char*>(times);
     const int64_t n_units = T * G;
+    const VoteOut fo = {fp_status, fp_bitmap, fp_majority, fm};
+    const VoteOut to = {t_status, t_bitmap, t_majority, tm};
     hipError_t e;
     if (R <= 4)
-        e = launch_votes<4>(fp, tp, time_kind, R, G, n_units, kappa, fp_status, fp_bitmap,
-                            fp_majority, t_status, t_bitmap, t_majority, fm, tm, stream);
+        e = launch_votes<4>(fp, tp, time_kind, R, G, n_units, kappa, fo, to, stream);
     else if (R <= 8)
-        e = launch_votes<8>(fp, tp, time_kind, R, G, n_units, kappa, fp_status, fp_bitmap,
-                            fp_majority, t_status, t_bitmap, t_majority, fm, tm, stream);
+        e = launch_votes<8>(fp, tp, time_kind, R, G, n_units, kappa, fo, to, stream);
     else
-        e = launch_votes<16>(fp, tp, time_kind, R, G, n_units, kappa, fp_status, fp_bitmap,
-                             fp_majority, t_status, t_bitmap, t_majority, fm, tm, stream);
+        e = launch_votes<16>(fp, tp, time_kind, R, G, n_units, kappa, fo, to, stream);
     if (e != hipSuccess) return e;
     const int Wt = (int64_t)window < T ? window : (int)T;
     const int64_t threads = ranks * kConfirmLanes;

@@ -3,13 +3,14 @@
 // kernels (c3_vote.hip) and the fused timing-consensus kernel
 // (c3_timing.hip), so both decide every unit with the same code.
 //
-// EXACT (Sec. 5.3): each replica counts the peers equal to it; a strict
-// majority exists iff some count c satisfies 2c > R, the majority replicas
-// are exactly those, the bitmap marks the others and the majority index is
-// the lowest majority replica.
+// EXACT (Sec. 5.3): a strict majority exists iff some value is held by
+// more than R / 2 replicas; those are the majority, the bitmap marks the
+// others and the majority index is the lowest majority replica.  The value
+// is found with R compares against replica 0 in the usual case, else with a
+// Boyer-Moore pass.
 //
-// STATISTICAL (Sec. 5.4), in fp64: order statistics from min/max bitonic
-// sorting networks over the finite values (non-finite ones sort last and are
+// STATISTICAL (Sec. 5.4), in fp64: order statistics from min/max sorting
+// networks over the finite values (non-finite ones sort last and are
 // outliers), RobustScale in the order MAD -> IQR / 2 (type-7 quartiles) ->
 // range / n_finite, strict |x - m| > kappa d, and the lower-median replica in
 // the stable (value, replica) order.  Files including this header are
@@ -69,53 +70,73 @@ __device__ __forceinline__ void load_row_bits(const char* base, int kind, int64_
 }
 
 template <int NMAX>
-__device__ __forceinline__ UnitVote exact_vote_row(const uint64_t (&e)[NMAX], int R) {
-    uint64_t maj = 0, other = 0;
+__device__ __forceinline__ uint64_t equal_mask(const uint64_t (&e)[NMAX], int R, uint64_t v) {
+    uint64_t m = 0;
 #pragma unroll
-    for (int r = 0; r < NMAX; ++r) {
+    for (int r = 0; r < NMAX; ++r) m |= (uint64_t)(r < R && e[r] == v) << r;
+    return m;
+}
+
+// A strict majority value, if any, is unique, so the majority replicas are
+// the holders of one candidate value.  The candidate is replica 0's value
+// when that already has a majority (the usual case: one pass of R
+// compares); otherwise the Boyer-Moore majority candidate, which is the
+// majority value whenever there is one.
+template <int NMAX>
+__device__ __forceinline__ UnitVote exact_vote_row(const uint64_t (&e)[NMAX], int R) {
+    uint64_t maj = equal_mask<NMAX>(e, R, e[0]);
+    if (2 * __builtin_popcountll(maj) <= R) {
+        uint64_t cand = e[0];
         int cnt = 0;
 #pragma unroll
-        for (int j = 0; j < NMAX; ++j) cnt += (j < R && e[j] == e[r]) ? 1 : 0;
-        if (r < R) {
-            if (2 * cnt > R) maj |= 1ull << r; else other |= 1ull << r;
+        for (int r = 0; r < NMAX; ++r) {
+            if (r < R) {
+                if (cnt == 0) cand = e[r];
+                cnt += e[r] == cand ? 1 : -1;
+            }
         }
+        maj = equal_mask<NMAX>(e, R, cand);
     }
     UnitVote v;
-    if (maj == 0) {
+    if (2 * __builtin_popcountll(maj) <= R) {
         v.status = C3_INCONCLUSIVE;
         v.bitmap = 0;
         v.majority = -1;
     } else {
-        v.status = other ? C3_ATTRIBUTED : C3_AGREE;
-        v.bitmap = other;
+        const uint64_t valid = R == 64 ? ~0ull : ((1ull << R) - 1);
+        v.bitmap = valid & ~maj;
+        v.status = v.bitmap ? C3_ATTRIBUTED : C3_AGREE;
         v.majority = __builtin_ctzll(maj);
     }
     return v;
 }
 
-// Bitonic sorting network over N register slots (N a power of two, values
-// without NaN): each comparator is one min and one max.
+// Batcher's odd-even merge sort over N register slots (N a power of two,
+// values without NaN): 5, 19 and 63 comparators for 4, 8 and 16 slots, each
+// one min and one max.
 __device__ __forceinline__ float vmin(float a, float b) { return fminf(a, b); }
 __device__ __forceinline__ float vmax(float a, float b) { return fmaxf(a, b); }
 __device__ __forceinline__ double vmin(double a, double b) { return fmin(a, b); }
 __device__ __forceinline__ double vmax(double a, double b) { return fmax(a, b); }
 
 template <int N, typename V>
-__device__ __forceinline__ void bitonic_sort(V (&v)[N]) {
-    constexpr int LOG = N == 2 ? 1 : N == 4 ? 2 : N == 8 ? 3 : 4;
-    static_assert((1 << LOG) == N, "power of two up to 16");
+__device__ __forceinline__ void sort_network(V (&v)[N]) {
+    static_assert(N >= 2 && (N & (N - 1)) == 0, "power of two");
 #pragma unroll
-    for (int kk = 1; kk <= LOG; ++kk) {
+    for (int p = 1; p < N; p <<= 1) {
 #pragma unroll
-        for (int jj = kk - 1; jj >= 0; --jj) {
+        for (int k = p; k >= 1; k >>= 1) {
 #pragma unroll
-            for (int i = 0; i < N; ++i) {
-                const int l = i ^ (1 << jj);
-                if (l > i) {
-                    const V lo = vmin(v[i], v[l]), hi = vmax(v[i], v[l]);
-                    const bool up = (i & (1 << kk)) == 0;
-                    v[i] = up ? lo : hi;
-                    v[l] = up ? hi : lo;
+            for (int j = k % p; j <= N - 1 - k; j += 2 * k) {
+#pragma unroll
+                for (int i = 0; i < k && i < N - j - k; ++i) {
+                    // only pairs inside one block of 2p slots
+                    if ((i + j) / (2 * p) == (i + j + k) / (2 * p)) {
+                        const V lo = vmin(v[i + j], v[i + j + k]);
+                        const V hi = vmax(v[i + j], v[i + j + k]);
+                        v[i + j] = lo;
+                        v[i + j + k] = hi;
+                    }
                 }
             }
         }
@@ -173,14 +194,37 @@ __device__ __forceinline__ UnitVote statistical_tail(const V (&x)[NMAX], const V
     const double inf = __builtin_huge_val();
     const int nf = NC > 0 ? NC : nf_rt;
     const double m = median_sorted<NMAX>(s, nf);
-    double dev[NMAX], ds[NMAX];
+    double dev[NMAX];
 #pragma unroll
-    for (int r = 0; r < NMAX; ++r) {
-        dev[r] = ((fin >> r) & 1ull) ? fabs((double)x[r] - m) : inf;
-        ds[r] = dev[r];
+    for (int r = 0; r < NMAX; ++r) dev[r] = ((fin >> r) & 1ull) ? fabs((double)x[r] - m) : inf;
+    double d;
+    if constexpr (NC > 0) {
+        // m lies between the two middle sorted values, so the deviations of
+        // the values below it and of those above it are two ascending runs
+        // lo and hi of h each; the two middle deviations are order
+        // statistics h - 1 and h of their merge: the minimum, over the ways
+        // of taking i from lo and the rest from hi, of the larger last taken.
+        constexpr int h = NC / 2;
+        double lo[h], hi[h];
+#pragma unroll
+        for (int k = 0; k < h; ++k) {
+            lo[k] = fabs((double)s[h - 1 - k] - m);
+            hi[k] = fabs((double)s[h + k] - m);
+        }
+        double a = fmin(hi[h - 1], lo[h - 1]);
+#pragma unroll
+        for (int i = 1; i < h; ++i) a = fmin(a, fmax(lo[i - 1], hi[h - 1 - i]));
+        double b = fmax(lo[0], hi[h - 1]);
+#pragma unroll
+        for (int i = 2; i <= h; ++i) b = fmin(b, fmax(lo[i - 1], hi[h - i]));
+        d = (a + b) * 0.5;
+    } else {
+        double ds[NMAX];
+#pragma unroll
+        for (int r = 0; r < NMAX; ++r) ds[r] = dev[r];
+        sort_network<NMAX>(ds);
+        d = median_sorted<NMAX>(ds, nf);
     }
-    bitonic_sort<NMAX>(ds);
-    double d = median_sorted<NMAX>(ds, nf);
     if (d == 0.0) {
         const double q3 = quantile7_sorted<NMAX>(s, nf, 0.75);
         const double q1 = quantile7_sorted<NMAX>(s, nf, 0.25);
@@ -241,7 +285,7 @@ __device__ __forceinline__ UnitVote statistical_vote_row(const uint64_t (&bits)[
         v.majority = -1;
         return v;
     }
-    bitonic_sort<NMAX>(s);
+    sort_network<NMAX>(s);
     if (nf == NMAX) return statistical_tail<NMAX, NMAX>(x, s, fin, nonfin, nf, kappa);
     return statistical_tail<NMAX, 0>(x, s, fin, nonfin, nf, kappa);
 }
