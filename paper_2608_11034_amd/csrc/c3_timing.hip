@@ -27,24 +27,12 @@ struct VoteOut {
     uint32_t* masks;
 };
 
-// One thread per unit u = t * G + g (a wave reads 64 consecutive rows, fully
-// coalesced), deciding with the per-unit functions of c3_vote_row.h.
-// Outlier bits also go to the per-rank masks [segment][r][g] (bit t mod 32
-// of word t / 32) by atomic OR; they are sparse, so the atomics cost little,
-// and the masks must start zeroed.
-template <int NMAX, int MODE, int KIND>
-__device__ __forceinline__ void vote_unit(const char* __restrict__ ev, int R, int64_t G,
-                                          int64_t n_units, double kappa, bool dense,
-                                          const VoteOut& o, int64_t ub) {
-    constexpr int vsize = (KIND == C3_EV_U64 || KIND == C3_EV_F64) ? 8 : 4;
-    const int64_t u = ub * kVoteThreads + threadIdx.x;
-    // the workgroup's rows start at a uniform offset; the lane's offset
-    // within them fits 32 bits
-    const char* row = ev + ub * kVoteThreads * R * vsize + (uint32_t)(threadIdx.x * R * vsize);
-    uint64_t e[NMAX];
-    load_row_bits<NMAX>(row, KIND, vsize, R, dense, e);
-    const UnitVote v = MODE == C3_EXACT ? exact_vote_row<NMAX>(e, R)
-                                        : statistical_vote_row<NMAX, KIND>(e, R, kappa);
+// Stores one unit's decision: the optional per-unit results, and each
+// outlier bit ORed into the per-rank masks [segment][r][g] (bit t mod 32 of
+// word t / 32).  Outlier bits are sparse, so the atomics cost little; the
+// masks must start zeroed.
+__device__ __forceinline__ void store_vote(const UnitVote& v, int R, int64_t G, int64_t n_units,
+                                           const VoteOut& o, int64_t u) {
     if (o.status != nullptr) {
         o.status[u] = v.status;
         o.bitmap[u] = v.bitmap;
@@ -61,22 +49,30 @@ __device__ __forceinline__ void vote_unit(const char* __restrict__ ev, int R, in
     }
 }
 
-// Both votes in one launch, so every CU overlaps the exact vote (waits on
-// memory) with the statistical one (VALU-bound).  Workgroups go to the 8
-// XCDs round-robin, so the kind alternates every 8 workgroups:
-// b = 16 q + 8 k + x votes kind k (0 fingerprints, 1 step times) on unit
-// block 8 q + x.
-template <int NMAX, int KIND>
+// Both votes of one unit u = t * G + g per thread: the fingerprint row
+// (exact) and the step-time row (statistical) are loaded together, so their
+// memory latency overlaps, and a wave reads 64 consecutive rows of each,
+// fully coalesced.  Decisions are the per-unit functions of c3_vote_row.h.
+// DENSE (both rows read with 128-bit loads) is a template argument so that
+// all loads of both rows sit in one basic block and are issued together.
+template <int NMAX, int KIND, bool DENSE>
 __global__ void __launch_bounds__(kVoteThreads) timing_votes_kernel(
     const char* __restrict__ fp, const char* __restrict__ tp, int R, int64_t G, int64_t n_units,
     double kappa, bool fp_dense, bool t_dense, VoteOut fo, VoteOut to) {
-    const uint32_t b = blockIdx.x;
-    const int64_t ub = (int64_t)(((b >> 4) << 3) | (b & 7u));
-    if (ub * kVoteThreads + threadIdx.x >= n_units) return;
-    if ((b & 8u) == 0u)
-        vote_unit<NMAX, C3_EXACT, C3_EV_U64>(fp, R, G, n_units, kappa, fp_dense, fo, ub);
-    else
-        vote_unit<NMAX, C3_STATISTICAL, KIND>(tp, R, G, n_units, kappa, t_dense, to, ub);
+    constexpr int tsize = KIND == C3_EV_F64 ? 8 : 4;
+    const int64_t ub = blockIdx.x;
+    const int64_t u = ub * kVoteThreads + threadIdx.x;
+    if (u >= n_units) return;
+    // the workgroup's rows start at a uniform offset; the lane's offset
+    // within them fits 32 bits
+    const uint32_t lane_rows = threadIdx.x * (uint32_t)R;
+    uint64_t ef[NMAX], et[NMAX];
+    load_row_bits<NMAX>(fp + ub * kVoteThreads * R * 8 + lane_rows * 8u, C3_EV_U64, 8, R,
+                        DENSE || fp_dense, ef);
+    load_row_bits<NMAX>(tp + ub * kVoteThreads * R * tsize + lane_rows * (uint32_t)tsize, KIND,
+                        tsize, R, DENSE || t_dense, et);
+    store_vote(exact_vote_row<NMAX>(ef, R), R, G, n_units, fo, u);
+    store_vote(statistical_vote_row<NMAX, KIND>(et, R, kappa), R, G, n_units, to, u);
 }
 
 // Clears n16 16-byte words (the mask area is a multiple of 256 bytes).
@@ -235,15 +231,20 @@ template <int NMAX, int KIND>
 static hipError_t launch_votes(const uint64_t* fp, const char* tp, int R, int64_t G,
                                int64_t n_units, double kappa, const VoteOut& fo, const VoteOut& to,
                                hipStream_t stream) {
-    const int64_t blocks = 2 * (((n_units + kVoteThreads - 1) / kVoteThreads + 7) / 8 * 8);
+    const int64_t blocks = (n_units + kVoteThreads - 1) / kVoteThreads;
     constexpr int64_t tsize = KIND == C3_EV_F64 ? 8 : 4;
     const bool fp_dense = (R * 8) % 16 == 0 && ((uintptr_t)fp & 15) == 0;
     const bool t_dense = (R * tsize) % 16 == 0 && ((uintptr_t)tp & 15) == 0;
     if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
     if (blocks == 0) return hipSuccess;
-    hipLaunchKernelGGL((timing_votes_kernel<NMAX, KIND>), dim3((unsigned)blocks),
-                       dim3(kVoteThreads), 0, stream, reinterpret_cast<const char*>(fp), tp, R, G,
-                       n_units, kappa, fp_dense, t_dense, fo, to);
+    if (fp_dense && t_dense)
+        hipLaunchKernelGGL((timing_votes_kernel<NMAX, KIND, true>), dim3((unsigned)blocks),
+                           dim3(kVoteThreads), 0, stream, reinterpret_cast<const char*>(fp), tp, R,
+                           G, n_units, kappa, fp_dense, t_dense, fo, to);
+    else
+        hipLaunchKernelGGL((timing_votes_kernel<NMAX, KIND, false>), dim3((unsigned)blocks),
+                           dim3(kVoteThreads), 0, stream, reinterpret_cast<const char*>(fp), tp, R,
+                           G, n_units, kappa, fp_dense, t_dense, fo, to);
     return hipGetLastError();
 }
 

@@ -39,33 +39,43 @@ __device__ inline uint64_t load_ev_bits(const char* p, int kind) {
 
 // Raw bits of the R values of one unit (4-byte kinds zero-extended).  With
 // `dense` the replicas are adjacent and the row is 16-byte aligned and a
-// whole number of 16-byte words, so it is read with 128-bit loads.
+// whole number of 16-byte words, so it is read with 128-bit loads.  Every
+// slot is loaded unconditionally (slots past R re-read the row's first word
+// and are zeroed afterwards): loads under a branch would each be waited for
+// at the branch's join, serializing them.
 template <int NMAX>
 __device__ __forceinline__ void load_row_bits(const char* base, int kind, int64_t rstride, int R,
                                               bool dense, uint64_t (&e)[NMAX]) {
     const bool wide = kind == C3_EV_U64 || kind == C3_EV_F64;
     if (dense && wide) {
+        vu32x4 v[NMAX / 2];
+#pragma unroll
+        for (int j = 0; j < NMAX / 2; ++j)
+            v[j] = *reinterpret_cast<const vu32x4*>(base + (2 * j < R ? 16 * j : 0));
 #pragma unroll
         for (int j = 0; j < NMAX / 2; ++j) {
-            vu32x4 v = {0u, 0u, 0u, 0u};
-            if (2 * j < R) v = *reinterpret_cast<const vu32x4*>(base + 16 * j);
-            e[2 * j] = ((uint64_t)v.y << 32) | v.x;
-            e[2 * j + 1] = ((uint64_t)v.w << 32) | v.z;
+            const bool in = 2 * j < R;
+            e[2 * j] = in ? ((uint64_t)v[j].y << 32) | v[j].x : 0ull;
+            e[2 * j + 1] = in ? ((uint64_t)v[j].w << 32) | v[j].z : 0ull;
         }
     } else if (dense && NMAX >= 4) {
+        vu32x4 v[NMAX / 4];
+#pragma unroll
+        for (int j = 0; j < NMAX / 4; ++j)
+            v[j] = *reinterpret_cast<const vu32x4*>(base + (4 * j < R ? 16 * j : 0));
 #pragma unroll
         for (int j = 0; j < NMAX / 4; ++j) {
-            vu32x4 v = {0u, 0u, 0u, 0u};
-            if (4 * j < R) v = *reinterpret_cast<const vu32x4*>(base + 16 * j);
-            e[4 * j] = v.x;
-            e[4 * j + 1] = v.y;
-            e[4 * j + 2] = v.z;
-            e[4 * j + 3] = v.w;
+            const bool in = 4 * j < R;
+            e[4 * j] = in ? v[j].x : 0u;
+            e[4 * j + 1] = in ? v[j].y : 0u;
+            e[4 * j + 2] = in ? v[j].z : 0u;
+            e[4 * j + 3] = in ? v[j].w : 0u;
         }
     } else {
 #pragma unroll
-        for (int r = 0; r < NMAX; ++r)
-            e[r] = r < R ? load_ev_bits(base + (int64_t)r * rstride, kind) : 0ull;
+        for (int r = 0; r < NMAX; ++r) e[r] = load_ev_bits(base + (r < R ? r : 0) * rstride, kind);
+#pragma unroll
+        for (int r = 0; r < NMAX; ++r) e[r] = r < R ? e[r] : 0ull;
     }
 }
 
