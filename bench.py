@@ -342,7 +342,7 @@ def bench_timing(args, torch, workloads, c3, dev):
         "roofline": {"bound": "hbm", "achieved": round(pass_bytes / (ms * 1e-3) / 1e9, 2),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(pass_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
-                     "traffic": None, "kernel": "timing_vote_kernel+timing_confirm_kernel",
+                     "traffic": None, "kernel": "timing_zero_kernel+timing_votes_staged_kernel+timing_confirm_kernel",
                      "kernel_ms": round(ms, 4), "algorithmic_bytes_per_launch": pass_bytes},
         "ms_per_step_verdicts_only": round(ms_verdicts, 4),
         "ms_per_step_separate_calls": round(ms_sep, 4),

@@ -75,6 +75,96 @@ __global__ void __launch_bounds__(kVoteThreads) timing_votes_kernel(
     store_vote(statistical_vote_row<NMAX, KIND>(et, R, kappa), R, G, n_units, to, u);
 }
 
+// Staged variant for R == NMAX with both kinds dense: rows are 32, 64 or
+// 128 bytes, read per lane they would take several 16-byte loads per row
+// that each touch every cache line of the wave's rows.  Instead each wave
+// reads its 64 rows of a kind with contiguous 1 KB loads (lane l, load j:
+// bytes 1024 j + 16 l), passes them through its own LDS region and takes
+// its row back.  Chunk c of row u sits at slot u * CP + ((c + (u >> s)) &
+// (CP - 1)), s = log2(16 / CP), which puts any 16 consecutive lanes on 16
+// distinct 16-byte bank groups for the writes and for the reads.  No
+// workgroup barrier: a wave only touches its own region, and LDS
+// instructions of one wave execute in order.
+template <int CP>
+__device__ __forceinline__ int stage_slot(int u, int c) {
+    constexpr int S = CP == 1 ? 4 : CP == 2 ? 3 : CP == 4 ? 2 : 1;
+    return u * CP + ((c + (u >> S)) & (CP - 1));
+}
+
+__device__ __forceinline__ void wave_lds_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Loads of one kind: the wave's rows start at wbase, nbytes of them exist
+// (whole rows, at least one); loads past them re-read the last 16 bytes.
+template <int CP>
+__device__ __forceinline__ void stage_load(const char* wbase, int64_t nbytes, int lane,
+                                           vu32x4 (&g)[CP]) {
+#pragma unroll
+    for (int j = 0; j < CP; ++j) {
+        int64_t off = 1024 * j + 16 * lane;
+        off = off < nbytes - 16 ? off : nbytes - 16;
+        g[j] = *reinterpret_cast<const vu32x4*>(wbase + off);
+    }
+}
+
+template <int CP>
+__device__ __forceinline__ void stage_swap(vu32x4* lds, int lane, const vu32x4 (&g)[CP],
+                                           vu32x4 (&v)[CP]) {
+#pragma unroll
+    for (int j = 0; j < CP; ++j) {
+        const int b = 1024 * j + 16 * lane;
+        lds[stage_slot<CP>(b / (16 * CP), (b / 16) % CP)] = g[j];
+    }
+    wave_lds_sync();
+#pragma unroll
+    for (int c = 0; c < CP; ++c) v[c] = lds[stage_slot<CP>(lane, c)];
+    wave_lds_sync();   // every lane has read before the region is written again
+}
+
+template <int NMAX, int KIND>
+__global__ void __launch_bounds__(kVoteThreads) timing_votes_staged_kernel(
+    const char* __restrict__ fp, const char* __restrict__ tp, int64_t G, int64_t n_units,
+    double kappa, VoteOut fo, VoteOut to) {
+    constexpr int R = NMAX;
+    constexpr int CPF = NMAX / 2;                                // u64 fingerprints
+    constexpr int CPT = KIND == C3_EV_F64 ? NMAX / 2 : NMAX / 4;  // step times
+    __shared__ vu32x4 stage[kVoteThreads / 64][64 * CPF];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t wu0 = (int64_t)blockIdx.x * kVoteThreads + wave * 64;
+    if (wu0 >= n_units) return;                                  // whole wave past the end
+    const int64_t nu = n_units - wu0 < 64 ? n_units - wu0 : 64;
+    vu32x4 gf[CPF], gt[CPT], vf[CPF], vt[CPT];
+    stage_load<CPF>(fp + wu0 * (16 * CPF), nu * (16 * CPF), lane, gf);
+    stage_load<CPT>(tp + wu0 * (16 * CPT), nu * (16 * CPT), lane, gt);
+    stage_swap<CPF>(stage[wave], lane, gf, vf);
+    stage_swap<CPT>(stage[wave], lane, gt, vt);
+    const int64_t u = wu0 + lane;
+    if (u >= n_units) return;
+    uint64_t ef[NMAX], et[NMAX];
+#pragma unroll
+    for (int c = 0; c < CPF; ++c) {
+        ef[2 * c] = ((uint64_t)vf[c].y << 32) | vf[c].x;
+        ef[2 * c + 1] = ((uint64_t)vf[c].w << 32) | vf[c].z;
+    }
+#pragma unroll
+    for (int c = 0; c < CPT; ++c) {
+        if constexpr (KIND == C3_EV_F64) {
+            et[2 * c] = ((uint64_t)vt[c].y << 32) | vt[c].x;
+            et[2 * c + 1] = ((uint64_t)vt[c].w << 32) | vt[c].z;
+        } else {
+            et[4 * c] = vt[c].x;
+            et[4 * c + 1] = vt[c].y;
+            et[4 * c + 2] = vt[c].z;
+            et[4 * c + 3] = vt[c].w;
+        }
+    }
+    store_vote(exact_vote_row<NMAX>(ef, R), R, G, n_units, fo, u);
+    store_vote(statistical_vote_row<NMAX, KIND>(et, R, kappa), R, G, n_units, to, u);
+}
+
 // Clears n16 16-byte words (the mask area is a multiple of 256 bytes).
 __global__ void __launch_bounds__(256) timing_zero_kernel(uint4* __restrict__ p, int64_t n16) {
     const int64_t step = (int64_t)gridDim.x * 256;
@@ -237,7 +327,11 @@ static hipError_t launch_votes(const uint64_t* fp, const char* tp, int R, int64_
     const bool t_dense = (R * tsize) % 16 == 0 && ((uintptr_t)tp & 15) == 0;
     if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
     if (blocks == 0) return hipSuccess;
-    if (fp_dense && t_dense)
+    if (fp_dense && t_dense && R == NMAX)
+        hipLaunchKernelGGL((timing_votes_staged_kernel<NMAX, KIND>), dim3((unsigned)blocks),
+                           dim3(kVoteThreads), 0, stream, reinterpret_cast<const char*>(fp), tp, G,
+                           n_units, kappa, fo, to);
+    else if (fp_dense && t_dense)
         hipLaunchKernelGGL((timing_votes_kernel<NMAX, KIND, true>), dim3((unsigned)blocks),
                            dim3(kVoteThreads), 0, stream, reinterpret_cast<const char*>(fp), tp, R,
                            G, n_units, kappa, fp_dense, t_dense, fo, to);

@@ -94,6 +94,7 @@ CASES = [
     (5, 64, 64, 64, False), (7, 66, 90, 64, True), (8, 20, 129, 63, False),
     (9, 64, 16, 16, False), (13, 33, 41, 16, True), (16, 64, 24, 8, False), (16, 3, 9, 64, False),
     (4, 66, 300, 1, False), (6, 9, 700, 2, True),   # several lanes per rank, short windows
+    (4, 50, 37, 4, True), (16, 40, 30, 16, True), (8, 1, 70, 16, True),   # fp64 times, R = 4, 16
     (20, 40, 50, 16, False),                 # R > 16: separate steps
     (8, 50, 120, 80, False),                 # W > 64: separate steps
 ]
