@@ -12,7 +12,7 @@
 // segment, notes the first attributed fingerprint and any two consecutive
 // attributed timings (the pair (t, t + 1) belongs to the segment of t), and
 // slides a window of W iterations over the window starts in its segment
-// (reading up to W - 1 iterations into the next segment).  For W <= 64 the
+// (reading up to W - 1 iterations, and at least one, into the next segment).  For W <= 64 the
 // thread first gathers its bits of the segment (and the next W - 1
 // iterations) into 64-bit masks with independent loads, then works on the
 // masks with shifts and popcounts; longer windows walk the bitmaps.
@@ -69,7 +69,9 @@ __global__ void __launch_bounds__(kConfThreads) confirm_segment_kernel(
                 lo |= (uint64_t)bit_of(tmb, t, G, g, r) << i;
             }
         }
-        const int64_t t_hi_end = min(T, t1 + Wt - 1);      // iterations read by windows
+        // iterations read past the segment: by its windows, and t1 for the
+        // pair (t1 - 1, t1) even when W = 1
+        const int64_t t_hi_end = min(T, t1 + (Wt > 1 ? Wt - 1 : 1));
 #pragma unroll
         for (int i = 0; i < kSeg - 1; ++i) {
             const int64_t t = t0 + kSeg + i;
@@ -138,7 +140,8 @@ __global__ void __launch_bounds__(kConfThreads) confirm_group_kernel(
     const int64_t g = idx - sgi * G;
     const int64_t t0 = sgi * SEG;
     const int64_t t1 = min(T, t0 + SEG);
-    const int64_t t_hi_end = min(T, t1 + Wt - 1);
+    // read past the segment for its windows, and t1 for the pair (t1 - 1, t1)
+    const int64_t t_hi_end = min(T, t1 + (Wt > 1 ? Wt - 1 : 1));
     uint64_t div[RMAX], lo[RMAX], hi[RMAX];
 #pragma unroll
     for (int r = 0; r < RMAX; ++r) div[r] = lo[r] = hi[r] = 0;

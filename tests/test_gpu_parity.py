@@ -345,7 +345,7 @@ def test_localize_matches_oracle(U):
 
 @pytest.mark.parametrize("R", [3, 8, 13, 20])
 @pytest.mark.parametrize("T,W", [(200, 16), (64, 16), (65, 16), (10, 16), (1, 1), (130, 7),
-                                 (200, 64), (200, 65), (90, 100), (300, 63)])
+                                 (200, 64), (200, 65), (90, 100), (300, 63), (300, 1), (129, 2)])
 def test_confirm_matches_oracle(T, W, R):
     _print_case("confirm", T, W, R)
     rng = np.random.default_rng(T * 31 + W + 1000 * R)
@@ -363,6 +363,27 @@ def test_confirm_matches_oracle(T, W, R):
     assert np.array_equal(out["slow_count"], ref["slow_count"])
     assert np.array_equal(out["max_window_slow"], ref["max_window"])
     assert np.array_equal(out["first_straggler_window"], ref["first_window"])
+
+
+@pytest.mark.parametrize("R", [8, 20])
+@pytest.mark.parametrize("W", [1, 2, 16, 80])
+def test_confirm_pair_across_segments(W, R):
+    # slow at t0 and t0 + 1 for one rank, across every segment boundary
+    # of 32 and 64 iterations
+    _print_case("confirm pair", W, R)
+    T, G = 260, 5
+    for t0 in (31, 63, 127, 191):
+        fp = np.zeros((T, G), dtype=np.uint64)
+        tm = np.zeros((T, G), dtype=np.uint64)
+        tm[t0, 2] = tm[t0 + 1, 2] = np.uint64(1 << 3)
+        out = c3.verdicts_numpy(c3.confirm(torch.from_numpy(fp.view(np.int64)).to(DEV),
+                                           torch.from_numpy(tm.view(np.int64)).to(DEV), R, W))
+        ref = oracle.confirm(fp, tm, R, W)
+        assert ref["flags"][3 * G + 2] & 4
+        for k, rk in (("flags", "flags"), ("slow_count", "slow_count"),
+                      ("max_window_slow", "max_window"),
+                      ("first_straggler_window", "first_window")):
+            assert np.array_equal(out[k], ref[rk]), (t0, k)
 
 
 # ---------------------------------------------------------------------------
