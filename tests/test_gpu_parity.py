@@ -304,6 +304,41 @@ def test_statistical_consensus_matches_oracle(R, dt):
     assert np.array_equal(mj.cpu().numpy(), omj)
 
 
+@pytest.mark.parametrize("R", [4, 5, 8, 16])
+@pytest.mark.parametrize("dt", [np.float32, np.float64])
+def test_statistical_consensus_extremes(R, dt):
+    # magnitudes where the median's sum and the deviations overflow to inf,
+    # subnormals, signed zeros and mixed signs at the top of the range
+    _print_case("statistical extremes", R, dt)
+    rng = np.random.default_rng(7 * R)
+    big = np.finfo(dt).max
+    tiny = np.finfo(dt).smallest_subnormal
+    rows = []
+    for _ in range(400):
+        kind = rng.integers(0, 7)
+        if kind == 0:
+            v = rng.choice([big, -big], size=R)
+        elif kind == 1:
+            v = big * (1 - rng.random(R) * 1e-3)
+        elif kind == 2:
+            v = np.where(rng.random(R) < 0.5, big * 0.9, -big * 0.9)
+        elif kind == 3:
+            v = tiny * rng.integers(0, 5, size=R)
+        elif kind == 4:
+            v = rng.choice([0.0, -0.0, tiny, -tiny], size=R)
+        elif kind == 5:
+            v = np.concatenate([np.full(R - 1, big / 2), [-big]])
+        else:
+            v = (big / 8) * np.clip(rng.standard_normal(R), -6, 6)
+        rows.append(v)
+    tau = np.array(rows, dtype=dt)
+    st, bm, mj = c3.consensus(torch.from_numpy(tau).to(DEV), c3.STATISTICAL)
+    ost, obm, omj = oracle.vote_statistical(tau, oracle.KAPPA_DEFAULT, replica_axis=1)
+    assert np.array_equal(st.cpu().numpy(), ost)
+    assert np.array_equal(bm.cpu().numpy().view(np.uint64), obm)
+    assert np.array_equal(mj.cpu().numpy(), omj)
+
+
 def test_statistical_closed_forms_on_gpu():
     _print_case("statistical closed forms")
     import os
