@@ -401,11 +401,17 @@ size_t c3_timing_consensus_workspace_size(int R, int64_t G, int64_t T, int windo
  *                 three NULL for a kind whose per-unit results are not
  *                 wanted (then only the verdicts are produced for it).
  *   verdicts      device [R*G], rank = r*G + g, as c3_confirm.
- * For R <= 16 and W <= 64 two fused kernels run: the votes of 16 (8 for
- * R > 8) iterations x 64 groups per workgroup, packing each rank's outlier
- * bits through LDS into the workspace, then one thread per rank confirms
- * from those bits.  Otherwise the three separate steps run, with the
- * per-unit results kept in the workspace when not requested.
+ * Execution (results do not depend on it):
+ *   - no per-unit results requested, R in {4, 8, 16}, both arrays 16-byte
+ *     aligned, 2 * ceil(T / 32) * R * 64 bytes <= 64 KiB and G / 16 at least
+ *     the device's compute-unit count: one kernel; each workgroup votes 16
+ *     groups over all T iterations, collects its ranks' outlier bits in LDS
+ *     and confirms them there (the workspace is not touched);
+ *   - otherwise, for R <= 16 and W <= 64: a clearing kernel, one kernel
+ *     voting both kinds that ORs each outlier bit into per-rank masks in the
+ *     workspace, and a confirmation kernel over those masks;
+ *   - otherwise the three separate steps (c3_consensus twice, c3_confirm),
+ *     with the per-unit results kept in the workspace when not requested.
  * Errors: C3_E_INVAL (sizes, kinds, kappa, outputs half given),
  * C3_E_WORKSPACE, C3_E_ALIGN, C3_E_HIP.  R * G == 0 does nothing.
  */

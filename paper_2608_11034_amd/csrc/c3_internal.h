@@ -40,8 +40,10 @@ hipError_t launch_adamw_slice(const AdamwPtrs& ptrs, const AdamwConst& c, int R,
                               hipStream_t stream);
 
 // Fused timing consensus (R <= 16, window <= 64): vote both evidence kinds
-// per (iteration, group), pack per-rank bits, confirm per rank.  The
-// workspace holds the packed masks (timing_masks_bytes).
+// per (iteration, group), collect per-rank outlier bits, confirm per rank.
+// Without per-unit results and at a shape that fills the device this is one
+// kernel with the bits in LDS; otherwise three launches with the bits in
+// the workspace (timing_masks_bytes).
 int64_t timing_masks_bytes(int R, int64_t G, int64_t T);
 hipError_t launch_timing_consensus(const uint64_t* fp, const void* times, int time_kind, int R,
                                    int64_t G, int64_t T, double kappa, int window,

@@ -6,10 +6,15 @@
 // c3_consensus; besides the optional per-unit results they OR each outlier
 // bit into a per-rank mask (one 32-bit word per rank, kind and 32
 // iterations), so the confirmation reads 8 bytes per rank and 32 iterations
-// instead of the per-unit bitmaps, and walks them a word at a time.
+// instead of the per-unit bitmaps, and walks them a word at a time.  The
+// masks live in the workspace (three launches: clear, votes, confirmation)
+// or, when no per-unit results are wanted, in the LDS of a single kernel
+// whose workgroups each own a set of groups over all iterations.
 #include "c3_device.h"
 #include "c3_internal.h"
 #include "c3_vote_row.h"
+
+#include <atomic>
 
 namespace c3 {
 
@@ -182,15 +187,19 @@ __global__ void __launch_bounds__(256) timing_zero_kernel(uint4* __restrict__ p,
 // of the 64 bits (segment : previous segment), evaluated only where a set
 // bit enters; longer windows keep a 64-bit shift register.  Segments whose
 // set bits cannot raise the maximum or reach the threshold are skipped.
+//
+// The masks of the rank's kinds are read at fpm[s * stride], tpm[s * stride]
+// for segment s: global memory in the three-launch path, LDS in the
+// single-pass kernel.
+struct ConfirmAcc {
+    uint32_t flags, dc, sc, mw;
+    int32_t fd, fw;
+};
+
 template <bool SHORT>
-__global__ void __launch_bounds__(kConfirmThreads) timing_confirm_kernel(
-    const uint32_t* __restrict__ fp_masks, const uint32_t* __restrict__ t_masks, int R, int64_t G,
-    int64_t T, int Wt, c3_rank_verdict_t* __restrict__ verdicts) {
-    const int64_t idx = (int64_t)blockIdx.x * kConfirmThreads + threadIdx.x;
-    const int64_t rank = idx / kConfirmLanes;
-    const int part = (int)(idx % kConfirmLanes);
-    const bool live = rank < (int64_t)R * G;    // dead lanes still join the shuffles
-    const int64_t r = live ? rank / G : 0, g = live ? rank - r * G : 0;
+__device__ __forceinline__ ConfirmAcc confirm_lane(const uint32_t* fpm, const uint32_t* tpm,
+                                                   int64_t stride, int64_t T, int Wt, int part,
+                                                   bool live) {
     const int64_t n_seg = (T + kSegIters - 1) / kSegIters;
     const int64_t per = (n_seg + kConfirmLanes - 1) / kConfirmLanes;   // segments per lane
     const int64_t s_lo = part * per;
@@ -201,12 +210,8 @@ __global__ void __launch_bounds__(kConfirmThreads) timing_confirm_kernel(
     // least one iteration past t_hi for the pair (t_hi - 1, t_hi).
     int64_t t_end = t_hi + (Wt > 1 ? Wt - 1 : 1);
     if (t_end > T) t_end = T;
-    uint32_t flags = 0, dc = 0, sc = 0, mw = 0;
-    int32_t fd = -1, fw = -1;
+    ConfirmAcc a{0u, 0u, 0u, 0u, -1, -1};
     if (live && t_lo < t_hi) {
-        const int64_t stride = (int64_t)R * G;
-        const uint32_t* fpm = fp_masks + r * G + g;
-        const uint32_t* tpm = t_masks + r * G + g;
         const uint32_t len = (uint32_t)(t_hi - t_lo);
         const uint32_t wlo = (uint32_t)(Wt - 1);
         const uint64_t wmask = Wt >= 64 ? ~0ull : ((1ull << Wt) - 1ull);
@@ -224,9 +229,9 @@ __global__ void __launch_bounds__(kConfirmThreads) timing_confirm_kernel(
             for (int j = 0; j < kPrefetch; ++j) {
                 // fingerprint bits: counts and the first attributed iteration
                 // (bits past T were never set)
-                if (fmv[j] != 0u && fd < 0)
-                    fd = (int32_t)((s0 + j) * kSegIters + __builtin_ctz(fmv[j]));
-                dc += (uint32_t)__builtin_popcount(fmv[j]);
+                if (fmv[j] != 0u && a.fd < 0)
+                    a.fd = (int32_t)((s0 + j) * kSegIters + __builtin_ctz(fmv[j]));
+                a.dc += (uint32_t)__builtin_popcount(fmv[j]);
                 const int64_t left = t_end - (s0 + j) * kSegIters;
                 const uint32_t n = left <= 0 ? 0u : left < kSegIters ? (uint32_t)left : kSegIters;
                 if (n == 0u) break;
@@ -234,12 +239,12 @@ __global__ void __launch_bounds__(kConfirmThreads) timing_confirm_kernel(
                 const uint32_t tm = n < 32u ? tmv[j] & ((1u << n) - 1u) : tmv[j];
                 // counts at positions q0 + i < len
                 const uint32_t cn = len > q0 ? (len - q0 < n ? len - q0 : n) : 0u;
-                sc += (uint32_t)__builtin_popcount(cn < 32u ? tm & ((1u << cn) - 1u) : tm);
+                a.sc += (uint32_t)__builtin_popcount(cn < 32u ? tm & ((1u << cn) - 1u) : tm);
                 // pairs ending at q0 + i with 1 <= q0 + i <= len
                 const uint32_t pairs = tm & ((tm << 1) | (prev >> 31));
                 const uint32_t p_hi = len + 1u > q0 ? (len + 1u - q0 < n ? len + 1u - q0 : n) : 0u;
                 const uint32_t p_mask = (p_hi < 32u ? (1u << p_hi) - 1u : ~0u) & (q0 == 0u ? ~1u : ~0u);
-                if (pairs & p_mask) flags |= C3_RANK_CONSEC2;
+                if (pairs & p_mask) a.flags |= C3_RANK_CONSEC2;
                 // windows ending at positions i in [lo_i, hi_i) of this segment
                 const uint32_t lo_i = wlo > q0 ? wlo - q0 : 0u;
                 const uint32_t hi_q = wlo + len - q0;       // exclusive, may exceed n
@@ -248,7 +253,7 @@ __global__ void __launch_bounds__(kConfirmThreads) timing_confirm_kernel(
                 // when all set bits of (segment : previous) could not.
                 const uint32_t ybits = (uint32_t)__builtin_popcount(tm) + __builtin_popcount(prev);
                 if (SHORT) {
-                    if ((ybits > mw || (2u * ybits > (uint32_t)Wt && fw < 0)) && lo_i < hi_i) {
+                    if ((ybits > a.mw || (2u * ybits > (uint32_t)Wt && a.fw < 0)) && lo_i < hi_i) {
                         // A window count only grows when a set bit enters, so
                         // the maximum and the first window over the threshold
                         // end at a set bit -- or at the lane's first window
@@ -264,9 +269,9 @@ __global__ void __launch_bounds__(kConfirmThreads) timing_confirm_kernel(
                             ev &= ev - 1u;
                             const uint32_t c = (uint32_t)__builtin_popcount(
                                 (uint32_t)(y >> (33u + i - (uint32_t)Wt)) & wm);
-                            mw = c > mw ? c : mw;
-                            if (2u * c > (uint32_t)Wt && fw < 0)
-                                fw = (int32_t)(t_lo + (int64_t)(q0 + i - wlo));
+                            a.mw = c > a.mw ? c : a.mw;
+                            if (2u * c > (uint32_t)Wt && a.fw < 0)
+                                a.fw = (int32_t)(t_lo + (int64_t)(q0 + i - wlo));
                         }
                     }
                 } else {
@@ -275,9 +280,9 @@ __global__ void __launch_bounds__(kConfirmThreads) timing_confirm_kernel(
                             hist = (hist << 1) | ((tm >> i) & 1u);
                             if (i >= lo_i && i < hi_i) {
                                 const uint32_t c = (uint32_t)__builtin_popcountll(hist & wmask);
-                                mw = c > mw ? c : mw;
-                                if (2u * c > (uint32_t)Wt && fw < 0)
-                                    fw = (int32_t)(t_lo + (int64_t)(q0 + i - wlo));
+                                a.mw = c > a.mw ? c : a.mw;
+                                if (2u * c > (uint32_t)Wt && a.fw < 0)
+                                    a.fw = (int32_t)(t_lo + (int64_t)(q0 + i - wlo));
                             }
                         }
                     }
@@ -286,30 +291,188 @@ __global__ void __launch_bounds__(kConfirmThreads) timing_confirm_kernel(
             }
         }
     }
-    // combine the lanes of one rank: sums, maxima, first (smallest >= 0) positions
+    return a;
+}
+
+// Combines the kConfirmLanes lanes of one rank (sums, maxima, first --
+// smallest non-negative -- positions); lane `part` 0 of a live rank writes
+// its verdict.  Every lane of the wave must call it.
+__device__ __forceinline__ void confirm_store(ConfirmAcc a, bool live, int part,
+                                              c3_rank_verdict_t* __restrict__ verdicts,
+                                              int64_t rank) {
 #pragma unroll
     for (int o = 1; o < kConfirmLanes; o <<= 1) {
-        flags |= (uint32_t)__shfl_xor((int)flags, o, kConfirmLanes);
-        dc += (uint32_t)__shfl_xor((int)dc, o, kConfirmLanes);
-        sc += (uint32_t)__shfl_xor((int)sc, o, kConfirmLanes);
-        const uint32_t m2 = (uint32_t)__shfl_xor((int)mw, o, kConfirmLanes);
-        mw = m2 > mw ? m2 : mw;
-        const int32_t f2 = __shfl_xor(fd, o, kConfirmLanes);
-        fd = (fd < 0 || (f2 >= 0 && f2 < fd)) ? f2 : fd;
-        const int32_t w2 = __shfl_xor(fw, o, kConfirmLanes);
-        fw = (fw < 0 || (w2 >= 0 && w2 < fw)) ? w2 : fw;
+        a.flags |= (uint32_t)__shfl_xor((int)a.flags, o, kConfirmLanes);
+        a.dc += (uint32_t)__shfl_xor((int)a.dc, o, kConfirmLanes);
+        a.sc += (uint32_t)__shfl_xor((int)a.sc, o, kConfirmLanes);
+        const uint32_t m2 = (uint32_t)__shfl_xor((int)a.mw, o, kConfirmLanes);
+        a.mw = m2 > a.mw ? m2 : a.mw;
+        const int32_t f2 = __shfl_xor(a.fd, o, kConfirmLanes);
+        a.fd = (a.fd < 0 || (f2 >= 0 && f2 < a.fd)) ? f2 : a.fd;
+        const int32_t w2 = __shfl_xor(a.fw, o, kConfirmLanes);
+        a.fw = (a.fw < 0 || (w2 >= 0 && w2 < a.fw)) ? w2 : a.fw;
     }
     if (!live || part != 0) return;
-    if (fw >= 0) flags |= C3_RANK_STRAGGLER;
-    if (fd >= 0) flags |= C3_RANK_PROTOCOL;
+    if (a.fw >= 0) a.flags |= C3_RANK_STRAGGLER;
+    if (a.fd >= 0) a.flags |= C3_RANK_PROTOCOL;
     c3_rank_verdict_t v;
-    v.flags = flags;
-    v.first_divergent_iter = fd;
-    v.divergent_count = dc;
-    v.slow_count = sc;
-    v.max_window_slow = mw;
-    v.first_straggler_window = fw;
+    v.flags = a.flags;
+    v.first_divergent_iter = a.fd;
+    v.divergent_count = a.dc;
+    v.slow_count = a.sc;
+    v.max_window_slow = a.mw;
+    v.first_straggler_window = a.fw;
     verdicts[rank] = v;
+}
+
+template <bool SHORT>
+__global__ void __launch_bounds__(kConfirmThreads) timing_confirm_kernel(
+    const uint32_t* __restrict__ fp_masks, const uint32_t* __restrict__ t_masks, int R, int64_t G,
+    int64_t T, int Wt, c3_rank_verdict_t* __restrict__ verdicts) {
+    const int64_t idx = (int64_t)blockIdx.x * kConfirmThreads + threadIdx.x;
+    const int64_t rank = idx / kConfirmLanes;
+    const int part = (int)(idx % kConfirmLanes);
+    const bool live = rank < (int64_t)R * G;    // dead lanes still join the shuffles
+    const int64_t r = live ? rank / G : 0, g = live ? rank - r * G : 0;
+    const ConfirmAcc a = confirm_lane<SHORT>(fp_masks + r * G + g, t_masks + r * G + g,
+                                             (int64_t)R * G, T, Wt, part, live);
+    confirm_store(a, live, part, verdicts, rank);
+}
+
+// ---------------------------------------------------------------------------
+// Single-pass timing consensus.  One workgroup owns kPassGroups consecutive
+// groups over all T iterations, so every outlier bit of its ranks lands in
+// its own LDS: the votes OR the bits into per-rank masks [kind][segment][r]
+// [group] there (no global atomics and no clearing launch), and after one
+// workgroup barrier the same workgroup confirms its ranks from LDS.  A
+// wave's step is 64 units, kPassIters iterations x kPassGroups groups; the
+// step's rows of one kind are kPassIters contiguous runs of kPassGroups
+// rows, read with 16-byte loads and passed through the wave's LDS region as
+// in the staged kernel (lane l takes back row l: iteration t0 + l /
+// kPassGroups, group g0 + l % kPassGroups).  Used when no per-unit results
+// are requested, R equals the group bound, both kinds' rows are 16-byte
+// aligned, the masks fit kPassMaskLds bytes and there are at least as many
+// workgroups as compute units.  Per-unit results would be written here as
+// 16- to 128-byte pieces of each iteration's row: measured on the 32,768-
+// rank workload the pass then took 117 us against 115 us for the three
+// launches, whose workgroups write whole runs of consecutive units, so
+// calls that want them take the three launches.
+// ---------------------------------------------------------------------------
+constexpr int kPassGroups = 16;                  // groups per workgroup
+constexpr int kPassIters = 64 / kPassGroups;     // iterations per wave step
+constexpr int64_t kPassMaskLds = 64 * 1024;      // LDS bytes for the masks
+
+template <int NMAX>
+struct PassShape {
+    static constexpr int waves = NMAX == 16 ? 8 : 16;
+    static constexpr int threads = 64 * waves;
+};
+
+// Loads of one kind for one wave step: row i of the step (i = 0..63) is unit
+// (t0 + i / kPassGroups, g0 + i % kPassGroups), RB = 16 CP bytes long; load j
+// of lane l reads the step's bytes 1024 j + 16 l.  Rows outside the T x ng
+// block read row (0, g0) instead; their lanes store nothing.
+template <int CP>
+__device__ __forceinline__ void pass_load(const char* __restrict__ base, int64_t G, int64_t T,
+                                          int64_t g0, int ng, int64_t t0, int lane,
+                                          vu32x4 (&g)[CP]) {
+    constexpr int RB = 16 * CP;
+#pragma unroll
+    for (int j = 0; j < CP; ++j) {
+        const int b = 1024 * j + 16 * lane;
+        const int row = b / RB;
+        const int ti = row / kPassGroups, gi = row % kPassGroups;
+        const int64_t t = t0 + ti;
+        const bool ok = t < T && gi < ng;
+        const int64_t off = ok ? (t * G + g0 + gi) * RB + (b % RB) : g0 * RB;
+        g[j] = *reinterpret_cast<const vu32x4*>(base + off);
+    }
+}
+
+template <int NMAX, int KIND, bool SHORT>
+__global__ void __launch_bounds__(PassShape<NMAX>::threads) timing_pass_kernel(
+    const char* __restrict__ fp, const char* __restrict__ tp, int64_t G, int64_t T, double kappa,
+    int Wt, c3_rank_verdict_t* __restrict__ verdicts) {
+    constexpr int R = NMAX;
+    constexpr int NW = PassShape<NMAX>::waves;
+    constexpr int CPF = NMAX / 2;                                // u64 fingerprints
+    constexpr int CPT = KIND == C3_EV_F64 ? NMAX / 2 : NMAX / 4;  // step times
+    constexpr int SEGW = R * kPassGroups;                        // mask words per segment
+    __shared__ vu32x4 stage[NW][64 * CPF];
+    extern __shared__ uint32_t pass_masks[];                     // [2][n_seg][R][kPassGroups]
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t g0 = (int64_t)blockIdx.x * kPassGroups;
+    const int ng = G - g0 < kPassGroups ? (int)(G - g0) : kPassGroups;
+    const int64_t n_seg = (T + kSegIters - 1) / kSegIters;
+    uint32_t* fmask = pass_masks;
+    uint32_t* tmask = pass_masks + n_seg * SEGW;
+    for (int64_t i = threadIdx.x; i < 2 * n_seg * SEGW; i += PassShape<NMAX>::threads)
+        pass_masks[i] = 0u;
+    __syncthreads();
+
+    const int ti = lane / kPassGroups, gi = lane % kPassGroups;
+    const int64_t n_steps = (T + kPassIters - 1) / kPassIters;
+    // The next step's rows are loaded before this step's results are
+    // stored: the vector-memory counter retires loads and stores in issue
+    // order, so waiting for loads issued after the stores would wait for
+    // the stores too.  The last step re-reads its own rows (L2 hits) rather
+    // than branch around the prefetch.
+    vu32x4 gf[CPF], gt[CPT];
+    if (wave < n_steps) {
+        pass_load<CPF>(fp, G, T, g0, ng, (int64_t)wave * kPassIters, lane, gf);
+        pass_load<CPT>(tp, G, T, g0, ng, (int64_t)wave * kPassIters, lane, gt);
+    }
+    for (int64_t st = wave; st < n_steps; st += NW) {
+        const int64_t t0 = st * kPassIters;
+        vu32x4 vf[CPF], vt[CPT];
+        stage_swap<CPF>(stage[wave], lane, gf, vf);
+        stage_swap<CPT>(stage[wave], lane, gt, vt);
+        const int64_t tn = (st + NW < n_steps ? st + NW : st) * kPassIters;
+        pass_load<CPF>(fp, G, T, g0, ng, tn, lane, gf);
+        pass_load<CPT>(tp, G, T, g0, ng, tn, lane, gt);
+        const int64_t t = t0 + ti;
+        if (t >= T || gi >= ng) continue;
+        uint64_t ef[NMAX], et[NMAX];
+#pragma unroll
+        for (int c = 0; c < CPF; ++c) {
+            ef[2 * c] = ((uint64_t)vf[c].y << 32) | vf[c].x;
+            ef[2 * c + 1] = ((uint64_t)vf[c].w << 32) | vf[c].z;
+        }
+#pragma unroll
+        for (int c = 0; c < CPT; ++c) {
+            if constexpr (KIND == C3_EV_F64) {
+                et[2 * c] = ((uint64_t)vt[c].y << 32) | vt[c].x;
+                et[2 * c + 1] = ((uint64_t)vt[c].w << 32) | vt[c].z;
+            } else {
+                et[4 * c] = vt[c].x;
+                et[4 * c + 1] = vt[c].y;
+                et[4 * c + 2] = vt[c].z;
+                et[4 * c + 3] = vt[c].w;
+            }
+        }
+        const UnitVote vfp = exact_vote_row<NMAX>(ef, R);
+        const UnitVote vtm = statistical_vote_row<NMAX, KIND>(et, R, kappa);
+        const uint32_t bit = 1u << (t & (kSegIters - 1));
+        const int64_t w0 = (t / kSegIters) * SEGW + gi;
+        for (uint64_t b = vfp.bitmap; b != 0ull; b &= b - 1ull)
+            atomicOr(fmask + w0 + __builtin_ctzll(b) * kPassGroups, bit);
+        for (uint64_t b = vtm.bitmap; b != 0ull; b &= b - 1ull)
+            atomicOr(tmask + w0 + __builtin_ctzll(b) * kPassGroups, bit);
+    }
+    __syncthreads();
+
+    // confirmation of the workgroup's ranks (r, g0 + gi), kConfirmLanes lanes each
+    constexpr int per_pass = PassShape<NMAX>::threads / kConfirmLanes;
+#pragma unroll 1
+    for (int base = 0; base < R * kPassGroups; base += per_pass) {
+        const int lr = base + (int)threadIdx.x / kConfirmLanes;    // r * kPassGroups + gi
+        const int part = (int)threadIdx.x % kConfirmLanes;
+        const int r = lr / kPassGroups, gr = lr % kPassGroups;
+        const bool live = lr < R * kPassGroups && gr < ng;
+        const int off = live ? r * kPassGroups + gr : 0;
+        const ConfirmAcc a = confirm_lane<SHORT>(fmask + off, tmask + off, SEGW, T, Wt, part, live);
+        confirm_store(a, live, part, verdicts, (int64_t)r * G + g0 + gr);
+    }
 }
 
 int64_t timing_masks_bytes(int R, int64_t G, int64_t T) {
@@ -351,6 +514,54 @@ static hipError_t launch_votes(const uint64_t* fp, const char* tp, int time_kind
     return launch_votes<NMAX, C3_EV_F64>(fp, tp, R, G, n_units, kappa, fo, to, stream);
 }
 
+// Compute units of the stream's device (cached per device).
+static int stream_cu_count(hipStream_t stream) {
+    static std::atomic<int> cache[64];
+    hipDevice_t dev = 0;
+    if (hipStreamGetDevice(stream, &dev) != hipSuccess) {
+        (void)hipGetLastError();
+        if (hipGetDevice(&dev) != hipSuccess) return 0;
+    }
+    if (dev < 0 || dev >= 64) return 0;
+    int n = cache[dev].load(std::memory_order_relaxed);
+    if (n > 0) return n;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+    cache[dev].store(n, std::memory_order_relaxed);
+    return n;
+}
+
+template <int NMAX, int KIND>
+static hipError_t launch_pass(const char* fp, const char* tp, int64_t G, int64_t T, double kappa,
+                              int Wt, c3_rank_verdict_t* verdicts, size_t lds, hipStream_t stream) {
+    const dim3 grid((unsigned)((G + kPassGroups - 1) / kPassGroups));
+    const dim3 block(PassShape<NMAX>::threads);
+    if (Wt <= 32)
+        hipLaunchKernelGGL((timing_pass_kernel<NMAX, KIND, true>), grid, block, lds, stream, fp, tp,
+                           G, T, kappa, Wt, verdicts);
+    else
+        hipLaunchKernelGGL((timing_pass_kernel<NMAX, KIND, false>), grid, block, lds, stream, fp,
+                           tp, G, T, kappa, Wt, verdicts);
+    return hipGetLastError();
+}
+
+// The single pass applies: R is a group bound with dense 16-byte aligned rows,
+// the masks fit in LDS, and the groups give every compute unit a workgroup.
+static bool pass_applies(const void* fp, const void* times, int time_kind, int R, int64_t G,
+                         int64_t T, int Wt, hipStream_t stream, size_t& lds) {
+    if (R != 4 && R != 8 && R != 16) return false;
+    const int tsize = time_kind == C3_EV_F64 ? 8 : 4;
+    if (((uintptr_t)fp & 15) != 0 || ((uintptr_t)times & 15) != 0 || (R * tsize) % 16 != 0)
+        return false;
+    if (T < 1 || Wt > 64) return false;
+    const int64_t n_seg = (T + kSegIters - 1) / kSegIters;
+    const int64_t bytes = 2 * n_seg * R * kPassGroups * 4;
+    if (bytes > kPassMaskLds) return false;
+    const int cus = stream_cu_count(stream);
+    if (cus <= 0 || (G + kPassGroups - 1) / kPassGroups < cus) return false;
+    lds = (size_t)bytes;
+    return true;
+}
+
 hipError_t launch_timing_consensus(const uint64_t* fp, const void* times, int time_kind, int R,
                                    int64_t G, int64_t T, double kappa, int window,
                                    uint8_t* fp_status, uint64_t* fp_bitmap, int32_t* fp_majority,
@@ -360,6 +571,23 @@ hipError_t launch_timing_consensus(const uint64_t* fp, const void* times, int ti
     if ((ranks * kConfirmLanes + kConfirmThreads - 1) / kConfirmThreads > 0x7FFFFFFF)
         return hipErrorInvalidValue;
     if (ranks == 0) return hipSuccess;
+    if (fp_status == nullptr && t_status == nullptr) {
+        const int Wt = (int64_t)window < T ? window : (int)T;
+        size_t lds = 0;
+        if (pass_applies(fp, times, time_kind, R, G, T, Wt, stream, lds)) {
+            const char* f = reinterpret_cast<const char*>(fp);
+            const char* tp = static_cast<const char*>(times);
+            const bool f64 = time_kind == C3_EV_F64;
+            if (R == 4)
+                return f64 ? launch_pass<4, C3_EV_F64>(f, tp, G, T, kappa, Wt, verdicts, lds, stream)
+                           : launch_pass<4, C3_EV_F32>(f, tp, G, T, kappa, Wt, verdicts, lds, stream);
+            if (R == 8)
+                return f64 ? launch_pass<8, C3_EV_F64>(f, tp, G, T, kappa, Wt, verdicts, lds, stream)
+                           : launch_pass<8, C3_EV_F32>(f, tp, G, T, kappa, Wt, verdicts, lds, stream);
+            return f64 ? launch_pass<16, C3_EV_F64>(f, tp, G, T, kappa, Wt, verdicts, lds, stream)
+                       : launch_pass<16, C3_EV_F32>(f, tp, G, T, kappa, Wt, verdicts, lds, stream);
+        }
+    }
     const int64_t half = timing_masks_bytes(R, G, T) / 2;
     uint32_t* fm = static_cast<uint32_t*>(ws);
     uint32_t* tm = reinterpret_cast<uint32_t*>(static_cast<char*>(ws) + half);

@@ -7,8 +7,10 @@ Inputs: seeded [T][G][R] fingerprints with ranks that diverge from a seeded
 iteration on and occasional splits; lognormal step times with persistent and
 intermittent stragglers, exact ties (so the IQR and range fallbacks of the
 scale are reached) and non-finite values.  Sizes cover ragged workgroup
-tiles (G around 64, T around the 16- and 8-iteration segments), R from 1 to
-16 on the fused kernels and above 16 or W above 64 on the separate steps.
+tiles (G around 64, T around the 32-iteration mask segments), R from 1 to 16
+on the fused kernels and above 16 or W above 64 on the separate steps, and
+the single-pass kernel's shapes (G of 4096 and more, ragged 16-group
+workgroups, T up to its LDS limit).
 """
 import numpy as np
 import pytest
@@ -100,11 +102,30 @@ CASES = [
 ]
 
 
-@pytest.mark.parametrize("R,G,T,W,f64", CASES)
+# Shapes of the single-pass kernel (taken when no per-unit results are
+# requested): R a group bound (4, 8, 16), at least one 16-group workgroup per
+# compute unit (G >= 4081 on 256 CUs), masks within the LDS budget (T <= 2048
+# at R = 8).  Ragged G leaves the last workgroup 1-15 groups; ragged T leaves
+# a partial 4-iteration step and a partial 32-iteration mask segment.
+PASS_CASES = [
+    (8, 4096, 40, 16, False), (8, 4100, 37, 16, False), (8, 4100, 129, 33, True),
+    (4, 4100, 70, 5, False), (4, 4097, 33, 64, True), (16, 4100, 45, 16, False),
+    (16, 4096, 20, 1, True), (8, 4096, 1, 16, False), (8, 4111, 2048, 16, False),
+]
+
+
+@pytest.mark.parametrize("R,G,T,W,f64", CASES + PASS_CASES[:3])
 def test_timing_consensus_matches_oracle(R, G, T, W, f64):
     _case("timing", R, G, T, W, f64)
     fp, tau = _inputs(R, G, T, seed=R * 1000 + G * 7 + T, f64=f64)
     _check(fp, tau, W)
+
+
+@pytest.mark.parametrize("R,G,T,W,f64", PASS_CASES)
+def test_timing_consensus_single_pass_matches_oracle(R, G, T, W, f64):
+    _case("timing single pass", R, G, T, W, f64)
+    fp, tau = _inputs(R, G, T, seed=R * 1000 + G * 7 + T, f64=f64)
+    _check(fp, tau, W, per_unit=False)
 
 
 @pytest.mark.parametrize("R,G,T,W", [(8, 100, 70, 16), (12, 70, 50, 16), (20, 10, 30, 16)])
@@ -114,19 +135,22 @@ def test_timing_consensus_without_per_unit_outputs(R, G, T, W):
     _check(fp, tau, W, per_unit=False)
 
 
+@pytest.mark.parametrize("G,per_unit", [(3, True), (4096, False)])
 @pytest.mark.parametrize("W", [1, 2, 16])
 @pytest.mark.parametrize("t0", [31, 63, 64, 127, 255])
-def test_timing_consensus_pair_across_lane_boundary(W, t0):
+def test_timing_consensus_pair_across_lane_boundary(W, t0, G, per_unit):
     # T = 300 splits into lanes of 64 iterations: slowness at t0 and t0 + 1
-    # straddles a lane boundary when t0 + 1 is a multiple of 64.
-    _case("timing pair", W, t0)
-    R, G, T = 8, 3, 300
+    # straddles a lane boundary when t0 + 1 is a multiple of 64.  G = 4096
+    # without per-unit results takes the single-pass kernel, G = 3 the three
+    # launches.
+    _case("timing pair", W, t0, G, per_unit)
+    R, T = 8, 300
     rng = np.random.default_rng(t0 * 10 + W)
     fp = np.repeat(rng.integers(-(2 ** 63), 2 ** 63 - 1, size=(T, G, 1), dtype=np.int64), R,
                    axis=2)
     tau = np.exp(rng.normal(0.0, 0.01, size=(T, G, R))).astype(np.float32)
     tau[t0:t0 + 2, 1, 5] = 4.0
-    v = _check(fp, tau, W)
+    v = _check(fp, tau, W, per_unit=per_unit)
     rank = 5 * G + 1
     assert v["flags"][rank] & c3.RANK_CONSEC2
     assert v["slow_count"][rank] >= 2
