@@ -10,6 +10,10 @@
 
 namespace c3 {
 
+// Compute units of the device `stream` runs on (cached per device; 0 if the
+// runtime cannot tell).
+int stream_cu_count(hipStream_t stream);
+
 static_assert(sizeof(c3_outlier_t) == 80, "outlier layout");
 static_assert(sizeof(c3_rank_verdict_t) == 24, "verdict layout");
 

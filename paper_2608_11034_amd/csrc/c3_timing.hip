@@ -14,8 +14,6 @@
 #include "c3_internal.h"
 #include "c3_vote_row.h"
 
-#include <atomic>
-
 namespace c3 {
 
 constexpr int kVoteThreads = 256;
@@ -512,22 +510,6 @@ static hipError_t launch_votes(const uint64_t* fp, const char* tp, int time_kind
     if (time_kind == C3_EV_F32)
         return launch_votes<NMAX, C3_EV_F32>(fp, tp, R, G, n_units, kappa, fo, to, stream);
     return launch_votes<NMAX, C3_EV_F64>(fp, tp, R, G, n_units, kappa, fo, to, stream);
-}
-
-// Compute units of the stream's device (cached per device).
-static int stream_cu_count(hipStream_t stream) {
-    static std::atomic<int> cache[64];
-    hipDevice_t dev = 0;
-    if (hipStreamGetDevice(stream, &dev) != hipSuccess) {
-        (void)hipGetLastError();
-        if (hipGetDevice(&dev) != hipSuccess) return 0;
-    }
-    if (dev < 0 || dev >= 64) return 0;
-    int n = cache[dev].load(std::memory_order_relaxed);
-    if (n > 0) return n;
-    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
-    cache[dev].store(n, std::memory_order_relaxed);
-    return n;
 }
 
 template <int NMAX, int KIND>
