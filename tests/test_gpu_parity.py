@@ -110,19 +110,25 @@ def test_tensor_signatures_match_oracle(k):
     assert np.array_equal(mj.cpu().numpy(), omj)
 
 
-def test_three_step_protocol_on_gpu():
-    _print_case("three-step protocol")
-    w = workloads.make(3, device=DEV, scale="small")
+@pytest.mark.parametrize("k", [1, 2, 3, 4])
+def test_three_step_protocol_on_gpu(k):
+    """Fault-injection protocol of the paper's evaluation: clean replicas give
+    no outlier and no undecided chunk, the planted faults give exactly their
+    (replica, chunk) pairs and split chunks, and removing them gives nothing
+    again."""
+    _print_case("three-step protocol", k)
+    w = workloads.make(k, device=DEV, scale="small")
     faulty = [list(rep) for rep in w.replicas]
-    src = next(r for r in range(w.R) if all(f.replica != r for f in w.faults))
+    faulted = {f.replica for f in w.faults} | {f.replica for f in w.split_faults}
+    src = next(r for r in range(w.R) if r not in faulted)
     clean = [[t.clone() for t in w.replicas[src]] for _ in range(w.R)]
-    want_out, _ = _expected(w)
+    want_out, want_und = _expected(w)
     for step, reps in (("clean", clean), ("fault", faulty), ("clean-again", clean)):
         w.replicas = reps
         g = _gpu_pipeline(w)
         got = set(zip(g["outliers"]["replica"].tolist(), g["outliers"]["chunk"].tolist()))
         assert got == (want_out if step == "fault" else set()), step
-        assert g["counts"][1] == 0
+        assert set(g["undecided"].tolist()) == (want_und if step == "fault" else set()), step
 
 
 # ---------------------------------------------------------------------------
