@@ -203,3 +203,18 @@ def test_rotating_slice_matches_oracle(numel, S):
     from oracle import adamw
     for k in range(-(-numel // S) * 2 + 1):
         assert c3.optimizer_slice(k, numel, S) == adamw.slice_bounds(k, numel, S)
+
+
+@pytest.mark.parametrize("header", ["c3.h", "c3_oob.h"])
+@pytest.mark.parametrize("compiler", [["gcc", "-x", "c", "-std=c99"], ["g++", "-x", "c++", "-std=c++17"]])
+def test_public_headers_compile_alone(header, compiler, tmp_path):
+    """Each public header is self-contained plain C (and C++): it needs no
+    HIP header, so a C client can include it with any host compiler."""
+    import subprocess
+    src = tmp_path / "use.c"
+    src.write_text(f'#include "{header}"\nint main(void) {{ return 0; }}\n')
+    r = subprocess.run(compiler + ["-Wall", "-Wextra", "-Werror", "-pedantic",
+                                   "-I", os.path.join(ROOT, "include"), str(src),
+                                   "-o", str(tmp_path / "use")],
+                       capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
