@@ -315,6 +315,9 @@ size_t c3_optimizer_check_workspace_size(const c3_optimizer_state_t *st);
  *      four input slices, read in place, and the three updated slices),
  *      one chunk each;
  *   3. c3_consensus (exact) over the seven units; 4. c3_localize.
+ * The outputs are those of these four calls; after the streaming kernel of
+ * step 2, one single-workgroup kernel combines the tile partials into the
+ * records, votes and writes the lists (R <= 64: always).
  * Healthy data-parallel replicas agree on all seven units; an outlier on an
  * input unit names replicas whose state diverged before the step, one on an
  * output unit only names replicas whose replayed update differs.

@@ -57,10 +57,22 @@ __device__ __forceinline__ Upd adamw_one(const AdamwConst& c, float p, float g, 
 
 }  // namespace
 
+// Copies n16 16-byte words from src to dst across the whole grid (the staged
+// plan of the signature pass that follows the replay).
+__device__ __forceinline__ void copy_staged(const uint4* __restrict__ src, uint4* __restrict__ dst,
+                                            int64_t n16) {
+    const int64_t stride = (int64_t)gridDim.x * gridDim.y * 256;
+    for (int64_t j = ((int64_t)blockIdx.y * gridDim.x + blockIdx.x) * 256 + threadIdx.x; j < n16;
+         j += stride)
+        dst[j] = src[j];
+}
+
 __global__ void __launch_bounds__(256) adamw_slice_kernel(AdamwPtrs ptrs, AdamwConst c,
                                                           int64_t offset, int64_t n,
-                                                          float* __restrict__ out,
-                                                          int64_t stride) {
+                                                          float* __restrict__ out, int64_t stride,
+                                                          const uint4* plan_src, uint4* plan_dst,
+                                                          int64_t plan_n16) {
+    copy_staged(plan_src, plan_dst, plan_n16);
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
     const int r = blockIdx.y;
     if (i >= n) return;
@@ -77,7 +89,10 @@ __global__ void __launch_bounds__(256) adamw_slice_kernel(AdamwPtrs ptrs, AdamwC
 __global__ void __launch_bounds__(256) adamw_slice_vec4_kernel(AdamwPtrs ptrs, AdamwConst c,
                                                                int64_t offset, int64_t n,
                                                                float* __restrict__ out,
-                                                               int64_t stride) {
+                                                               int64_t stride,
+                                                               const uint4* plan_src,
+                                                               uint4* plan_dst, int64_t plan_n16) {
+    copy_staged(plan_src, plan_dst, plan_n16);
     const int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x;  // element quad
     const int r = blockIdx.y;
     if (4 * q >= n) return;
@@ -99,17 +114,21 @@ __global__ void __launch_bounds__(256) adamw_slice_vec4_kernel(AdamwPtrs ptrs, A
 
 hipError_t launch_adamw_slice(const AdamwPtrs& ptrs, const AdamwConst& c, int R, bool vec4,
                               int64_t offset, int64_t n, float* out, int64_t stride,
-                              hipStream_t stream) {
-    if (n <= 0) return hipSuccess;
+                              hipStream_t stream, const void* plan_src, void* plan_dst,
+                              size_t plan_bytes) {
+    const int64_t n16 = plan_src != nullptr ? (int64_t)((plan_bytes + 15) / 16) : 0;
+    if (n <= 0) return n16 > 0 ? launch_plan_fetch(plan_src, plan_dst, plan_bytes, stream) : hipSuccess;
     const int64_t threads = vec4 ? n / 4 : n;
     const int64_t blocks = (threads + 255) / 256;
     if (blocks > 0x7FFFFFFF || R > 65535) return hipErrorInvalidValue;
+    const uint4* src = static_cast<const uint4*>(plan_src);
+    uint4* dst = static_cast<uint4*>(plan_dst);
     if (vec4)
         hipLaunchKernelGGL(adamw_slice_vec4_kernel, dim3((unsigned)blocks, (unsigned)R), dim3(256), 0,
-                           stream, ptrs, c, offset, n, out, stride);
+                           stream, ptrs, c, offset, n, out, stride, src, dst, n16);
     else
         hipLaunchKernelGGL(adamw_slice_kernel, dim3((unsigned)blocks, (unsigned)R), dim3(256), 0,
-                           stream, ptrs, c, offset, n, out, stride);
+                           stream, ptrs, c, offset, n, out, stride, src, dst, n16);
     return hipGetLastError();
 }
 

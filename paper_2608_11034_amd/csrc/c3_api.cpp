@@ -6,6 +6,7 @@
 #include <string.h>
 
 #include <atomic>
+#include <functional>
 #include <mutex>
 #include <vector>
 
@@ -175,12 +176,20 @@ struct Stager {
 Stager g_stagers[kMaxDevices];
 
 // Copies `bytes` of `src` to device `dst` on `s`; returns a HIP error code.
-hipError_t stage_to_device(void* dst, const void* src, size_t bytes, hipStream_t s) {
+// `enqueue(h)` launches the kernel that copies the staged bytes from the
+// pinned slot h to dst (with whatever else it does); when staging falls back
+// to a pageable copy, that copy is enqueued first and enqueue(nullptr)
+// after it.
+hipError_t stage_to_device(void* dst, const void* src, size_t bytes, hipStream_t s,
+                           const std::function<hipError_t(const void*)>& enqueue) {
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return e;
-    if (dev < 0 || dev >= kMaxDevices || bytes > kStageSlotBytes)
-        return hipMemcpyAsync(dst, src, bytes, hipMemcpyHostToDevice, s);
+    auto pageable = [&]() {
+        hipError_t e2 = hipMemcpyAsync(dst, src, bytes, hipMemcpyHostToDevice, s);
+        return e2 != hipSuccess ? e2 : enqueue(nullptr);
+    };
+    if (dev < 0 || dev >= kMaxDevices || bytes > kStageSlotBytes) return pageable();
     Stager& st = g_stagers[dev];
     std::lock_guard<std::mutex> lock(st.mu);
     if (!st.ready && !st.failed) {
@@ -194,16 +203,22 @@ hipError_t stage_to_device(void* dst, const void* src, size_t bytes, hipStream_t
             st.ready = !st.failed;
         }
     }
-    if (!st.ready) return hipMemcpyAsync(dst, src, bytes, hipMemcpyHostToDevice, s);
+    if (!st.ready) return pageable();
     const int slot = st.next;
     st.next = (st.next + 1) % kStageSlots;
     if (st.pending[slot] && (e = hipEventSynchronize(st.ev[slot])) != hipSuccess) return e;
     unsigned char* h = st.host + (size_t)slot * kStageSlotBytes;
     memcpy(h, src, bytes);
-    if ((e = c3::launch_plan_fetch(h, dst, bytes, s)) != hipSuccess) return e;
+    if ((e = enqueue(h)) != hipSuccess) return e;
     if ((e = hipEventRecord(st.ev[slot], s)) != hipSuccess) return e;
     st.pending[slot] = true;
     return hipSuccess;
+}
+
+hipError_t stage_to_device(void* dst, const void* src, size_t bytes, hipStream_t s) {
+    return stage_to_device(dst, src, bytes, s, [&](const void* h) {
+        return h != nullptr ? c3::launch_plan_fetch(h, dst, bytes, s) : hipSuccess;
+    });
 }
 
 }  // namespace
@@ -242,12 +257,15 @@ size_t c3_signature_workspace_size_ex(const c3_tensor_meta_t* metas, int T, int 
     return make_plan(metas, T, R, chunk_bytes, tile_bytes, p) == C3_OK ? (size_t)p.h.total_bytes : 0;
 }
 
-int c3_signature_ex(const void* const* ptrs, const c3_tensor_meta_t* metas, int T, int R,
-                    uint64_t chunk_bytes, c3_chunk_record_t* records, void* ws, size_t ws_bytes,
-                    c3_stream_t stream, const c3_launch_opts_t* opts) {
+}  // extern "C"
+
+namespace {
+
+// Argument checks, the plan and the bytes to stage into the workspace.
+int prepare_signature(const void* const* ptrs, const c3_tensor_meta_t* metas, int T, int R,
+                      uint64_t chunk_bytes, c3_chunk_record_t* records, void* ws, size_t ws_bytes,
+                      uint64_t tile, Plan& p, std::vector<unsigned char>& buf) {
     if (ptrs == nullptr || records == nullptr) return C3_E_INVAL;
-    Plan p;
-    const uint64_t tile = opts ? opts->tile_bytes : 0;
     const int rc = make_plan(metas, T, R, chunk_bytes, tile, p);
     if (rc != C3_OK) return rc;
     if (ws == nullptr || !aligned(ws, 256) || ws_bytes < p.h.total_bytes) return C3_E_WORKSPACE;
@@ -259,8 +277,8 @@ int c3_signature_ex(const void* const* ptrs, const c3_tensor_meta_t* metas, int 
             if (q == nullptr) return C3_E_INVAL;
             if (!aligned(q, 16)) return C3_E_ALIGN;
         }
-    // stage the plan: header, pointer table, bases, tensor info
-    std::vector<unsigned char> buf(align_up(p.h.off_partials, 16), 0);
+    // the plan: header, pointer table, bases, tensor info
+    buf.assign(align_up(p.h.off_partials, 16), 0);
     memcpy(buf.data(), &p.h, sizeof(SigPlan));
     for (size_t i = 0; i < (size_t)R * (size_t)T; ++i) {
         const uint64_t a = (uint64_t)(uintptr_t)ptrs[i];
@@ -271,17 +289,88 @@ int c3_signature_ex(const void* const* ptrs, const c3_tensor_meta_t* metas, int 
     memcpy(buf.data() + p.h.off_tmeta, p.tinfo.data(), sizeof(TensorInfo) * (size_t)T);
     memcpy(buf.data() + p.h.off_order, p.order.data(), 4ull * T);
     memcpy(buf.data() + p.h.off_gtile, p.gtile.data(), 8ull * (T + 1));
+    return C3_OK;
+}
+
+// Argument checks and fp32 factors of one AdamW replay (nothing launched);
+// out_stride 0 means n.
+int adamw_prepare(const float* const* param, const float* const* grad,
+                  const float* const* exp_avg, const float* const* exp_avg_sq, int R,
+                  int64_t numel, int64_t offset, int64_t n, const c3_adamw_hparams_t* hp,
+                  float* out, int64_t& out_stride, c3::AdamwPtrs& ptrs, c3::AdamwConst& c,
+                  bool& vec4) {
+    if (param == nullptr || grad == nullptr || exp_avg == nullptr || exp_avg_sq == nullptr ||
+        hp == nullptr || R < 1 || R > C3_MAX_REPLICAS || numel < 0 || offset < 0 || n < 0 ||
+        offset > numel || n > numel - offset || hp->step < 1)
+        return C3_E_INVAL;
+    if (out_stride == 0) out_stride = n;
+    if (out_stride < n) return C3_E_INVAL;
+    if (!(hp->lr >= 0.0) || !(hp->beta1 >= 0.0 && hp->beta1 < 1.0) ||
+        !(hp->beta2 >= 0.0 && hp->beta2 < 1.0) || !(hp->eps > 0.0) || !(hp->weight_decay >= 0.0))
+        return C3_E_INVAL;
+    if (n == 0) return C3_OK;
+    if (out == nullptr) return C3_E_INVAL;
+    if (!aligned(out, 4)) return C3_E_ALIGN;
+    memset(&ptrs, 0, sizeof(ptrs));
+    for (int r = 0; r < R; ++r) {
+        if (param[r] == nullptr || grad[r] == nullptr || exp_avg[r] == nullptr ||
+            exp_avg_sq[r] == nullptr)
+            return C3_E_INVAL;
+        if (!aligned(param[r], 4) || !aligned(grad[r], 4) || !aligned(exp_avg[r], 4) ||
+            !aligned(exp_avg_sq[r], 4))
+            return C3_E_ALIGN;
+        ptrs.param[r] = param[r];
+        ptrs.grad[r] = grad[r];
+        ptrs.exp_avg[r] = exp_avg[r];
+        ptrs.exp_avg_sq[r] = exp_avg_sq[r];
+    }
+    // scalar factors in fp64, rounded once to fp32
+    const double t = (double)hp->step;
+    c.decay = (float)(1.0 - hp->lr * hp->weight_decay);
+    c.w = (float)(1.0 - hp->beta1);
+    c.one_minus_w = 1.0f - c.w;
+    c.lerp_small = fabsf(c.w) < 0.5f;
+    c.beta2 = (float)hp->beta2;
+    c.c2 = (float)(1.0 - hp->beta2);
+    c.s2 = (float)sqrt(1.0 - pow(hp->beta2, t));
+    c.eps = (float)hp->eps;
+    c.neg_step = -(float)(hp->lr / (1.0 - pow(hp->beta1, t)));
+    vec4 = offset % 4 == 0 && n % 4 == 0 && out_stride % 4 == 0 && aligned(out, 16);
+    for (int r = 0; r < R && vec4; ++r)
+        vec4 = aligned(param[r], 16) && aligned(grad[r], 16) && aligned(exp_avg[r], 16) &&
+               aligned(exp_avg_sq[r], 16);
+    return C3_OK;
+}
+
+int signature_impl(const void* const* ptrs, const c3_tensor_meta_t* metas, int T, int R,
+                   uint64_t chunk_bytes, c3_chunk_record_t* records, void* ws, size_t ws_bytes,
+                   c3_stream_t stream, const c3_launch_opts_t* opts) {
+    Plan p;
+    std::vector<unsigned char> buf;
+    const int rc = prepare_signature(ptrs, metas, T, R, chunk_bytes, records, ws, ws_bytes,
+                                     opts ? opts->tile_bytes : 0, p, buf);
+    if (rc != C3_OK) return rc;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     const bool staged = opts != nullptr && (opts->flags & C3_OPT_PLAN_STAGED) != 0;
     if (!staged && stage_to_device(ws, buf.data(), buf.size(), s) != hipSuccess) return C3_E_HIP;
     // the end event follows the whole pass: the streaming kernels and, for
     // tiled plans, the combine of their partials
     hipError_t e = c3::launch_signature(
-        static_cast<const SigPlan*>(ws), p.h, p.groups, records, opts ? opts->grid_blocks : 0, s,
-        opts ? reinterpret_cast<hipEvent_t>(opts->ev_kernel_begin) : nullptr, nullptr);
+        static_cast<const SigPlan*>(ws), p.h, p.groups, records, opts ? opts->grid_blocks : 0,
+        true, s, opts ? reinterpret_cast<hipEvent_t>(opts->ev_kernel_begin) : nullptr, nullptr);
     if (e == hipSuccess && opts != nullptr && opts->ev_kernel_end != nullptr)
         e = hipEventRecord(reinterpret_cast<hipEvent_t>(opts->ev_kernel_end), s);
     return e == hipSuccess ? C3_OK : C3_E_HIP;
+}
+
+}  // namespace
+
+extern "C" {
+
+int c3_signature_ex(const void* const* ptrs, const c3_tensor_meta_t* metas, int T, int R,
+                    uint64_t chunk_bytes, c3_chunk_record_t* records, void* ws, size_t ws_bytes,
+                    c3_stream_t stream, const c3_launch_opts_t* opts) {
+    return signature_impl(ptrs, metas, T, R, chunk_bytes, records, ws, ws_bytes, stream, opts);
 }
 
 int c3_signature(const void* const* ptrs, const c3_tensor_meta_t* metas, int T, int R,
@@ -305,48 +394,12 @@ int c3_adamw_slice(const float* const* param, const float* const* grad, const fl
                    const float* const* exp_avg_sq, int R, int64_t numel, int64_t offset, int64_t n,
                    const c3_adamw_hparams_t* hp, float* out, int64_t out_stride,
                    c3_stream_t stream) {
-    if (param == nullptr || grad == nullptr || exp_avg == nullptr || exp_avg_sq == nullptr ||
-        hp == nullptr || R < 1 || R > C3_MAX_REPLICAS || numel < 0 || offset < 0 || n < 0 ||
-        offset > numel || n > numel - offset || hp->step < 1)
-        return C3_E_INVAL;
-    if (out_stride == 0) out_stride = n;
-    if (out_stride < n) return C3_E_INVAL;
-    if (!(hp->lr >= 0.0) || !(hp->beta1 >= 0.0 && hp->beta1 < 1.0) ||
-        !(hp->beta2 >= 0.0 && hp->beta2 < 1.0) || !(hp->eps > 0.0) || !(hp->weight_decay >= 0.0))
-        return C3_E_INVAL;
-    if (n == 0) return C3_OK;
-    if (out == nullptr) return C3_E_INVAL;
-    if (!aligned(out, 4)) return C3_E_ALIGN;
     c3::AdamwPtrs ptrs;
-    memset(&ptrs, 0, sizeof(ptrs));
-    for (int r = 0; r < R; ++r) {
-        if (param[r] == nullptr || grad[r] == nullptr || exp_avg[r] == nullptr ||
-            exp_avg_sq[r] == nullptr)
-            return C3_E_INVAL;
-        if (!aligned(param[r], 4) || !aligned(grad[r], 4) || !aligned(exp_avg[r], 4) ||
-            !aligned(exp_avg_sq[r], 4))
-            return C3_E_ALIGN;
-        ptrs.param[r] = param[r];
-        ptrs.grad[r] = grad[r];
-        ptrs.exp_avg[r] = exp_avg[r];
-        ptrs.exp_avg_sq[r] = exp_avg_sq[r];
-    }
-    // scalar factors in fp64, rounded once to fp32
     c3::AdamwConst c;
-    const double t = (double)hp->step;
-    c.decay = (float)(1.0 - hp->lr * hp->weight_decay);
-    c.w = (float)(1.0 - hp->beta1);
-    c.one_minus_w = 1.0f - c.w;
-    c.lerp_small = fabsf(c.w) < 0.5f;
-    c.beta2 = (float)hp->beta2;
-    c.c2 = (float)(1.0 - hp->beta2);
-    c.s2 = (float)sqrt(1.0 - pow(hp->beta2, t));
-    c.eps = (float)hp->eps;
-    c.neg_step = -(float)(hp->lr / (1.0 - pow(hp->beta1, t)));
-    bool vec4 = offset % 4 == 0 && n % 4 == 0 && out_stride % 4 == 0 && aligned(out, 16);
-    for (int r = 0; r < R && vec4; ++r)
-        vec4 = aligned(param[r], 16) && aligned(grad[r], 16) && aligned(exp_avg[r], 16) &&
-               aligned(exp_avg_sq[r], 16);
+    bool vec4 = false;
+    const int rc = adamw_prepare(param, grad, exp_avg, exp_avg_sq, R, numel, offset, n, hp, out,
+                                 out_stride, ptrs, c, vec4);
+    if (rc != C3_OK || n == 0) return rc;
     const hipError_t e = c3::launch_adamw_slice(ptrs, c, R, vec4, offset, n, out, out_stride,
                                                 reinterpret_cast<hipStream_t>(stream));
     return e == hipSuccess ? C3_OK : C3_E_HIP;
@@ -487,9 +540,14 @@ int c3_optimizer_check(const c3_optimizer_state_t* st, int64_t k, const c3_adamw
     const int64_t off = (k % n_slices) * S;
     const int64_t n = st->numel - off < S ? st->numel - off : S;
     for (int i = 0; i < 7; ++i) metas[i].shape[0] = n;
+    if (!c3::small_tail_fits(R, 7)) return C3_E_UNSUPPORTED;
     // the replay writes row (r, j) at updated + (3 r + j) S
-    rc = c3_adamw_slice(st->param, st->grad, st->exp_avg, st->exp_avg_sq, R, st->numel, off, n,
-                        hp, out->updated, S, stream);
+    c3::AdamwPtrs aptrs;
+    c3::AdamwConst ac;
+    bool vec4 = false;
+    int64_t ostride = S;
+    rc = adamw_prepare(st->param, st->grad, st->exp_avg, st->exp_avg_sq, R, st->numel, off, n, hp,
+                       out->updated, ostride, aptrs, ac, vec4);
     if (rc != C3_OK) return rc;
     const void* ptrs[7 * C3_MAX_REPLICAS];
     for (int r = 0; r < R; ++r) {
@@ -500,19 +558,26 @@ int c3_optimizer_check(const c3_optimizer_state_t* st, int64_t k, const c3_adamw
         row[3] = st->exp_avg_sq[r] + off;
         for (int j = 0; j < 3; ++j) row[4 + j] = out->updated + (3 * (int64_t)r + j) * S;
     }
-    c3_launch_opts_t opts;
-    memset(&opts, 0, sizeof(opts));
-    opts.tile_bytes = tile;
     const uint64_t sig_ws = align_up(optimizer_sig_ws(st, metas, chunk, tile), 256);
-    rc = c3_signature_ex(ptrs, metas, 7, R, chunk, out->records, ws, sig_ws, stream, &opts);
+    Plan p;
+    std::vector<unsigned char> buf;
+    rc = prepare_signature(ptrs, metas, 7, R, chunk, out->records, ws, sig_ws, tile, p, buf);
     if (rc != C3_OK) return rc;
-    rc = c3_consensus(out->records, C3_EV_U64, 7 * (int64_t)sizeof(c3_chunk_record_t),
-                      (int64_t)sizeof(c3_chunk_record_t), R, 7, C3_EXACT, C3_KAPPA_DEFAULT,
-                      out->status, out->bitmap, out->majority_idx, stream);
-    if (rc != C3_OK) return rc;
-    return c3_localize(out->status, out->bitmap, out->majority_idx, out->records, R, 7,
-                       out->outliers, 7 * (int64_t)R, out->undecided, 7, out->counts,
-                       static_cast<unsigned char*>(ws) + sig_ws, ws_bytes - sig_ws, stream);
+    // Three launches: the replay, which also copies the staged signature
+    // plan into the workspace; the streaming signature kernel; one workgroup
+    // that combines tile partials into records, votes and writes the lists.
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    hipError_t e = stage_to_device(ws, buf.data(), buf.size(), s, [&](const void* h) {
+        return c3::launch_adamw_slice(aptrs, ac, R, vec4, off, n, out->updated, S, s, h,
+                                      h != nullptr ? ws : nullptr, h != nullptr ? buf.size() : 0);
+    });
+    const SigPlan* dplan = static_cast<const SigPlan*>(ws);
+    if (e == hipSuccess)
+        e = c3::launch_signature(dplan, p.h, p.groups, out->records, 0, false, s, nullptr, nullptr);
+    if (e == hipSuccess)
+        e = c3::launch_small_tail(dplan, out->records, out->status, out->bitmap, out->majority_idx,
+                                  out->outliers, 7 * (int64_t)R, out->undecided, 7, out->counts, s);
+    return e == hipSuccess ? C3_OK : C3_E_HIP;
 }
 
 // ---------------------------------------------------------------------------

@@ -17,9 +17,19 @@ int stream_cu_count(hipStream_t stream);
 static_assert(sizeof(c3_outlier_t) == 80, "outlier layout");
 static_assert(sizeof(c3_rank_verdict_t) == 24, "verdict layout");
 
+// finalize: combine tile partials into records when a chunk spans several
+// tiles (false leaves that to launch_small_tail).
 hipError_t launch_signature(const SigPlan* dplan, const SigPlan& hplan, const SigGroups& groups,
-                            c3_chunk_record_t* records, int grid_blocks, hipStream_t stream,
-                            hipEvent_t ev0, hipEvent_t ev1);
+                            c3_chunk_record_t* records, int grid_blocks, bool finalize,
+                            hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1);
+
+// Records (from partials unless chunks are whole tiles), exact votes and
+// lists of a small plan in one workgroup; see small_tail_fits.
+bool small_tail_fits(int R, int64_t C);
+hipError_t launch_small_tail(const SigPlan* dplan, c3_chunk_record_t* records, uint8_t* status,
+                             uint64_t* bitmap, int32_t* majority, c3_outlier_t* outliers,
+                             int64_t out_cap, int64_t* undecided, int64_t und_cap, int64_t* counts,
+                             hipStream_t stream);
 
 // Copies `bytes` (rounded up to 16) from pinned, device-visible host memory
 // to device memory with a kernel on `stream`.
@@ -39,9 +49,12 @@ struct AdamwConst {
     float decay, w, one_minus_w, beta2, c2, s2, eps, neg_step;
     int lerp_small;
 };
+// With plan_src set, the same launch also copies plan_bytes (rounded up to
+// 16) from plan_src (pinned host memory) to plan_dst.
 hipError_t launch_adamw_slice(const AdamwPtrs& ptrs, const AdamwConst& c, int R, bool vec4,
                               int64_t offset, int64_t n, float* out, int64_t stride,
-                              hipStream_t stream);
+                              hipStream_t stream, const void* plan_src = nullptr,
+                              void* plan_dst = nullptr, size_t plan_bytes = 0);
 
 // Fused timing consensus (R <= 16, window <= 64): vote both evidence kinds
 // per (iteration, group), collect per-rank outlier bits, confirm per rank.

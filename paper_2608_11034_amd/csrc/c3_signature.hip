@@ -36,6 +36,7 @@
 // classifies every element.  Healthy data never takes that path.
 #include "c3_device.h"
 #include "c3_internal.h"
+#include "c3_vote_row.h"
 
 namespace c3 {
 
@@ -361,33 +362,138 @@ __global__ void __launch_bounds__(kSigThreads, C3_SIG_WAVES_PER_EU)
     }
 }
 
-// Combine the partials of each (replica, chunk) in tile order.
-__global__ void __launch_bounds__(256) finalize_kernel(const SigPlan* __restrict__ plan,
-                                                       c3_chunk_record_t* __restrict__ records) {
+// Record of (replica r, chunk c) from its tile partials, combined in tile
+// order.
+__device__ inline void combine_chunk(const SigPlan* __restrict__ plan, int64_t r, int64_t c,
+                                     c3_chunk_record_t* out) {
     const char* pb = reinterpret_cast<const char*>(plan);
     const int64_t* tile_base = reinterpret_cast<const int64_t*>(pb + plan->off_tile_base);
     const int64_t* chunk_base = reinterpret_cast<const int64_t*>(pb + plan->off_chunk_base);
     const TensorInfo* tinfo = reinterpret_cast<const TensorInfo*>(pb + plan->off_tmeta);
     const TilePartial* partials = reinterpret_cast<const TilePartial*>(pb + plan->off_partials);
+    const int t = find_segment(chunk_base, plan->T, c);
+    const uint64_t k = (uint64_t)(c - chunk_base[t]);
+    const uint64_t nbytes = tinfo[t].nbytes;
+    const int64_t tiles_t = tile_base[t + 1] - tile_base[t];
+    const int64_t lt0 = (int64_t)k * plan->tiles_per_chunk;
+    const int64_t nt = min((int64_t)plan->tiles_per_chunk, tiles_t - lt0);
+    const TilePartial* pp = partials + r * plan->tiles_per_replica + tile_base[t] + lt0;
+    TilePartial p = pp[0];
+    for (int64_t x = 1; x < nt; ++x) partial_add(p, pp[x]);
+    const uint64_t coff = k * plan->chunk_bytes;
+    const uint64_t n = nbytes > coff ? min(plan->chunk_bytes, nbytes - coff) : 0;
+    write_record(out, tinfo + t, t, k, n, p);
+}
+
+// Combine the partials of each (replica, chunk) in tile order.
+__global__ void __launch_bounds__(256) finalize_kernel(const SigPlan* __restrict__ plan,
+                                                       c3_chunk_record_t* __restrict__ records) {
     const int64_t C = plan->C;
     const int64_t total = C * plan->R;
     for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
          idx += (int64_t)gridDim.x * blockDim.x) {
         const int64_t r = idx / C;
-        const int64_t c = idx - r * C;
-        const int t = find_segment(chunk_base, plan->T, c);
-        const uint64_t k = (uint64_t)(c - chunk_base[t]);
-        const uint64_t nbytes = tinfo[t].nbytes;
-        const int64_t tiles_t = tile_base[t + 1] - tile_base[t];
-        const int64_t lt0 = (int64_t)k * plan->tiles_per_chunk;
-        const int64_t nt = min((int64_t)plan->tiles_per_chunk, tiles_t - lt0);
-        const TilePartial* pp = partials + r * plan->tiles_per_replica + tile_base[t] + lt0;
-        TilePartial p = pp[0];
-        for (int64_t x = 1; x < nt; ++x) partial_add(p, pp[x]);
-        const uint64_t coff = k * plan->chunk_bytes;
-        const uint64_t n = nbytes > coff ? min(plan->chunk_bytes, nbytes - coff) : 0;
-        write_record(&records[idx], tinfo + t, t, k, n, p);
+        combine_chunk(plan, r, idx - r * C, &records[idx]);
     }
+}
+
+// ---------------------------------------------------------------------------
+// Finalize, exact vote and localize of a small plan in one workgroup (the
+// optimizer-boundary check signs 7 chunks per replica): three launches of a
+// few microseconds each become one.  (1) Every record -- combined from its
+// tile partials, or as the streaming kernel wrote it when chunks are whole
+// tiles -- is written out and kept in LDS.  (2) One thread per chunk votes
+// with exact_vote_row, the rule c3_consensus applies, on the signatures.
+// (3) One thread lists the outliers (chunk ascending, replica ascending,
+// both replicas' summaries) and the undecided chunks, with the counts, as
+// c3_localize does.  Needs R * C <= kTailMaxRecords and C <= kTailThreads.
+// ---------------------------------------------------------------------------
+constexpr int kTailThreads = 256;
+constexpr int kTailMaxRecords = 512;
+
+__global__ void __launch_bounds__(kTailThreads) small_tail_kernel(
+    const SigPlan* __restrict__ plan, c3_chunk_record_t* __restrict__ records,
+    uint8_t* __restrict__ status, uint64_t* __restrict__ bitmap, int32_t* __restrict__ majority,
+    c3_outlier_t* __restrict__ outliers, int64_t out_cap, int64_t* __restrict__ undecided,
+    int64_t und_cap, int64_t* __restrict__ counts) {
+    __shared__ c3_chunk_record_t rec[kTailMaxRecords];
+    __shared__ UnitVote votes[kTailThreads];
+    const int R = plan->R;
+    const int C = (int)plan->C;
+    for (int i = threadIdx.x; i < R * C; i += kTailThreads) {
+        if (plan->direct) {
+            rec[i] = records[i];
+        } else {
+            combine_chunk(plan, i / C, i % C, &rec[i]);
+            records[i] = rec[i];
+        }
+    }
+    __syncthreads();
+    if ((int)threadIdx.x < C) {
+        const int u = threadIdx.x;
+        UnitVote v;
+        if (R <= 16) {
+            uint64_t e[16];
+#pragma unroll
+            for (int r = 0; r < 16; ++r) e[r] = r < R ? rec[r * C + u].sig : 0ull;
+            v = exact_vote_row<16>(e, R);
+        } else {
+            uint64_t e[C3_MAX_REPLICAS];
+            for (int r = 0; r < C3_MAX_REPLICAS; ++r) e[r] = r < R ? rec[r * C + u].sig : 0ull;
+            v = exact_vote_row<C3_MAX_REPLICAS>(e, R);
+        }
+        status[u] = v.status;
+        bitmap[u] = v.bitmap;
+        majority[u] = v.majority;
+        votes[u] = v;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int64_t no = 0, nu = 0, na = 0;
+        for (int u = 0; u < C; ++u) {
+            const UnitVote v = votes[u];
+            if (v.status == C3_INCONCLUSIVE) {
+                if (nu < und_cap) undecided[nu] = u;
+                ++nu;
+                continue;
+            }
+            if (v.bitmap == 0ull) continue;
+            ++na;
+            for (uint64_t b = v.bitmap; b != 0ull; b &= b - 1ull) {
+                const int r = __builtin_ctzll(b);
+                if (no < out_cap) {
+                    c3_outlier_t o;
+                    o.chunk = u;
+                    o.replica = r;
+                    o.majority_replica = v.majority;
+                    const c3_chunk_record_t* s2[2] = {&rec[r * C + u], &rec[v.majority * C + u]};
+                    for (int z = 0; z < 2; ++z) {
+                        o.nan_count[z] = s2[z]->nan_count;
+                        o.inf_count[z] = s2[z]->inf_count;
+                        o.absmax[z] = s2[z]->absmax;
+                        o.sum[z] = s2[z]->sum;
+                        o.sumsq[z] = s2[z]->sumsq;
+                    }
+                    outliers[no] = o;
+                }
+                ++no;
+            }
+        }
+        counts[0] = no;
+        counts[1] = nu;
+        counts[2] = na;
+    }
+}
+
+bool small_tail_fits(int R, int64_t C) { return C >= 1 && C <= kTailThreads && R * C <= kTailMaxRecords; }
+
+hipError_t launch_small_tail(const SigPlan* dplan, c3_chunk_record_t* records, uint8_t* status,
+                             uint64_t* bitmap, int32_t* majority, c3_outlier_t* outliers,
+                             int64_t out_cap, int64_t* undecided, int64_t und_cap, int64_t* counts,
+                             hipStream_t stream) {
+    hipLaunchKernelGGL(small_tail_kernel, dim3(1), dim3(kTailThreads), 0, stream, dplan, records,
+                       status, bitmap, majority, outliers, out_cap, undecided, und_cap, counts);
+    return hipGetLastError();
 }
 
 // Copies the staged plan from pinned host memory into the workspace on the
@@ -421,8 +527,8 @@ static hipError_t launch_group(const SigPlan* dplan, c3_chunk_record_t* records,
 }
 
 hipError_t launch_signature(const SigPlan* dplan, const SigPlan& hplan, const SigGroups& groups,
-                            c3_chunk_record_t* records, int grid_blocks, hipStream_t stream,
-                            hipEvent_t ev0, hipEvent_t ev1) {
+                            c3_chunk_record_t* records, int grid_blocks, bool finalize,
+                            hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1) {
     hipError_t e;
     if (ev0 && (e = hipEventRecord(ev0, stream)) != hipSuccess) return e;
     for (int d = 0; d < 4; ++d) {
@@ -438,7 +544,7 @@ hipError_t launch_signature(const SigPlan* dplan, const SigPlan& hplan, const Si
         if (e != hipSuccess) return e;
     }
     if (ev1 && (e = hipEventRecord(ev1, stream)) != hipSuccess) return e;
-    if (!hplan.direct) {
+    if (!hplan.direct && finalize) {
         const int64_t total = hplan.C * hplan.R;
         const int64_t blocks = (total + 255) / 256 < 65536 ? (total + 255) / 256 : 65536;
         hipLaunchKernelGGL(finalize_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, dplan,
