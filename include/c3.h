@@ -31,6 +31,13 @@
  *     run concurrently.
  *   - Outputs are deterministic: identical inputs give identical bits
  *     whatever the grid size.
+ *   - HIP graph capture: c3_consensus, c3_localize, c3_confirm,
+ *     c3_timing_consensus and c3_tensor_signature only launch kernels and
+ *     can be captured.  c3_signature stages its plan from host memory when
+ *     called; capture it with C3_OPT_PLAN_STAGED after an eager call with
+ *     the same arguments staged the plan into the workspace, and each
+ *     replay reads the tensors' current bytes.  c3_optimizer_check stages a
+ *     new plan per slice and is not meant for capture.
  */
 #ifndef C3_H_
 #define C3_H_
