@@ -208,8 +208,11 @@ size_t c3_signature_workspace_size_ex(const c3_tensor_meta_t *metas, int T, int 
  *               be 16-byte aligned (C3_E_ALIGN) and non-NULL unless the
  *               tensor is empty.
  *   metas       host array [T]; shared by all replicas.
- *   T, R        tensors per replica (>= 1) and replicas (2..64; R = 1 is a
- *               singleton group with nothing to compare, Sec. 4: C3_E_INVAL).
+ *   T, R        tensors per replica (>= 1) and replicas (1..64).  Records
+ *               are per replica and do not depend on R: with R = 1 a rank
+ *               signs its own replica, as each rank of a group spread over
+ *               GPUs would before the records are gathered (Algorithm 1's
+ *               AllGather); comparing is c3_consensus's job.
  *   chunk_bytes positive multiple of 1024.
  *   records     device [R][C] c3_chunk_record_t, 8-byte aligned; written.
  *   ws, ws_bytes  device workspace of at least

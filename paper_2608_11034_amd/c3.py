@@ -231,8 +231,8 @@ class SignaturePlan:
     """
 
     def __init__(self, replicas, chunk_bytes: int, tile_bytes: int = 0):
-        if len(replicas) < 2:
-            raise C3Error("need at least two replicas")
+        if len(replicas) < 1:
+            raise C3Error("need at least one replica")
         T = len(replicas[0])
         dev = replicas[0][0].device
         for r, rep in enumerate(replicas):

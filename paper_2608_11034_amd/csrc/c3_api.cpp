@@ -79,7 +79,7 @@ struct Plan {
 // Builds the plan; returns C3_OK or an error code.
 int make_plan(const c3_tensor_meta_t* metas, int T, int R, uint64_t chunk_bytes,
               uint64_t tile_bytes, Plan& p) {
-    if (metas == nullptr || T < 1 || R < 2 || R > C3_MAX_REPLICAS) return C3_E_INVAL;
+    if (metas == nullptr || T < 1 || R < 1 || R > C3_MAX_REPLICAS) return C3_E_INVAL;
     if (chunk_bytes == 0 || chunk_bytes % 1024 != 0 || chunk_bytes > (1ull << 40)) return C3_E_INVAL;
     if (tile_bytes == 0) tile_bytes = default_tile(chunk_bytes);
     if (tile_bytes < 1024 || (tile_bytes & (tile_bytes - 1)) != 0 || chunk_bytes % tile_bytes != 0 ||

@@ -145,7 +145,7 @@ int main(void) {
         const void *ptrs[R] = {dev[0], dev[1], (const char *)dev[2] + 4};
         CHECK(c3_signature(ptrs, &meta, 1, R, CHUNK, rec, ws, ws_bytes, (c3_stream_t)s) ==
               C3_E_ALIGN);
-        CHECK(c3_signature(ptrs, &meta, 1, 1, CHUNK, rec, ws, ws_bytes, (c3_stream_t)s) ==
+        CHECK(c3_signature(ptrs, &meta, 1, 0, CHUNK, rec, ws, ws_bytes, (c3_stream_t)s) ==
               C3_E_INVAL);
         CHECK(c3_signature(ptrs, &meta, 1, R, 1000, rec, ws, ws_bytes, (c3_stream_t)s) ==
               C3_E_INVAL);

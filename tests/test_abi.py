@@ -79,7 +79,8 @@ def test_plan_rejects_bad_arguments():
     assert L.c3_num_chunks(md, 0, 1024) == -1           # no tensors
     assert L.c3_num_chunks(_metas([(7, (10,))]), 1, 1024) == -1     # unknown dtype
     assert L.c3_num_chunks(_metas([(c3.F32, (-1,))]), 1, 1024) == -1
-    assert L.c3_signature_workspace_size(md, 1, 1, 1024) == 0        # R = 1
+    assert L.c3_signature_workspace_size(md, 1, 0, 1024) == 0        # R = 0
+    assert L.c3_signature_workspace_size(md, 1, 1, 1024) > 0         # one replica
     assert L.c3_signature_workspace_size(md, 1, 65, 1024) == 0       # R > 64
     assert L.c3_signature_workspace_size(md, 1, 8, 1024) > 0
     assert L.c3_signature_workspace_size_ex(md, 1, 8, 4096, 3072) == 0   # tile not a power of 2
@@ -93,7 +94,8 @@ def test_argument_errors_return_before_gpu_work():
     null = ctypes.c_void_p(0)
     rec = ctypes.c_void_p(64)
     ws = ctypes.c_void_p(256)
-    assert L.c3_signature(ptrs, md, 1, 1, 1024, rec, ws, 1 << 20, null) == -1     # R = 1
+    assert L.c3_signature(ptrs, md, 1, 0, 1024, rec, ws, 1 << 20, null) == -1     # R = 0
+    assert L.c3_signature(ptrs, md, 1, 65, 1024, rec, ws, 1 << 20, null) == -1    # R > 64
     assert L.c3_signature(ptrs, md, 1, 2, 1000, rec, ws, 1 << 20, null) == -1     # chunk
     assert L.c3_signature(ptrs, md, 1, 2, 1024, rec, null, 1 << 20, null) == -4   # workspace
     assert L.c3_signature(ptrs, md, 1, 2, 1024, rec, ws, 8, null) == -4           # too small

@@ -177,6 +177,30 @@ def test_edge_shapes_every_record(dtype, chunk_bytes):
     compare_all_records(c3.records_numpy(rec), ref)
 
 
+@pytest.mark.parametrize("k", [2, 3, 4])
+def test_sharded_protocol_emulated(k):
+    """The protocol with one replica per GPU, on one GPU: every replica is
+    signed on its own (R = 1, what each rank does), the record tables are
+    stacked (what the AllGather of Algorithm 1 delivers), and consensus and
+    localize on the stacked table give exactly the joint call's bits."""
+    _print_case("sharded protocol", k)
+    w = workloads.make(k, device=DEV, scale="small")
+    joint = _gpu_pipeline(w)
+    parts = [c3.signature([rep], w.chunk_bytes) for rep in w.replicas]
+    stacked = torch.cat(parts, dim=0)
+    assert stacked.shape == joint["rec"].shape
+    st, bm, mj = c3.consensus(stacked, c3.EXACT)
+    outl, und, cnt = c3.localize(st, bm, mj, stacked)
+    torch.cuda.synchronize()
+    assert stacked.cpu().numpy().tobytes() == joint["rec"].cpu().numpy().tobytes()
+    assert np.array_equal(st.cpu().numpy(), joint["status"])
+    assert np.array_equal(bm.cpu().numpy().view(np.uint64), joint["bitmap"])
+    assert np.array_equal(mj.cpu().numpy(), joint["maj"])
+    assert cnt.cpu().numpy().tolist() == joint["counts"].tolist()
+    o = c3.outliers_numpy(outl, cnt)
+    assert o.tobytes() == joint["outliers"].tobytes()
+
+
 @pytest.mark.parametrize("R", [2, 5, 64])
 def test_replica_count_bounds(R):
     _print_case("replica count", R)
@@ -200,16 +224,16 @@ def test_replica_count_bounds(R):
 def test_argument_errors():
     _print_case("argument errors")
     x = torch.randn(4096, device=DEV)
-    with pytest.raises(c3.C3Error, match="two replicas"):
-        c3.signature([[x]], 1024)                                 # handled in Python
+    with pytest.raises(c3.C3Error, match="at least one replica"):
+        c3.signature([], 1024)                                    # handled in Python
     L = c3.lib()
     metas = c3.make_metas([x])
     rec = torch.empty(16 * 64, dtype=torch.uint8, device=DEV)
     ws = torch.empty(1 << 20, dtype=torch.uint8, device=DEV)
     p1 = (ctypes.c_void_p * 1)(x.data_ptr())
     s = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
-    assert L.c3_signature(p1, metas, 1, 1, 1024, ctypes.c_void_p(rec.data_ptr()),
-                          ctypes.c_void_p(ws.data_ptr()), ws.numel(), s) == -1    # R = 1
+    assert L.c3_signature(p1, metas, 1, 0, 1024, ctypes.c_void_p(rec.data_ptr()),
+                          ctypes.c_void_p(ws.data_ptr()), ws.numel(), s) == -1    # R = 0
     p2 = (ctypes.c_void_p * 2)(x.data_ptr(), x.data_ptr())
     assert L.c3_signature(p2, metas, 1, 2, 1000, ctypes.c_void_p(rec.data_ptr()),
                           ctypes.c_void_p(ws.data_ptr()), ws.numel(), s) == -1    # chunk
