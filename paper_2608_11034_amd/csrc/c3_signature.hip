@@ -41,7 +41,6 @@
 namespace c3 {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef uint16_t u16x2 __attribute__((ext_vector_type(2)));
 typedef const __attribute__((address_space(1))) u32x4 gu32x4;
 
 struct LaneKeys {
@@ -53,13 +52,48 @@ __device__ inline u32x4 load16(const u32x4* p) {
     return __builtin_nontemporal_load((gu32x4*)p);
 }
 
+// Raw buffer resource over the `len` bytes at `base` (stride 0, untyped
+// 32-bit data format in the descriptor's last word, as gfx9 buffer loads
+// require); loads past `len` return zero.  Tiles are at most 16 MiB, so `len`
+// fits the 32-bit record count.  The plan is read with vector loads (the
+// kernel also writes through it), so base and length are taken from the first
+// lane: the resource must sit in scalar registers.
+constexpr int kRawBufferWord3 = 0x00020000;
+
+__device__ inline __amdgpu_buffer_rsrc_t tile_resource(const uint8_t* base, uint32_t len) {
+    const uint64_t a = reinterpret_cast<uint64_t>(base);
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)a);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(a >> 32));
+    const int n = __builtin_amdgcn_readfirstlane((int)len);
+    void* b = reinterpret_cast<void*>(((uint64_t)hi << 32) | lo);
+    return __builtin_amdgcn_make_buffer_rsrc(b, (short)0, n, kRawBufferWord3);
+}
+
+// 128-bit non-temporal buffer load at voffset + soffset bytes.
+__device__ inline u32x4 load16_buf(__amdgpu_buffer_rsrc_t rs, uint32_t voff, uint32_t soff) {
+    constexpr int kNonTemporal = 2;
+    return __builtin_amdgcn_raw_buffer_load_b128(rs, (int)voff, (int)soff, kNonTemporal);
+}
+
+// beta of block b (wave-uniform, so it stays in a scalar register)
+__device__ inline uint32_t block_beta(uint32_t b) { return b * kBlockMul; }
+
+// m + k + beta as one three-input add with beta as the scalar operand.  The
+// compiler would otherwise re-associate to m + (k + beta) and spend a
+// separate add on each of the six key sums per block.
+__device__ inline uint32_t add3(uint32_t m, uint32_t k, uint32_t beta) {
+    uint32_t r;
+    asm("v_add3_u32 %0, %1, %2, %3" : "=v"(r) : "v"(m), "v"(k), "s"(beta));
+    return r;
+}
+
 // NH over one 16-byte segment (two word pairs) at key offset 4 * lane.
 __device__ inline void nh16(const u32x4 v, const LaneKeys& K, uint32_t beta, uint64_t& A,
                             uint64_t& B) {
-    A += (uint64_t)(v.x + K.k0 + beta) * (uint64_t)(v.y + K.k1 + beta);
-    B += (uint64_t)(v.x + K.k2 + beta) * (uint64_t)(v.y + K.k3 + beta);
-    A += (uint64_t)(v.z + K.k2 + beta) * (uint64_t)(v.w + K.k3 + beta);
-    B += (uint64_t)(v.z + K.k4 + beta) * (uint64_t)(v.w + K.k5 + beta);
+    A += (uint64_t)add3(v.x, K.k0, beta) * (uint64_t)add3(v.y, K.k1, beta);
+    B += (uint64_t)add3(v.x, K.k2, beta) * (uint64_t)add3(v.y, K.k3, beta);
+    A += (uint64_t)add3(v.z, K.k2, beta) * (uint64_t)add3(v.w, K.k3, beta);
+    B += (uint64_t)add3(v.z, K.k4, beta) * (uint64_t)add3(v.w, K.k5, beta);
 }
 
 __device__ inline double f16_to_f64(uint32_t h) {
@@ -68,41 +102,59 @@ __device__ inline double f16_to_f64(uint32_t h) {
 }
 
 // ---------------------------------------------------------------------------
-// fast statistics: no classification; `mx` collects magnitude bits (two
-// packed u16 lanes for the 16-bit types)
+// fast statistics: no classification.  `mf` collects the largest magnitude as
+// an fp32 value (every fp32, bf16 and fp16 value is one exactly); a NaN or
+// Inf may poison it, but such a lane takes the classifying path below, which
+// starts over.
 // ---------------------------------------------------------------------------
+// max(|a|, |b|, |c|) in one instruction (abs source modifiers); NaN
+// propagates, which only matters on lanes the classifying path redoes.
+__device__ inline float absmax3(float a, float b, float c) {
+    float r;
+    asm("v_maximum3_f32 %0, |%1|, |%2|, |%3|" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+    return r;
+}
+
 template <int DT>
-__device__ inline void stats_fast(const u32x4 v, double& s, double& q, uint32_t& mx) {
+__device__ inline void stats_fast(const u32x4 v, double& s, double& q, float& mf) {
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
     if constexpr (DT == C3_F32) {
-        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             double d = (double)__uint_as_float(w[i]);
             s += d;
             q = __fma_rn(d, d, q);
-            mx = max(mx, w[i] & 0x7FFFFFFFu);
         }
+        mf = absmax3(mf, absmax3(__uint_as_float(w[0]), __uint_as_float(w[1]), __uint_as_float(w[2])),
+                     __uint_as_float(w[3]));
     } else if constexpr (DT == C3_BF16 || DT == C3_F16) {
-        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-        u16x2 m2 = __builtin_bit_cast(u16x2, mx);
+        float x[8];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            double lo, hi;
             if constexpr (DT == C3_BF16) {
-                lo = (double)__uint_as_float(w[i] << 16);
-                hi = (double)__uint_as_float(w[i] & 0xFFFF0000u);
+                x[2 * i] = __uint_as_float(w[i] << 16);
+                x[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
             } else {
-                lo = f16_to_f64(w[i] & 0xFFFFu);
-                hi = f16_to_f64(w[i] >> 16);
+                x[2 * i] = (float)__builtin_bit_cast(_Float16, (uint16_t)(w[i] & 0xFFFFu));
+                x[2 * i + 1] = (float)__builtin_bit_cast(_Float16, (uint16_t)(w[i] >> 16));
             }
-            s += lo;
-            q = __fma_rn(lo, lo, q);
-            s += hi;
-            q = __fma_rn(hi, hi, q);
-            m2 = __builtin_elementwise_max(m2, __builtin_bit_cast(u16x2, w[i] & 0x7FFF7FFFu));
         }
-        mx = __builtin_bit_cast(uint32_t, m2);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const double d = (double)x[i];
+            s += d;
+            q = __fma_rn(d, d, q);
+        }
+        mf = absmax3(absmax3(x[0], x[1], x[2]), absmax3(x[3], x[4], x[5]), absmax3(x[6], x[7], mf));
     }
+}
+
+// magnitude bits of the type from the fp32 value of a finite magnitude
+template <int DT>
+__device__ inline uint32_t magnitude_bits(float mf) {
+    if constexpr (DT == C3_BF16) return __float_as_uint(mf) >> 16;  // exact: a bf16 value
+    if constexpr (DT == C3_F16) return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)mf);
+    return __float_as_uint(mf);
 }
 
 // slow statistics: classify each element; `mx` is a plain magnitude
@@ -160,42 +212,47 @@ struct LaneFold {
 };
 
 // One wave's share of a tile: blocks wave, wave + 4, ... of `len` bytes.
+// Full blocks are read with raw buffer loads: the resource is the tile (a
+// wave-uniform base, `len` bytes), the scalar offset the block, the vector
+// offset the lane's 16 bytes, so no load spends vector instructions on its
+// address.  Each block's beta is pinned in a scalar register, so every key
+// sum is one three-input add.
 template <int DT, int U>
 __device__ inline LaneFold fold_lane(const uint8_t* tile, uint32_t len, uint32_t blk0,
                                      const LaneKeys& K, int wave, int lane) {
     LaneFold f{0, 0, 0.0, 0.0, 0u, 0u, 0u};
-    const u32x4* p = reinterpret_cast<const u32x4*>(tile) + lane;
+    float mf = 0.0f;
+    const uint32_t off = (uint32_t)lane * 16u;
     const int nfull = (int)(len >> 10);
     const uint32_t tail = len & 1023u;
+    const __amdgpu_buffer_rsrc_t rs = tile_resource(tile, len);
     int k = wave;
     for (; k + 4 * (U - 1) < nfull; k += 4 * U) {
         u32x4 v[U];
 #pragma unroll
-        for (int u = 0; u < U; ++u) v[u] = load16(p + (size_t)(k + 4 * u) * 64);
+        for (int u = 0; u < U; ++u) v[u] = load16_buf(rs, off, (uint32_t)(k + 4 * u) << 10);
         // keep all U loads in flight before the first use
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const uint32_t beta = (blk0 + (uint32_t)(k + 4 * u)) * kBlockMul;
+            const uint32_t beta = block_beta(blk0 + (uint32_t)(k + 4 * u));
             nh16(v[u], K, beta, f.A, f.B);
-            stats_fast<DT>(v[u], f.s, f.q, f.mx);
+            stats_fast<DT>(v[u], f.s, f.q, mf);
         }
     }
     for (; k < nfull; k += 4) {
-        u32x4 v = load16(p + (size_t)k * 64);
-        nh16(v, K, (blk0 + (uint32_t)k) * kBlockMul, f.A, f.B);
-        stats_fast<DT>(v, f.s, f.q, f.mx);
+        u32x4 v = load16_buf(rs, off, (uint32_t)k << 10);
+        nh16(v, K, block_beta(blk0 + (uint32_t)k), f.A, f.B);
+        stats_fast<DT>(v, f.s, f.q, mf);
     }
-    const uint32_t off = (uint32_t)lane * 16u;
     const bool has_tail = tail != 0u && (nfull & 3) == wave && off < tail;
     if (has_tail) {
         const uint8_t* seg = tile + ((size_t)nfull << 10) + off;
         u32x4 v = (off + 16u <= tail) ? load16(reinterpret_cast<const u32x4*>(seg))
                                       : load_partial(seg, tail - off);
         nh16(v, K, (blk0 + (uint32_t)nfull) * kBlockMul, f.A, f.B);
-        stats_fast<DT>(v, f.s, f.q, f.mx);
+        stats_fast<DT>(v, f.s, f.q, mf);
     }
-    if constexpr (DT == C3_BF16 || DT == C3_F16) f.mx = max(f.mx & 0xFFFFu, f.mx >> 16);
     if constexpr (DT != C3_RAW) {
         if (!__builtin_isfinite(f.s) || !__builtin_isfinite(f.q)) {
             // rare: this lane saw a NaN or Inf; redo its statistics classifying
@@ -203,13 +260,16 @@ __device__ inline LaneFold fold_lane(const uint8_t* tile, uint32_t len, uint32_t
             f.q = 0.0;
             f.mx = 0u;
             for (int kk = wave; kk < nfull; kk += 4)
-                stats_slow<DT>(load16(p + (size_t)kk * 64), f.s, f.q, f.mx, f.nan_c, f.inf_c);
+                stats_slow<DT>(load16(reinterpret_cast<const u32x4*>(tile + ((size_t)kk << 10) + off)),
+                               f.s, f.q, f.mx, f.nan_c, f.inf_c);
             if (has_tail) {
                 const uint8_t* seg = tile + ((size_t)nfull << 10) + off;
                 u32x4 v = (off + 16u <= tail) ? load16(reinterpret_cast<const u32x4*>(seg))
                                               : load_partial(seg, tail - off);
                 stats_slow<DT>(v, f.s, f.q, f.mx, f.nan_c, f.inf_c);
             }
+        } else {
+            f.mx = magnitude_bits<DT>(mf);
         }
     }
     return f;
@@ -307,7 +367,8 @@ __global__ void __launch_bounds__(kSigThreads, C3_SIG_WAVES_PER_EU)
                      int gk0, int gk1, int64_t gtiles) {
     __shared__ TilePartial lds[kSigThreads / 64];
     const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
+    // the wave index, uniform across the wave (keeps beta and addresses scalar)
+    const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
     const char* pb = reinterpret_cast<const char*>(plan);
     const uint64_t* ptrs = reinterpret_cast<const uint64_t*>(pb + plan->off_ptrs);
     const int64_t* tile_base = reinterpret_cast<const int64_t*>(pb + plan->off_tile_base);

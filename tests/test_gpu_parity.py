@@ -177,6 +177,56 @@ def test_edge_shapes_every_record(dtype, chunk_bytes):
     compare_all_records(c3.records_numpy(rec), ref)
 
 
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16, torch.float16])
+def test_absmax_finite_extremes_every_record(dtype):
+    """Chunks without NaN or Inf (the kernel's unclassified path) whose largest
+    magnitude is a signed zero, a subnormal, the largest finite value or a
+    negative number, at random positions: absmax must be the exact magnitude."""
+    _print_case("absmax finite extremes", dtype)
+    iv, pos_max, sub_max = {torch.float32: (torch.int32, 0x7F7FFFFF, 0x007FFFFF),
+                            torch.bfloat16: (torch.int16, 0x7F7F, 0x007F),
+                            torch.float16: (torch.int16, 0x7BFF, 0x03FF)}[dtype]
+    sign = -(2 ** 31) if dtype == torch.float32 else -(2 ** 15)
+    chunk = 4096
+    per = chunk // (4 if dtype == torch.float32 else 2)
+    gen = torch.Generator(device="cpu")
+    gen.manual_seed(17)
+    pieces = []
+    for kind in range(6):
+        if kind == 0:    # zeros, some negative
+            bits = torch.where(torch.rand(per, generator=gen) < 0.5, 0, sign)
+        elif kind == 1:  # subnormals only, mixed signs
+            bits = torch.randint(1, sub_max + 1, (per,), generator=gen)
+            bits = torch.where(torch.rand(per, generator=gen) < 0.5, bits, bits + sign)
+        elif kind == 2:  # subnormals and zeros, the largest one negative
+            bits = torch.randint(0, sub_max // 2, (per,), generator=gen)
+            bits[int(torch.randint(0, per, (1,), generator=gen))] = sub_max + sign
+        elif kind == 3:  # the largest finite value, positive, once
+            bits = torch.randint(0, pos_max // 2, (per,), generator=gen)
+            bits[int(torch.randint(0, per, (1,), generator=gen))] = pos_max
+        elif kind == 4:  # the largest finite value, negative, several times
+            bits = torch.randint(0, pos_max, (per,), generator=gen)
+            bits[torch.randint(0, per, (5,), generator=gen)] = pos_max + sign
+        else:            # all values negative normals
+            bits = torch.randint(0x00800000 if dtype == torch.float32 else 0x0080 if dtype ==
+                                 torch.bfloat16 else 0x0400, pos_max, (per,), generator=gen) + sign
+        pieces.append(bits)
+    host = torch.cat(pieces).to(iv).view(dtype)
+    t = host.to(DEV)
+    assert not torch.isnan(host.float()).any() and not torch.isinf(host.float()).any()
+    reps = [[t.clone()] for _ in range(3)]
+    reps[2][0].view(torch.uint8)[3 * chunk + 1] ^= 0x01   # one differing chunk
+    plan = c3.SignaturePlan(reps, chunk)
+    rec = plan.new_records()
+    plan.run(rec, plan.new_workspace())
+    torch.cuda.synchronize()
+    meta = workloads.F32 if dtype == torch.float32 else workloads.BF16 if dtype == torch.bfloat16 \
+        else workloads.F16
+    ref = oracle.signature([[workloads.host_bytes(r[0])] for r in reps], [(meta, tuple(t.shape))], chunk)
+    compare_all_records(c3.records_numpy(rec), ref)
+    assert (ref["absmax"][0] > 0).sum() == 5        # the zero chunk's absmax is +0
+
+
 @pytest.mark.parametrize("k", [2, 3, 4])
 def test_sharded_protocol_emulated(k):
     """The protocol with one replica per GPU, on one GPU: every replica is
