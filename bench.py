@@ -67,6 +67,19 @@ def measured_traffic(workload: str):
     return t.get("hbm_bytes_per_launch")
 
 
+def host_cpu():
+    """Host CPU model and the number of cores this process may run on."""
+    model = "unknown"
+    try:
+        for ln in open("/proc/cpuinfo"):
+            if ln.startswith("model name"):
+                model = ln.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"model": model, "cores_available": len(os.sched_getaffinity(0))}
+
+
 def cpu_baseline(w, budget_s: float):
     """Oracle over the first chunks of every replica: bounded sample, one thread."""
     import numpy as np
@@ -94,7 +107,7 @@ def cpu_baseline(w, budget_s: float):
     return {"value": sample_bytes / dt / 1e9, "unit": "GB/s", "cores": 1, "kind": "oracle",
             "sample": f"first {T} tensors of all {w.R} replicas ({sample_bytes} bytes, "
                       f"{rec['sig'].shape[1]} chunks), signature+vote+localize, {dt:.1f} s",
-            "seconds": dt}
+            "seconds": dt, "host": host_cpu()}
 
 
 def main():
@@ -454,7 +467,8 @@ def bench_optimizer(args, torch, workloads, c3, dev):
         dt = time.perf_counter() - t1
         cpu = {"value": round(done / dt, 3), "unit": "checks/s", "cores": 1, "kind": "oracle",
                "sample": f"{done} checks over {n_host} resident 64K-element slices of all {R} "
-                         f"replicas (AdamW replay, 56 slice signatures, vote, localize), {dt:.1f} s"}
+                         f"replicas (AdamW replay, 56 slice signatures, vote, localize), {dt:.1f} s",
+               "host": host_cpu()}
     res = {
         "metric": "optimizer-boundary checks/s (64K-element AdamW slice, 8 replicas)",
         "value": round(1e3 / ms, 1),
