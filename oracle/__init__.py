@@ -20,6 +20,11 @@ function cites the paper passage it follows:
 * ``vote_statistical`` Sec. 5.4, Algorithm 1 Statistical branch.
 * ``localize``         Sec. 5.1: bitmap bit i names peer i; the result keeps
                        which peers disagree.
+
+Peer groups hold up to ``MAX_PEERS`` replicas (the paper's Table 2 lists
+data-parallel peer degrees up to 192).  A unit's outlier bitmap is then
+ceil(R / 64) 64-bit words, bit b of word w naming replica 64 w + b: the vote
+functions return bitmaps of shape [U] for R <= 64 and [U, ceil(R / 64)] above.
 * ``confirm``          Sec. 10 protocol: stragglers are confirmed across
                        repeated timing rounds.
 * ``adamw``            Sec. 9 optimizer boundary: the replayed AdamW step on a
@@ -41,6 +46,7 @@ F32, BF16, F16, RAW = 0, 1, 2, 3
 AGREE, ATTRIBUTED, INCONCLUSIVE = 0, 1, 2
 EV_U64, EV_U32, EV_F32, EV_F64 = 0, 1, 2, 3
 KAPPA_DEFAULT = 3.5 / 0.6745          # Iglewicz-Hoaglin modified z > 3.5
+MAX_PEERS = 256
 ELEM_SIZE = {F32: 4, BF16: 2, F16: 2, RAW: 1}
 
 _lib = None
@@ -216,6 +222,22 @@ def tensor_signature(rec: dict, T: int) -> np.ndarray:
 # --------------------------------------------------------------------------
 # votes
 # --------------------------------------------------------------------------
+def bitmap_words(R: int) -> int:
+    """64-bit words of one unit's outlier bitmap."""
+    return (R + 63) // 64
+
+
+def _new_bitmap(U: int, R: int) -> np.ndarray:
+    if not 1 <= R <= MAX_PEERS:
+        raise ValueError(f"R = {R} outside 1..{MAX_PEERS}")
+    return np.zeros(U, np.uint64) if R <= 64 else np.zeros((U, bitmap_words(R)), np.uint64)
+
+
+def bitmap_bits(bitmap: np.ndarray, R: int) -> np.ndarray:
+    """[U, R] bool array: replica r is flagged at unit u."""
+    b = np.ascontiguousarray(bitmap, np.uint64).reshape(-1, bitmap_words(R))
+    r = np.arange(R)
+    return ((b[:, r // 64] >> (r % 64).astype(np.uint64)) & np.uint64(1)).astype(bool)
 def _ev_kind(ev: np.ndarray) -> int:
     return {np.dtype(np.uint64): EV_U64, np.dtype(np.int64): EV_U64, np.dtype(np.uint32): EV_U32,
             np.dtype(np.int32): EV_U32, np.dtype(np.float32): EV_F32,
@@ -232,7 +254,7 @@ def vote_exact(ev: np.ndarray, replica_axis: int = 0):
         U, R = ev.shape
         us, rs = ev.strides
     st = np.zeros(U, np.uint8)
-    bm = np.zeros(U, np.uint64)
+    bm = _new_bitmap(U, R)
     mj = np.zeros(U, np.int32)
     _load().c3o_vote_exact(_p(ev), _ev_kind(ev), rs, us, R, U, _p(st), _p(bm), _p(mj))
     return st, bm, mj
@@ -245,7 +267,7 @@ def vote_bytes(chunks):
     ptrs = (ctypes.c_void_p * (R * U))(*[c.ctypes.data if c.size else 0 for c in keep])
     lens = np.array([c.size for c in chunks[0]], np.uint64)
     st = np.zeros(U, np.uint8)
-    bm = np.zeros(U, np.uint64)
+    bm = _new_bitmap(U, R)
     mj = np.zeros(U, np.int32)
     _load().c3o_vote_bytes(ptrs, _p(lens), R, U, _p(st), _p(bm), _p(mj))
     return st, bm, mj
@@ -261,7 +283,7 @@ def vote_statistical(ev: np.ndarray, kappa: float = KAPPA_DEFAULT, replica_axis:
         U, R = ev.shape
         us, rs = ev.strides
     st = np.zeros(U, np.uint8)
-    bm = np.zeros(U, np.uint64)
+    bm = _new_bitmap(U, R)
     mj = np.zeros(U, np.int32)
     _load().c3o_vote_statistical(_p(ev), _ev_kind(ev), rs, us, R, U, ctypes.c_double(kappa),
                                  _p(st), _p(bm), _p(mj))
@@ -269,11 +291,14 @@ def vote_statistical(ev: np.ndarray, kappa: float = KAPPA_DEFAULT, replica_axis:
 
 
 def localize(status, bitmap, majority_idx, R: int, out_cap=None, und_cap=None):
-    """Outlier (unit, replica, majority replica) list and undecided units."""
+    """Outlier (unit, replica, majority replica) list and undecided units.
+    bitmap: [U] (R <= 64) or [U, ceil(R / 64)] uint64."""
+    if not 1 <= R <= MAX_PEERS:
+        raise ValueError(f"R = {R} outside 1..{MAX_PEERS}")
     status = np.ascontiguousarray(status, np.uint8)
-    bitmap = np.ascontiguousarray(bitmap, np.uint64)
-    majority_idx = np.ascontiguousarray(majority_idx, np.int32)
     U = status.size
+    bitmap = np.ascontiguousarray(bitmap, np.uint64).reshape(U * bitmap_words(R))
+    majority_idx = np.ascontiguousarray(majority_idx, np.int32)
     if out_cap is None:
         out_cap = int(sum(bin(int(b)).count("1") for b in bitmap)) if U < 100000 else U * R
     if und_cap is None:

@@ -43,10 +43,13 @@
  *   c3o_tensor_signature    pinned indirectly: its vote equals the byte-equality
  *                           vote over whole tensors
  *   c3o_vote_exact          pinned (brute force over all label vectors, paper
- *                           cases, Boyer-Moore MJRTY)
+ *                           cases, Boyer-Moore MJRTY; groups of 65-256 by
+ *                           rows whose vote is fixed by construction)
  *   c3o_vote_bytes          the definition itself (byte equality)
- *   c3o_vote_statistical    pinned (numpy median / percentile, closed forms)
- *   c3o_localize            pinned (brute-force enumeration of set bits)
+ *   c3o_vote_statistical    pinned (numpy median / percentile, closed forms,
+ *                           up to 256 replicas)
+ *   c3o_localize            pinned (brute-force enumeration of set bits over
+ *                           every bitmap word)
  *   c3o_confirm             pinned (brute-force window enumeration)
  *
  * Build: gcc -O2 -ffp-contract=off -fno-fast-math -shared -fPIC (no FMA
@@ -64,6 +67,43 @@
 enum { O_F32 = 0, O_BF16 = 1, O_F16 = 2, O_RAW = 3 };
 enum { O_AGREE = 0, O_ATTRIBUTED = 1, O_INCONCLUSIVE = 2 };
 enum { O_EV_U64 = 0, O_EV_U32 = 1, O_EV_F32 = 2, O_EV_F64 = 3 };
+
+/* ------------------------------------------------------------------ */
+/* Peer groups of up to O_MAX_R replicas (the data-parallel peer        */
+/* degrees the paper tabulates reach 192, Table 2).  The outlier bitmap */
+/* B of a unit is N bits (Sec. 5.1): ceil(R / 64) 64-bit words, bit b   */
+/* of word w naming replica 64 w + b.  For R <= 64 that is one word.    */
+/* ------------------------------------------------------------------ */
+enum { O_MAX_R = 256 };
+
+static int bm_words(int R)
+{
+    return (R + 63) / 64;
+}
+
+static void bm_clear(uint64_t *B, int R)
+{
+    int w;
+    for (w = 0; w < bm_words(R); w++) B[w] = 0;
+}
+
+static void bm_set(uint64_t *B, int r)
+{
+    B[r / 64] |= 1ULL << (r % 64);
+}
+
+static int bm_test(const uint64_t *B, int r)
+{
+    return (int)((B[r / 64] >> (r % 64)) & 1ULL);
+}
+
+static int bm_any(const uint64_t *B, int R)
+{
+    int w;
+    for (w = 0; w < bm_words(R); w++)
+        if (B[w]) return 1;
+    return 0;
+}
 
 /* ------------------------------------------------------------------ */
 /* SplitMix64 (Steele, Lea, Flood 2014): state advances by the golden   */
@@ -380,12 +420,16 @@ static uint64_t ev_bits(const uint8_t *base, int kind, int64_t off)
 
 int c3o_vote_exact(const uint8_t *evidence, int kind, int64_t replica_stride,
                    int64_t unit_stride, int R, int64_t n_units,
-                   uint8_t *status, uint64_t *bitmap, int32_t *majority_idx)
+                   uint8_t *status, uint64_t *bitmap /* [n_units][ceil(R/64)] */,
+                   int32_t *majority_idx)
 {
     int64_t u;
+    const int W = bm_words(R);
+    if (R < 1 || R > O_MAX_R) return -1;
     for (u = 0; u < n_units; u++) {
-        uint64_t e[64];
-        int cnt[64], r, j, best = 0, arg = -1;
+        uint64_t e[O_MAX_R];
+        uint64_t *B = bitmap + u * W;
+        int cnt[O_MAX_R], r, j, best = 0, arg = -1;
         for (r = 0; r < R; r++)
             e[r] = ev_bits(evidence, kind, u * unit_stride + (int64_t)r * replica_stride);
         /* most frequent value and its count (lowest replica on ties) */
@@ -394,20 +438,16 @@ int c3o_vote_exact(const uint8_t *evidence, int kind, int64_t replica_stride,
             for (j = 0; j < R; j++) cnt[r] += (e[j] == e[r]);
             if (cnt[r] > best) { best = cnt[r]; arg = r; }
         }
+        bm_clear(B, R);
         if (2 * best <= R) {          /* c* <= N/2: no strict majority */
             status[u] = O_INCONCLUSIVE;
-            bitmap[u] = 0;
             majority_idx[u] = -1;
             continue;
         }
-        {
-            uint64_t B = 0;
-            for (r = 0; r < R; r++)
-                if (e[r] != e[arg]) B |= 1ULL << r;
-            bitmap[u] = B;
-            status[u] = B ? O_ATTRIBUTED : O_AGREE;
-            majority_idx[u] = arg;
-        }
+        for (r = 0; r < R; r++)
+            if (e[r] != e[arg]) bm_set(B, r);
+        status[u] = bm_any(B, R) ? O_ATTRIBUTED : O_AGREE;
+        majority_idx[u] = arg;
     }
     return 0;
 }
@@ -420,11 +460,15 @@ int c3o_vote_exact(const uint8_t *evidence, int kind, int64_t replica_stride,
  */
 int c3o_vote_bytes(const uint8_t *const *chunk_ptrs, const uint64_t *chunk_len,
                    int R, int64_t n_units,
-                   uint8_t *status, uint64_t *bitmap, int32_t *majority_idx)
+                   uint8_t *status, uint64_t *bitmap /* [n_units][ceil(R/64)] */,
+                   int32_t *majority_idx)
 {
     int64_t u;
+    const int W = bm_words(R);
+    if (R < 1 || R > O_MAX_R) return -1;
     for (u = 0; u < n_units; u++) {
-        int cnt[64], r, j, best = 0, arg = -1;
+        uint64_t *B = bitmap + u * W;
+        int cnt[O_MAX_R], r, j, best = 0, arg = -1;
         uint64_t len = chunk_len[u];
         for (r = 0; r < R; r++) {
             const uint8_t *pr = chunk_ptrs[(int64_t)r * n_units + u];
@@ -435,23 +479,21 @@ int c3o_vote_bytes(const uint8_t *const *chunk_ptrs, const uint64_t *chunk_len,
             }
             if (cnt[r] > best) { best = cnt[r]; arg = r; }
         }
+        bm_clear(B, R);
         if (2 * best <= R) {
             status[u] = O_INCONCLUSIVE;
-            bitmap[u] = 0;
             majority_idx[u] = -1;
             continue;
         }
         {
-            uint64_t B = 0;
             const uint8_t *pa = chunk_ptrs[(int64_t)arg * n_units + u];
             for (r = 0; r < R; r++) {
                 const uint8_t *pr = chunk_ptrs[(int64_t)r * n_units + u];
-                if (len != 0 && memcmp(pr, pa, len) != 0) B |= 1ULL << r;
+                if (len != 0 && memcmp(pr, pa, len) != 0) bm_set(B, r);
             }
-            bitmap[u] = B;
-            status[u] = B ? O_ATTRIBUTED : O_AGREE;
-            majority_idx[u] = arg;
         }
+        status[u] = bm_any(B, R) ? O_ATTRIBUTED : O_AGREE;
+        majority_idx[u] = arg;
     }
     return 0;
 }
@@ -488,13 +530,17 @@ static double quantile7(const double *s, int n, double p)
 
 int c3o_vote_statistical(const uint8_t *evidence, int kind, int64_t replica_stride,
                          int64_t unit_stride, int R, int64_t n_units, double kappa,
-                         uint8_t *status, uint64_t *bitmap, int32_t *majority_idx)
+                         uint8_t *status, uint64_t *bitmap /* [n_units][ceil(R/64)] */,
+                         int32_t *majority_idx)
 {
     int64_t u;
+    const int W = bm_words(R);
+    if (R < 1 || R > O_MAX_R) return -1;
     for (u = 0; u < n_units; u++) {
-        double tau[64], s[64], dev[64], devs[64], m, d, thr;
-        int fin[64], r, nf = 0, k, lowmed;
-        uint64_t B = 0;
+        double tau[O_MAX_R], s[O_MAX_R], dev[O_MAX_R], devs[O_MAX_R], m, d, thr;
+        int fin[O_MAX_R], r, nf = 0, k, lowmed;
+        uint64_t *B = bitmap + u * W;
+        bm_clear(B, R);
         for (r = 0; r < R; r++) {
             int64_t off = u * unit_stride + (int64_t)r * replica_stride;
             if (kind == O_EV_F32) {
@@ -506,11 +552,11 @@ int c3o_vote_statistical(const uint8_t *evidence, int kind, int64_t replica_stri
             }
             fin[r] = isfinite(tau[r]) ? 1 : 0;
             if (fin[r]) s[nf++] = tau[r];
-            else B |= 1ULL << r;     /* a non-finite timing is an outlier */
+            else bm_set(B, r);       /* a non-finite timing is an outlier */
         }
         if (2 * nf <= R) {            /* finite values are not a majority */
             status[u] = O_INCONCLUSIVE;
-            bitmap[u] = 0;
+            bm_clear(B, R);
             majority_idx[u] = -1;
             continue;
         }
@@ -526,7 +572,7 @@ int c3o_vote_statistical(const uint8_t *evidence, int kind, int64_t replica_stri
         if (d != 0.0) {
             thr = kappa * d;
             for (r = 0; r < R; r++)
-                if (fin[r] && dev[r] > thr) B |= 1ULL << r;
+                if (fin[r] && dev[r] > thr) bm_set(B, r);
         }
         /* lower-median replica: the finite replica at sorted position
          * (nf-1)/2, ties broken by the lower replica index */
@@ -545,8 +591,7 @@ int c3o_vote_statistical(const uint8_t *evidence, int kind, int64_t replica_stri
                 }
             }
         }
-        bitmap[u] = B;
-        status[u] = B ? O_ATTRIBUTED : O_AGREE;
+        status[u] = bm_any(B, R) ? O_ATTRIBUTED : O_AGREE;
         majority_idx[u] = lowmed;
     }
     return 0;
@@ -556,23 +601,27 @@ int c3o_vote_statistical(const uint8_t *evidence, int kind, int64_t replica_stri
 /* Localization: every set bitmap bit, in (unit asc, replica asc) order; */
 /* the undecided (Inconclusive) units in ascending order.                */
 /* ------------------------------------------------------------------ */
-int c3o_localize(const uint8_t *status, const uint64_t *bitmap, const int32_t *majority_idx,
-                 int R, int64_t n_units,
+int c3o_localize(const uint8_t *status,
+                 const uint64_t *bitmap /* [n_units][ceil(R/64)] */,
+                 const int32_t *majority_idx, int R, int64_t n_units,
                  int64_t *out_unit, int32_t *out_replica, int32_t *out_majority, int64_t out_cap,
                  int64_t *undecided, int64_t und_cap, int64_t *counts)
 {
     int64_t u, no = 0, nu = 0, na = 0;
     int r;
+    const int W = bm_words(R);
+    if (R < 1 || R > O_MAX_R) return -1;
     for (u = 0; u < n_units; u++) {
+        const uint64_t *B = bitmap + u * W;
         if (status[u] == O_INCONCLUSIVE) {
             if (nu < und_cap) undecided[nu] = u;
             nu++;
             continue;
         }
-        if (bitmap[u] == 0) continue;
+        if (!bm_any(B, R)) continue;
         na++;
         for (r = 0; r < R; r++) {
-            if ((bitmap[u] >> r) & 1ULL) {
+            if (bm_test(B, r)) {
                 if (no < out_cap) {
                     out_unit[no] = u;
                     out_replica[no] = r;

@@ -331,6 +331,106 @@ def test_exact_vote_agrees_with_mjrty():
                 assert mj[u] == min(r for r in range(R) if ev[u, r] == m)
 
 
+def _row_int(bm, u, R):
+    """Outlier bitmap of unit u as one Python integer (bit r = replica r)."""
+    w = np.asarray(bm, np.uint64).reshape(-1, oracle.bitmap_words(R))[u]
+    return sum(int(x) << (64 * i) for i, x in enumerate(w))
+
+
+def _wide_rows(R, rng):
+    """Rows of R labels with their vote fixed by construction, not counted:
+    (labels, status, outlier set, majority replica)."""
+    rows = []
+    for kind in range(6):
+        for _ in range(8):
+            if kind == 0:      # everyone agrees
+                lab = np.full(R, 7)
+                rows.append((lab, oracle.AGREE, set(), 0))
+            elif kind == 1:    # a majority class of k > R/2 at random positions
+                k = int(rng.integers(R // 2 + 1, R + 1))
+                pos = rng.choice(R, size=k, replace=False)
+                lab = 1000 + np.arange(R)                 # all others distinct
+                lab[pos] = 5
+                out = set(range(R)) - set(pos.tolist())
+                rows.append((lab, oracle.ATTRIBUTED if out else oracle.AGREE, out, int(pos.min())))
+            elif kind == 2:    # replica 0 outside a bare majority
+                k = R // 2 + 1
+                pos = rng.choice(np.arange(1, R), size=k, replace=False)
+                lab = np.full(R, 3)
+                lab[pos] = 9
+                out = set(range(R)) - set(pos.tolist())
+                rows.append((lab, oracle.ATTRIBUTED, out, int(pos.min())))
+            elif kind == 3:    # two classes of R/2 (or a largest class below R/2)
+                lab = np.where(rng.permutation(R) < R // 2, 1, 2)
+                if R % 2:   # class 2 has (R + 1) / 2: move one of its members out
+                    lab[int(rng.choice(np.flatnonzero(lab == 2)))] = 3
+                rows.append((lab, oracle.INCONCLUSIVE, set(), -1))
+            elif kind == 4:    # many small classes
+                lab = rng.integers(0, 5, size=R)
+                while (np.bincount(lab).max() * 2) > R:
+                    lab = rng.integers(0, 5, size=R)
+                rows.append((lab, oracle.INCONCLUSIVE, set(), -1))
+            else:              # majority of exactly floor(R/2) + 1, rest in one other class
+                k = R // 2 + 1
+                pos = rng.choice(R, size=k, replace=False)
+                lab = np.full(R, 4)
+                lab[pos] = 8
+                out = set(range(R)) - set(pos.tolist())
+                rows.append((lab, oracle.ATTRIBUTED, out, int(pos.min())))
+    return rows
+
+
+@pytest.mark.parametrize("R", [65, 100, 127, 128, 129, 192, 255, 256])
+def test_exact_vote_wide_groups_by_construction(R):
+    """Peer groups above 64 (the paper's Table 2 lists degrees up to 192):
+    multi-word bitmaps, every word's bits where the construction puts them."""
+    rng = np.random.default_rng(R)
+    rows = _wide_rows(R, rng)
+    ev = np.array([r[0] for r in rows], np.uint64)
+    st, bm, mj = oracle.vote_exact(ev, replica_axis=1)
+    assert bm.shape == (len(rows), (R + 63) // 64)
+    for u, (_, want_st, out, want_mj) in enumerate(rows):
+        assert int(st[u]) == want_st, (u, want_st)
+        assert _row_int(bm, u, R) == sum(1 << r for r in out), u
+        assert int(mj[u]) == want_mj, u
+    # the replica-major layout gives the same votes
+    st2, bm2, mj2 = oracle.vote_exact(np.ascontiguousarray(ev.T), replica_axis=0)
+    assert np.array_equal(st, st2) and np.array_equal(bm, bm2) and np.array_equal(mj, mj2)
+
+
+def test_exact_vote_wide_groups_agree_with_mjrty():
+    rng = np.random.default_rng(29)
+    for R in (65, 96, 160, 192, 256):
+        ev = rng.integers(0, 3, size=(60, R)).astype(np.uint64)
+        ev[::3, : R // 2 + 2] = 1
+        st, bm, mj = oracle.vote_exact(ev, replica_axis=1)
+        for u in range(ev.shape[0]):
+            m = _mjrty(ev[u].tolist())
+            if m is None:
+                assert st[u] == oracle.INCONCLUSIVE and _row_int(bm, u, R) == 0
+            else:
+                assert _row_int(bm, u, R) == sum(1 << r for r in range(R) if ev[u, r] != m)
+                assert mj[u] == min(r for r in range(R) if ev[u, r] == m)
+
+
+def test_byte_vote_wide_group_by_construction():
+    rng = np.random.default_rng(31)
+    R = 130
+    rows = _wide_rows(R, rng)[::4]
+    chunks = [[np.full(24, lab[r] % 251, np.uint8) if lab[r] < 1000 else
+               np.frombuffer(int(lab[r]).to_bytes(24, "little"), np.uint8) for _, lab in
+               enumerate([row[0] for row in rows])] for r in range(R)]
+    st, bm, mj = oracle.vote_bytes(chunks)
+    for u, (_, want_st, out, want_mj) in enumerate(rows):
+        assert (int(st[u]), _row_int(bm, u, R), int(mj[u])) == (want_st, sum(1 << r for r in out),
+                                                                 want_mj), u
+
+
+def test_wide_groups_out_of_range():
+    with pytest.raises(ValueError):
+        oracle.vote_exact(np.zeros((257, 2), np.uint64))
+
+
 # ---------------------------------------------------------------------------
 # byte-equality definition == signature vote
 # ---------------------------------------------------------------------------
@@ -456,6 +556,31 @@ def test_statistical_vote_matches_numpy():
                 assert tau[u][mj[u]] == srt[(fin.sum() - 1) // 2]
 
 
+@pytest.mark.parametrize("R", [65, 128, 192, 256])
+def test_statistical_vote_wide_groups_match_numpy(R):
+    rng = np.random.default_rng(37 + R)
+    k = oracle.KAPPA_DEFAULT
+    tau = np.exp(rng.standard_normal((80, R)) * 0.02)
+    tau[::5, 70 % R] *= 1.4                            # a slow replica in a high word
+    tau[::7, R - 1] *= 0.6
+    tau[3, : R // 2 + 1] = 1.0                         # majority equal: MAD 0, IQR path
+    tau[9] = 1.0
+    tau[9, R - 2] = 1.5                                # all equal but one: range path
+    tau[11, 64 % R] = np.nan
+    tau[12, : R // 2] = np.inf                         # finite values a majority only for odd R
+    for dt in (np.float32, np.float64):
+        t = tau.astype(dt)
+        st, bm, mj = oracle.vote_statistical(t, k, replica_axis=1)
+        for u in range(t.shape[0]):
+            ws, wb = _stat_numpy(t[u], k)
+            assert (int(st[u]), _row_int(bm, u, R)) == (ws, wb), (R, dt, u)
+            if ws != oracle.INCONCLUSIVE:
+                x = t[u].astype(np.float64)
+                fin = np.isfinite(x)
+                order = [r for r in np.argsort(np.where(fin, x, np.inf), kind="stable") if fin[r]]
+                assert mj[u] == order[(fin.sum() - 1) // 2]
+
+
 def test_statistical_nonfinite_majority_is_inconclusive():
     ev = np.array([[1.0, np.nan, np.inf, 1.0]], np.float64)
     st, bm, mj = oracle.vote_statistical(ev, replica_axis=1)
@@ -482,6 +607,27 @@ def test_localize_brute_force_and_truncation():
     assert cut["counts"].tolist() == loc["counts"].tolist()
     assert list(zip(cut["unit"].tolist(), cut["replica"].tolist())) == want[:3]
     assert cut["undecided"].tolist() == und[:2]
+
+
+@pytest.mark.parametrize("R", [65, 192, 256])
+def test_localize_wide_groups_brute_force(R):
+    rng = np.random.default_rng(41 + R)
+    U = 300
+    ev = rng.integers(0, 2, size=(U, R)).astype(np.uint64)
+    ev[rng.random(U) < 0.6] = 0
+    ev[::9, R - 3:] = 5                                  # outliers in the last word
+    st, bm, mj = oracle.vote_exact(ev, replica_axis=1)
+    want = [(u, r) for u in range(U) for r in range(R) if (_row_int(bm, u, R) >> r) & 1]
+    und = [u for u in range(U) if st[u] == oracle.INCONCLUSIVE]
+    assert any(r >= 64 for _, r in want)
+    loc = oracle.localize(st, bm, mj, R)
+    assert list(zip(loc["unit"].tolist(), loc["replica"].tolist())) == want
+    assert loc["undecided"].tolist() == und
+    n_att = sum(1 for u in range(U) if _row_int(bm, u, R) != 0)
+    assert loc["counts"].tolist() == [len(want), len(und), n_att]
+    cut = oracle.localize(st, bm, mj, R, out_cap=5, und_cap=1)
+    assert list(zip(cut["unit"].tolist(), cut["replica"].tolist())) == want[:5]
+    assert cut["counts"].tolist() == loc["counts"].tolist()
 
 
 @pytest.mark.parametrize("T,W", [(64, 16), (10, 16), (40, 5), (1, 16)])
