@@ -54,7 +54,16 @@ typedef struct ihipStream_t *c3_stream_t;
 typedef struct ihipEvent_t *c3_event_t;
 
 #define C3_ABI_VERSION 1
-#define C3_MAX_REPLICAS 64 /* one 64-bit outlier bitmap word per unit */
+/* Replicas per peer group.  c3_signature, c3_tensor_signature, c3_consensus
+ * and c3_localize take up to C3_MAX_PEERS (the data-parallel peer degrees the
+ * paper tabulates reach 192, Table 2); the fused entry points
+ * (c3_timing_consensus, c3_confirm, c3_adamw_slice, c3_optimizer_check) take
+ * up to C3_MAX_REPLICAS. */
+#define C3_MAX_REPLICAS 64
+#define C3_MAX_PEERS 256
+/* 64-bit words of one unit's outlier bitmap: bit b of word w names replica
+ * 64 w + b (Sec. 5.1's N-bit B).  One word for R <= 64. */
+#define C3_BITMAP_WORDS(R) (((R) + 63) / 64)
 #define C3_MAX_NDIM 8
 
 typedef enum {
@@ -208,7 +217,7 @@ size_t c3_signature_workspace_size_ex(const c3_tensor_meta_t *metas, int T, int 
  *               be 16-byte aligned (C3_E_ALIGN) and non-NULL unless the
  *               tensor is empty.
  *   metas       host array [T]; shared by all replicas.
- *   T, R        tensors per replica (>= 1) and replicas (1..64).  Records
+ *   T, R        tensors per replica (>= 1) and replicas (1..C3_MAX_PEERS).  Records
  *               are per replica and do not depend on R: with R = 1 a rank
  *               signs its own replica, as each rank of a group spread over
  *               GPUs would before the records are gathered (Algorithm 1's
@@ -237,6 +246,7 @@ int c3_signature_ex(const void *const *ptrs, const c3_tensor_meta_t *metas, int 
  *   records  device [R][C] as written by c3_signature (tensor ids must be
  *            non-decreasing along each replica's row, as c3_signature
  *            writes them).
+ *   R        replicas, 1..C3_MAX_PEERS.
  *   T        number of tensors (>= 1).
  *   out      device [R][T] u64, 8-byte aligned.  Vote on it with
  *            c3_consensus(out, C3_EV_U64, T * 8, 8, R, T, C3_EXACT, ...).
@@ -361,9 +371,9 @@ int c3_optimizer_check(const c3_optimizer_state_t *st, int64_t k, const c3_adamw
  *     |x_r - m| > kappa * d.  majority_idx = replica at the lower median.
  *     kappa > 0 (C3_KAPPA_DEFAULT recommended); ignored for EXACT.
  *
- *   status [n_units] u8 (c3_verdict_t), bitmap [n_units] u64 (8-byte
- *   aligned), majority_idx [n_units] i32 (-1 when Inconclusive); device.
- *   R in 1..64 (R = 1 gives Agree), n_units >= 0.
+ *   status [n_units] u8 (c3_verdict_t), bitmap [n_units][C3_BITMAP_WORDS(R)]
+ *   u64 (8-byte aligned), majority_idx [n_units] i32 (-1 when Inconclusive);
+ *   device.  R in 1..C3_MAX_PEERS (R = 1 gives Agree), n_units >= 0.
  */
 int c3_consensus(const void *evidence, int evidence_kind, int64_t replica_stride_bytes,
                  int64_t unit_stride_bytes, int R, int64_t n_units, int mode, double kappa,
@@ -377,6 +387,8 @@ size_t c3_localize_workspace_size(int64_t n_units);
  * chunk, what summary (Sec. 5.1: B[i] = 1 attributes the divergence to peer
  * i; Sec. 9: reports keep the peers and bitmaps).
  *
+ *   status, bitmap, majority_idx  as c3_consensus writes them: bitmap is
+ *              [n_units][C3_BITMAP_WORDS(R)] u64; R in 1..C3_MAX_PEERS.
  *   outliers   device [out_cap]: one entry per set bitmap bit, ordered by
  *              (unit ascending, replica ascending).  With records (device
  *              [R][n_units], may be NULL) each entry carries the outlier's

@@ -37,6 +37,8 @@ EXACT, STATISTICAL = 0, 1
 EV_U64, EV_U32, EV_F32, EV_F64 = 0, 1, 2, 3
 AGREE, ATTRIBUTED, INCONCLUSIVE = 0, 1, 2
 KAPPA_DEFAULT = 3.5 / 0.6745
+MAX_REPLICAS = 64    # fused entry points: timing consensus, confirm, AdamW replay, optimizer check
+MAX_PEERS = 256      # signature, tensor signature, consensus, localize
 RANK_STRAGGLER, RANK_PROTOCOL, RANK_CONSEC2 = 1, 2, 4
 OUTCOME_OK, OUTCOME_STRAGGLER, OUTCOME_SDC, OUTCOME_HANG = 0, 1, 2, 3
 OPT_PLAN_STAGED = 1
@@ -184,6 +186,20 @@ def _dev_tensor(t: torch.Tensor, name: str) -> torch.Tensor:
     return t
 
 
+def _check_out(t, dtype, numel: int, name: str):
+    """A caller-supplied output must hold what the kernels write."""
+    _dev_tensor(t, name)
+    if t.dtype != dtype:
+        raise C3Error(f"{name} must be {dtype}, got {t.dtype}")
+    if t.numel() < numel:
+        raise C3Error(f"{name} holds {t.numel()} values, needs {numel}")
+
+
+def bitmap_words(R: int) -> int:
+    """int64 words of one unit's outlier bitmap (C3_BITMAP_WORDS)."""
+    return (R + 63) // 64
+
+
 def _ptr(t):
     return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
 
@@ -301,7 +317,9 @@ def consensus(evidence: torch.Tensor, mode: int = EXACT, *, kind: int = None, R:
 
     ``evidence`` is either the records tensor [R, C, 64] (signatures are voted)
     or a value tensor [U, R] / [..., R] of int64/float32/float64 with the
-    replicas on the last axis.  Strides are in bytes.
+    replicas on the last axis.  Strides are in bytes.  The bitmap is [U]
+    int64 for R <= 64 and [U, bitmap_words(R)] above (bit b of word w names
+    replica 64 w + b).
     """
     _dev_tensor(evidence, "evidence")
     if evidence.dtype == torch.uint8 and evidence.dim() == 3 and evidence.shape[2] == 64:
@@ -321,11 +339,15 @@ def consensus(evidence: torch.Tensor, mode: int = EXACT, *, kind: int = None, R:
         unit_stride = R * es if unit_stride is None else unit_stride
         n_units = evidence.numel() // R if n_units is None else n_units
     dev = evidence.device
+    W = bitmap_words(R) if 1 <= R <= MAX_PEERS else 1
     if out is not None:
         status, bitmap, maj = out
+        _check_out(status, torch.uint8, n_units, "status")
+        _check_out(bitmap, torch.int64, n_units * W, "bitmap")
+        _check_out(maj, torch.int32, n_units, "majority")
     else:
         status = _empty((n_units,), torch.uint8, dev)
-        bitmap = _empty((n_units,), torch.int64, dev)
+        bitmap = _empty((n_units,) if W == 1 else (n_units, W), torch.int64, dev)
         maj = _empty((n_units,), torch.int32, dev)
     rc = lib().c3_consensus(_ptr(evidence), kind, replica_stride, unit_stride, R, n_units, mode,
                             float(kappa), _ptr(status), _ptr(bitmap), _ptr(maj), _stream(stream))
@@ -335,12 +357,16 @@ def consensus(evidence: torch.Tensor, mode: int = EXACT, *, kind: int = None, R:
 
 def localize(status, bitmap, majority_idx, records=None, R: int = None, out_cap: int = None,
              und_cap: int = None, stream=None, out=None, workspace=None):
-    """Outlier entries [out_cap, 80] (uint8), undecided [und_cap] int64, counts [3] int64."""
+    """Outlier entries [out_cap, 80] (uint8), undecided [und_cap] int64, counts [3] int64.
+    ``bitmap`` holds bitmap_words(R) int64 words per unit, as consensus writes it."""
     n_units = status.numel()
     if R is None:
         if records is None:
             raise C3Error("R is required without records")
         R = records.shape[0]
+    if 1 <= R <= MAX_PEERS and n_units > 0:
+        _check_out(bitmap, torch.int64, n_units * bitmap_words(R), "bitmap")
+        _check_out(majority_idx, torch.int32, n_units, "majority")
     dev = status.device
     out_cap = n_units * R if out_cap is None else out_cap
     und_cap = n_units if und_cap is None else und_cap

@@ -79,7 +79,7 @@ struct Plan {
 // Builds the plan; returns C3_OK or an error code.
 int make_plan(const c3_tensor_meta_t* metas, int T, int R, uint64_t chunk_bytes,
               uint64_t tile_bytes, Plan& p) {
-    if (metas == nullptr || T < 1 || R < 1 || R > C3_MAX_REPLICAS) return C3_E_INVAL;
+    if (metas == nullptr || T < 1 || R < 1 || R > C3_MAX_PEERS) return C3_E_INVAL;
     if (chunk_bytes == 0 || chunk_bytes % 1024 != 0 || chunk_bytes > (1ull << 40)) return C3_E_INVAL;
     if (tile_bytes == 0) tile_bytes = default_tile(chunk_bytes);
     if (tile_bytes < 1024 || (tile_bytes & (tile_bytes - 1)) != 0 || chunk_bytes % tile_bytes != 0 ||
@@ -381,7 +381,7 @@ int c3_signature(const void* const* ptrs, const c3_tensor_meta_t* metas, int T, 
 
 int c3_tensor_signature(const c3_chunk_record_t* records, int R, int64_t C, int T, uint64_t* out,
                         c3_stream_t stream) {
-    if (R < 1 || R > C3_MAX_REPLICAS || C < 0 || T < 1 || C > (int64_t)0x7FFFFFFF * 64)
+    if (R < 1 || R > C3_MAX_PEERS || C < 0 || T < 1 || C > (int64_t)0x7FFFFFFF * 64)
         return C3_E_INVAL;
     if (out == nullptr || (C > 0 && records == nullptr)) return C3_E_INVAL;
     if (!aligned(records, 8) || !aligned(out, 8)) return C3_E_ALIGN;
@@ -408,7 +408,7 @@ int c3_adamw_slice(const float* const* param, const float* const* grad, const fl
 int c3_consensus(const void* evidence, int evidence_kind, int64_t replica_stride_bytes,
                  int64_t unit_stride_bytes, int R, int64_t n_units, int mode, double kappa,
                  uint8_t* status, uint64_t* bitmap, int32_t* majority_idx, c3_stream_t stream) {
-    if (R < 1 || R > C3_MAX_REPLICAS || n_units < 0) return C3_E_INVAL;
+    if (R < 1 || R > C3_MAX_PEERS || n_units < 0) return C3_E_INVAL;
     if (mode != C3_EXACT && mode != C3_STATISTICAL) return C3_E_INVAL;
     int vsize;
     switch (evidence_kind) {
@@ -441,7 +441,7 @@ int c3_localize(const uint8_t* status, const uint64_t* bitmap, const int32_t* ma
                 const c3_chunk_record_t* records, int R, int64_t n_units, c3_outlier_t* outliers,
                 int64_t out_cap, int64_t* undecided, int64_t und_cap, int64_t* counts, void* ws,
                 size_t ws_bytes, c3_stream_t stream) {
-    if (R < 1 || R > C3_MAX_REPLICAS || n_units < 0 || out_cap < 0 || und_cap < 0)
+    if (R < 1 || R > C3_MAX_PEERS || n_units < 0 || out_cap < 0 || und_cap < 0)
         return C3_E_INVAL;
     if (counts == nullptr) return C3_E_INVAL;
     if (n_units > 0 && (status == nullptr || bitmap == nullptr || majority_idx == nullptr))

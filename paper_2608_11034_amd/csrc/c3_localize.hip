@@ -12,7 +12,8 @@
 //                 through LDS, and writes entries at segment offset + local
 //                 offset while that position is below the caller's capacity.
 // A thread owns kPerThread consecutive units, so list order is (unit
-// ascending, replica ascending) by construction.
+// ascending, replica ascending) by construction.  A unit's bitmap is W =
+// ceil(R / 64) words, bit b of word w naming replica 64 w + b.
 #include "c3_device.h"
 #include "c3_internal.h"
 
@@ -26,8 +27,16 @@ struct SegCount {
     int64_t n_out, n_und, n_att;
 };
 
-__device__ inline void thread_counts(const uint8_t* status, const uint64_t* bitmap, int64_t u0,
-                                     int64_t n_units, int64_t& o, int64_t& un, int64_t& at) {
+// Set bits of unit u's bitmap.
+__device__ inline int unit_popcount(const uint64_t* bitmap, int W, int64_t u) {
+    int n = 0;
+    for (int w = 0; w < W; ++w) n += __builtin_popcountll(bitmap[u * W + w]);
+    return n;
+}
+
+__device__ inline void thread_counts(const uint8_t* status, const uint64_t* bitmap, int W,
+                                     int64_t u0, int64_t n_units, int64_t& o, int64_t& un,
+                                     int64_t& at) {
     o = un = at = 0;
     for (int i = 0; i < kPerThread; ++i) {
         const int64_t u = u0 + i;
@@ -36,10 +45,10 @@ __device__ inline void thread_counts(const uint8_t* status, const uint64_t* bitm
         if (s == C3_INCONCLUSIVE) {
             ++un;
         } else {
-            const uint64_t b = bitmap[u];
-            if (b) {
+            const int n = unit_popcount(bitmap, W, u);
+            if (n) {
                 ++at;
-                o += __builtin_popcountll(b);
+                o += n;
             }
         }
     }
@@ -68,12 +77,12 @@ __device__ inline int64_t block_inclusive_scan(int64_t v, int64_t* lds_wave, int
 }
 
 __global__ void __launch_bounds__(kLocThreads) localize_count_kernel(
-    const uint8_t* __restrict__ status, const uint64_t* __restrict__ bitmap, int64_t n_units,
-    SegCount* __restrict__ seg) {
+    const uint8_t* __restrict__ status, const uint64_t* __restrict__ bitmap, int W,
+    int64_t n_units, SegCount* __restrict__ seg) {
     __shared__ int64_t lds[3][kLocThreads / 64];
     const int64_t u0 = (int64_t)blockIdx.x * kSegUnits + (int64_t)threadIdx.x * kPerThread;
     int64_t o, un, at;
-    thread_counts(status, bitmap, u0, n_units, o, un, at);
+    thread_counts(status, bitmap, W, u0, n_units, o, un, at);
     int64_t to, tu, ta;
     block_inclusive_scan(o, lds[0], to);
     block_inclusive_scan(un, lds[1], tu);
@@ -109,7 +118,7 @@ __global__ void __launch_bounds__(kLocThreads) localize_scan_kernel(SegCount* __
 __device__ inline void emit_units(const uint8_t* __restrict__ status,
                                   const uint64_t* __restrict__ bitmap,
                                   const int32_t* __restrict__ majority_idx,
-                                  const c3_chunk_record_t* __restrict__ records, int R,
+                                  const c3_chunk_record_t* __restrict__ records, int R, int W,
                                   int64_t n_units, int64_t u0, int64_t po, int64_t pu,
                                   c3_outlier_t* __restrict__ outliers, int64_t out_cap,
                                   int64_t* __restrict__ undecided, int64_t und_cap);
@@ -146,16 +155,16 @@ __device__ inline void write_outlier(c3_outlier_t* dst, int64_t u, int r, int32_
 __global__ void __launch_bounds__(kLocThreads) localize_emit_kernel(
     const uint8_t* __restrict__ status, const uint64_t* __restrict__ bitmap,
     const int32_t* __restrict__ majority_idx, const c3_chunk_record_t* __restrict__ records, int R,
-    int64_t n_units, const SegCount* __restrict__ seg, c3_outlier_t* __restrict__ outliers,
+    int W, int64_t n_units, const SegCount* __restrict__ seg, c3_outlier_t* __restrict__ outliers,
     int64_t out_cap, int64_t* __restrict__ undecided, int64_t und_cap) {
     __shared__ int64_t lds[2][kLocThreads / 64];
     const int64_t u0 = (int64_t)blockIdx.x * kSegUnits + (int64_t)threadIdx.x * kPerThread;
     int64_t o, un, at;
-    thread_counts(status, bitmap, u0, n_units, o, un, at);
+    thread_counts(status, bitmap, W, u0, n_units, o, un, at);
     int64_t to, tu;
     int64_t po = block_inclusive_scan(o, lds[0], to) - o + seg[blockIdx.x].n_out;
     int64_t pu = block_inclusive_scan(un, lds[1], tu) - un + seg[blockIdx.x].n_und;
-    emit_units(status, bitmap, majority_idx, records, R, n_units, u0, po, pu, outliers, out_cap,
+    emit_units(status, bitmap, majority_idx, records, R, W, n_units, u0, po, pu, outliers, out_cap,
                undecided, und_cap);
 }
 
@@ -164,7 +173,7 @@ __global__ void __launch_bounds__(kLocThreads) localize_emit_kernel(
 __device__ inline void emit_units(const uint8_t* __restrict__ status,
                                   const uint64_t* __restrict__ bitmap,
                                   const int32_t* __restrict__ majority_idx,
-                                  const c3_chunk_record_t* __restrict__ records, int R,
+                                  const c3_chunk_record_t* __restrict__ records, int R, int W,
                                   int64_t n_units, int64_t u0, int64_t po, int64_t pu,
                                   c3_outlier_t* __restrict__ outliers, int64_t out_cap,
                                   int64_t* __restrict__ undecided, int64_t und_cap) {
@@ -176,45 +185,58 @@ __device__ inline void emit_units(const uint8_t* __restrict__ status,
             ++pu;
             continue;
         }
-        uint64_t b = bitmap[u];
-        if (!b) continue;
         const int32_t mj = majority_idx[u];
-        while (b) {
-            const int r = __builtin_ctzll(b);
-            b &= b - 1;
-            if (po < out_cap) write_outlier(&outliers[po], u, r, mj, records, R, n_units);
-            ++po;
+        for (int w = 0; w < W; ++w) {
+            uint64_t b = bitmap[u * W + w];
+            while (b) {
+                const int r = 64 * w + __builtin_ctzll(b);
+                b &= b - 1;
+                if (po < out_cap) write_outlier(&outliers[po], u, r, mj, records, R, n_units);
+                ++po;
+            }
         }
     }
 }
 
 // Small inputs: one workgroup of kSingleThreads walks the units in rounds of
 // kSingleThreads * kPerThread, carrying list offsets between rounds.  One
-// launch instead of three.  Each thread loads its units once and keeps them
-// in registers; the three per-thread counts travel through a single scan
-// packed into 21-bit fields of one 64-bit word (a round holds at most
-// 1024 * 8 * 64 = 2^19 outliers, so no field overflows).
+// launch instead of three.  Each thread loads its units once (one-word
+// bitmaps stay in registers; wider ones are counted on load and read again
+// to emit); the three per-thread counts travel through a single scan packed
+// into one 64-bit word: outliers in the low 24 bits (a round holds at most
+// 1024 * 8 units * 256 replicas = 2^21), undecided and attributed units in
+// 20 bits each (at most 2^13 per round), so no field overflows.
 constexpr int kSingleThreads = 1024;
 constexpr int64_t kSingleMaxUnits = 4 * (int64_t)kSingleThreads * kPerThread;
-constexpr int kField = 21;
-constexpr int64_t kFieldMask = (1ll << kField) - 1;
+constexpr int kOutBits = 24;
+constexpr int kUnitBits = 20;
+constexpr int64_t kOutMask = (1ll << kOutBits) - 1;
+constexpr int64_t kUnitMask = (1ll << kUnitBits) - 1;
+static_assert((int64_t)kSingleThreads * kPerThread * C3_MAX_PEERS <= kOutMask,
+              "outlier field too narrow");
+static_assert((int64_t)kSingleThreads * kPerThread <= kUnitMask, "unit fields too narrow");
+static_assert(kOutBits + 2 * kUnitBits <= 64, "fields exceed one word");
 
+template <bool WIDE>
 __global__ void __launch_bounds__(kSingleThreads) localize_single_kernel(
     const uint8_t* __restrict__ status, const uint64_t* __restrict__ bitmap,
     const int32_t* __restrict__ majority_idx, const c3_chunk_record_t* __restrict__ records, int R,
-    int64_t n_units, c3_outlier_t* __restrict__ outliers, int64_t out_cap,
+    int W, int64_t n_units, c3_outlier_t* __restrict__ outliers, int64_t out_cap,
     int64_t* __restrict__ undecided, int64_t und_cap, int64_t* __restrict__ counts) {
     __shared__ int64_t lds[kSingleThreads / 64];
     int64_t carry_o = 0, carry_u = 0, carry_a = 0;
     for (int64_t base = 0; base < n_units; base += (int64_t)kSingleThreads * kPerThread) {
         const int64_t u0 = base + (int64_t)threadIdx.x * kPerThread;
         uint8_t st[kPerThread];
-        uint64_t bm[kPerThread];
+        uint64_t bm[kPerThread];  // the word (one-word bitmaps) or the set-bit count
 #pragma unroll
         for (int i = 0; i < kPerThread; ++i) {
             const int64_t u = u0 + i;
             st[i] = u < n_units ? status[u] : (uint8_t)C3_AGREE;
-            bm[i] = u < n_units ? bitmap[u] : 0ull;
+            if constexpr (WIDE)
+                bm[i] = u < n_units ? (uint64_t)unit_popcount(bitmap, W, u) : 0ull;
+            else
+                bm[i] = u < n_units ? bitmap[u] : 0ull;
         }
         int64_t o = 0, un = 0, at = 0;
 #pragma unroll
@@ -223,14 +245,14 @@ __global__ void __launch_bounds__(kSingleThreads) localize_single_kernel(
                 ++un;
             } else if (bm[i]) {
                 ++at;
-                o += __builtin_popcountll(bm[i]);
+                o += WIDE ? (int64_t)bm[i] : __builtin_popcountll(bm[i]);
             }
         }
-        const int64_t packed = o | (un << kField) | (at << (2 * kField));
+        const int64_t packed = o | (un << kOutBits) | (at << (kOutBits + kUnitBits));
         int64_t tot;
         const int64_t excl = block_inclusive_scan<kSingleThreads>(packed, lds, tot) - packed;
-        int64_t po = carry_o + (excl & kFieldMask);
-        int64_t pu = carry_u + ((excl >> kField) & kFieldMask);
+        int64_t po = carry_o + (excl & kOutMask);
+        int64_t pu = carry_u + ((excl >> kOutBits) & kUnitMask);
 #pragma unroll
         for (int i = 0; i < kPerThread; ++i) {
             const int64_t u = u0 + i;
@@ -239,19 +261,21 @@ __global__ void __launch_bounds__(kSingleThreads) localize_single_kernel(
                 ++pu;
                 continue;
             }
-            uint64_t b = bm[i];
-            if (!b) continue;
+            if (!bm[i]) continue;
             const int32_t mj = majority_idx[u];
-            while (b) {
-                const int r = __builtin_ctzll(b);
-                b &= b - 1;
-                if (po < out_cap) write_outlier(&outliers[po], u, r, mj, records, R, n_units);
-                ++po;
+            for (int w = 0; w < (WIDE ? W : 1); ++w) {
+                uint64_t b = WIDE ? bitmap[u * W + w] : bm[i];
+                while (b) {
+                    const int r = 64 * w + __builtin_ctzll(b);
+                    b &= b - 1;
+                    if (po < out_cap) write_outlier(&outliers[po], u, r, mj, records, R, n_units);
+                    ++po;
+                }
             }
         }
-        carry_o += tot & kFieldMask;
-        carry_u += (tot >> kField) & kFieldMask;
-        carry_a += (tot >> (2 * kField)) & kFieldMask;
+        carry_o += tot & kOutMask;
+        carry_u += (tot >> kOutBits) & kUnitMask;
+        carry_a += (tot >> (kOutBits + kUnitBits)) & kUnitMask;
     }
     if (threadIdx.x == 0) {
         counts[0] = carry_o;
@@ -270,10 +294,16 @@ hipError_t launch_localize(const uint8_t* status, const uint64_t* bitmap,
                            int64_t n_units, c3_outlier_t* outliers, int64_t out_cap,
                            int64_t* undecided, int64_t und_cap, int64_t* counts, void* ws,
                            hipStream_t stream) {
+    const int W = (R + 63) / 64;
     if (n_units <= kSingleMaxUnits) {
-        hipLaunchKernelGGL(localize_single_kernel, dim3(1), dim3(kSingleThreads), 0, stream, status,
-                           bitmap, majority_idx, records, R, n_units, outliers, out_cap, undecided,
-                           und_cap, counts);
+        if (W == 1)
+            hipLaunchKernelGGL(localize_single_kernel<false>, dim3(1), dim3(kSingleThreads), 0,
+                               stream, status, bitmap, majority_idx, records, R, W, n_units,
+                               outliers, out_cap, undecided, und_cap, counts);
+        else
+            hipLaunchKernelGGL(localize_single_kernel<true>, dim3(1), dim3(kSingleThreads), 0,
+                               stream, status, bitmap, majority_idx, records, R, W, n_units,
+                               outliers, out_cap, undecided, und_cap, counts);
         return hipGetLastError();
     }
     const int64_t n_seg = (n_units + kSegUnits - 1) / kSegUnits;
@@ -281,7 +311,7 @@ hipError_t launch_localize(const uint8_t* status, const uint64_t* bitmap,
     SegCount* seg = static_cast<SegCount*>(ws);
     if (n_seg > 0) {
         hipLaunchKernelGGL(localize_count_kernel, dim3((unsigned)n_seg), dim3(kLocThreads), 0, stream,
-                           status, bitmap, n_units, seg);
+                           status, bitmap, W, n_units, seg);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
@@ -290,7 +320,7 @@ hipError_t launch_localize(const uint8_t* status, const uint64_t* bitmap,
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || n_seg == 0) return e;
     hipLaunchKernelGGL(localize_emit_kernel, dim3((unsigned)n_seg), dim3(kLocThreads), 0, stream,
-                       status, bitmap, majority_idx, records, R, n_units, seg, outliers, out_cap,
+                       status, bitmap, majority_idx, records, R, W, n_units, seg, outliers, out_cap,
                        undecided, und_cap);
     return hipGetLastError();
 }

@@ -81,7 +81,9 @@ def test_plan_rejects_bad_arguments():
     assert L.c3_num_chunks(_metas([(c3.F32, (-1,))]), 1, 1024) == -1
     assert L.c3_signature_workspace_size(md, 1, 0, 1024) == 0        # R = 0
     assert L.c3_signature_workspace_size(md, 1, 1, 1024) > 0         # one replica
-    assert L.c3_signature_workspace_size(md, 1, 65, 1024) == 0       # R > 64
+    assert L.c3_signature_workspace_size(md, 1, 65, 1024) > 0        # wide peer groups
+    assert L.c3_signature_workspace_size(md, 1, 256, 1024) > 0
+    assert L.c3_signature_workspace_size(md, 1, 257, 1024) == 0      # R > C3_MAX_PEERS
     assert L.c3_signature_workspace_size(md, 1, 8, 1024) > 0
     assert L.c3_signature_workspace_size_ex(md, 1, 8, 4096, 3072) == 0   # tile not a power of 2
     assert L.c3_signature_workspace_size_ex(md, 1, 8, 4096, 8192) == 0   # tile larger than chunk
@@ -95,7 +97,7 @@ def test_argument_errors_return_before_gpu_work():
     rec = ctypes.c_void_p(64)
     ws = ctypes.c_void_p(256)
     assert L.c3_signature(ptrs, md, 1, 0, 1024, rec, ws, 1 << 20, null) == -1     # R = 0
-    assert L.c3_signature(ptrs, md, 1, 65, 1024, rec, ws, 1 << 20, null) == -1    # R > 64
+    assert L.c3_signature(ptrs, md, 1, 257, 1024, rec, ws, 1 << 20, null) == -1   # R > 256
     assert L.c3_signature(ptrs, md, 1, 2, 1000, rec, ws, 1 << 20, null) == -1     # chunk
     assert L.c3_signature(ptrs, md, 1, 2, 1024, rec, null, 1 << 20, null) == -4   # workspace
     assert L.c3_signature(ptrs, md, 1, 2, 1024, rec, ws, 8, null) == -4           # too small
@@ -113,6 +115,13 @@ def test_argument_errors_return_before_gpu_work():
                           null, null, null, null) == 0                          # nothing to do
     assert L.c3_localize(null, null, null, null, 4, 10, null, 0, null, 0, ctypes.c_void_p(8),
                          ctypes.c_void_p(256), 4096, null) == -1
+    assert L.c3_consensus(ctypes.c_void_p(8), c3.EV_U64, 8, 64, 257, 10, c3.EXACT, 1.0,
+                          ctypes.c_void_p(8), ctypes.c_void_p(8), ctypes.c_void_p(8), null) == -1
+    assert L.c3_consensus(ctypes.c_void_p(8), c3.EV_U64, 8, 64, 256, 0, c3.EXACT, 1.0,
+                          null, null, null, null) == 0                          # R = 256 valid
+    assert L.c3_localize(null, null, null, null, 257, 0, null, 0, null, 0, ctypes.c_void_p(8),
+                         ctypes.c_void_p(256), 4096, null) == -1                # R > 256
+    assert L.c3_tensor_signature(null, 257, 0, 1, ctypes.c_void_p(8), null) == -1
     assert L.c3_confirm(null, null, 8, 4, 16, 0, ctypes.c_void_p(8), ctypes.c_void_p(256), 4096,
                         null) == -1                                              # window 0
     assert L.c3_tensor_signature(null, 8, 10, 0, ctypes.c_void_p(8), null) == -1

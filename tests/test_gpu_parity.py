@@ -292,8 +292,8 @@ def test_argument_errors():
                           ctypes.c_void_p(ws.data_ptr()), ws.numel(), s) == -2    # alignment
     assert L.c3_signature(p2, metas, 1, 2, 1024, ctypes.c_void_p(rec.data_ptr()),
                           ctypes.c_void_p(ws.data_ptr()), 16, s) == -4            # workspace
-    assert L.c3_signature(p2, metas, 1, 65, 1024, ctypes.c_void_p(rec.data_ptr()),
-                          ctypes.c_void_p(ws.data_ptr()), ws.numel(), s) == -1    # R > 64
+    assert L.c3_signature(p2, metas, 1, 257, 1024, ctypes.c_void_p(rec.data_ptr()),
+                          ctypes.c_void_p(ws.data_ptr()), ws.numel(), s) == -1    # R > 256
     torch.cuda.synchronize()
 
 
