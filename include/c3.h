@@ -178,7 +178,8 @@ typedef struct {
  *     to the workspace since; staging is skipped.  The caller is responsible
  *     for that promise: a stale plan reads stale pointers.
  *   tile_bytes: bytes one workgroup folds into one partial; 0 chooses the
- *     default.  Must be a power-of-two multiple of 1024 dividing chunk_bytes
+ *     default (the largest power of two up to 256 KiB dividing chunk_bytes).
+ *     Must be a power-of-two multiple of 1024 dividing chunk_bytes
  *     (checked); the fp64 sums may differ in the last bits between tile
  *     sizes, everything else is identical. */
 typedef struct {

@@ -54,7 +54,7 @@ static_assert(sizeof(c3_chunk_record_t) == 64, "record layout");
 // Tuning knobs of the streaming kernel (compile-time; results do not depend
 // on them except for the last bits of the fp64 sums through the tile size).
 #ifndef C3_SIG_TILE_MAX
-#define C3_SIG_TILE_MAX (1024 * 1024)
+#define C3_SIG_TILE_MAX (256 * 1024)
 #endif
 #ifndef C3_SIG_UNROLL
 #define C3_SIG_UNROLL 16
