@@ -7,7 +7,10 @@
  *     is attributed, majority replica 0, no undecided chunk;
  *   - the outlier's summary is the records' (NaN count after an exponent
  *     flip that makes a NaN, absmax of the majority);
- *   - argument errors come back as codes with nothing launched.
+ *   - argument errors come back as codes with nothing launched;
+ *   - a 130-replica group (C3_BITMAP_WORDS(130) = 3 words per unit): the
+ *     outliers planted in replicas 1, 64 and 129 land in the right words and
+ *     list entries, a replica-0 fault is attributed with majority replica 1.
  * Built by the package build next to libc3.so; run by tests/test_gpu_c_abi.py.
  * Prints "ok" and exits 0 on success.
  */
@@ -139,6 +142,66 @@ int main(void) {
     CHECK(isfinite(b.outliers[0].sum[0]) && isfinite(b.outliers[0].sum[1]));
     for (int64_t c = 0; c < C; ++c)
         CHECK(b.status[c] == (c == b.outliers[0].chunk ? C3_ATTRIBUTED : C3_AGREE));
+
+    /* a wide peer group: U units x 130 replicas of u64 evidence, unit-major */
+    {
+        enum { RW = 130, UW = 1000 };
+        const int W = C3_BITMAP_WORDS(RW);
+        uint64_t *hev = (uint64_t *)malloc(sizeof(uint64_t) * RW * UW);
+        uint64_t *dev_ev, *dbm, hbm[3];
+        uint8_t *dst, hst[UW];
+        int32_t *dmj, hmj[UW];
+        CHECK(W == 3 && hev != NULL);
+        for (int u = 0; u < UW; ++u)
+            for (int r = 0; r < RW; ++r) hev[(size_t)u * RW + r] = 0x1234567890ull * (uint64_t)(u + 1);
+        hev[(size_t)10 * RW + 1] ^= 1;   /* unit 10: replica 1 (word 0) */
+        hev[(size_t)10 * RW + 64] ^= 2;  /* unit 10: replica 64 (word 1) */
+        hev[(size_t)500 * RW + 129] ^= 4; /* unit 500: replica 129 (word 2) */
+        hev[(size_t)777 * RW + 0] ^= 8;  /* unit 777: replica 0 is the outlier */
+        HIP_OK(hipMalloc((void **)&dev_ev, sizeof(uint64_t) * RW * UW));
+        HIP_OK(hipMalloc((void **)&dbm, sizeof(uint64_t) * W * UW));
+        HIP_OK(hipMalloc((void **)&dst, UW));
+        HIP_OK(hipMalloc((void **)&dmj, 4 * UW));
+        HIP_OK(hipMemcpy(dev_ev, hev, sizeof(uint64_t) * RW * UW, hipMemcpyHostToDevice));
+        CHECK(c3_consensus(dev_ev, C3_EV_U64, 8, 8 * RW, RW, UW, C3_EXACT, C3_KAPPA_DEFAULT, dst,
+                           dbm, dmj, (c3_stream_t)s) == C3_OK);
+        {
+            const size_t lw = c3_localize_workspace_size(UW);
+            void *dlws;
+            c3_outlier_t o[8];
+            int64_t cw[3];
+            HIP_OK(hipMalloc(&dlws, lw));
+            CHECK(c3_localize(dst, dbm, dmj, NULL, RW, UW, outl, 8, und, 8, cnt, dlws, lw,
+                              (c3_stream_t)s) == C3_OK);
+            HIP_OK(hipStreamSynchronize(s));
+            HIP_OK(hipMemcpy(cw, cnt, sizeof(cw), hipMemcpyDeviceToHost));
+            HIP_OK(hipMemcpy(o, outl, sizeof(o), hipMemcpyDeviceToHost));
+            CHECK(cw[0] == 4 && cw[1] == 0 && cw[2] == 3);
+            CHECK(o[0].chunk == 10 && o[0].replica == 1 && o[0].majority_replica == 0);
+            CHECK(o[1].chunk == 10 && o[1].replica == 64);
+            CHECK(o[2].chunk == 500 && o[2].replica == 129);
+            CHECK(o[3].chunk == 777 && o[3].replica == 0 && o[3].majority_replica == 1);
+            HIP_OK(hipFree(dlws));
+        }
+        HIP_OK(hipMemcpy(hst, dst, UW, hipMemcpyDeviceToHost));
+        HIP_OK(hipMemcpy(hmj, dmj, 4 * UW, hipMemcpyDeviceToHost));
+        HIP_OK(hipMemcpy(hbm, dbm + (size_t)10 * W, sizeof(hbm), hipMemcpyDeviceToHost));
+        CHECK(hbm[0] == 2ull && hbm[1] == 1ull && hbm[2] == 0ull);
+        HIP_OK(hipMemcpy(hbm, dbm + (size_t)500 * W, sizeof(hbm), hipMemcpyDeviceToHost));
+        CHECK(hbm[0] == 0ull && hbm[1] == 0ull && hbm[2] == 2ull);
+        for (int u = 0; u < UW; ++u) {
+            const int bad = u == 10 || u == 500 || u == 777;
+            CHECK(hst[u] == (bad ? C3_ATTRIBUTED : C3_AGREE));
+            CHECK(hmj[u] == (u == 777 ? 1 : 0));
+        }
+        CHECK(c3_consensus(dev_ev, C3_EV_U64, 8, 8 * RW, C3_MAX_PEERS + 1, UW, C3_EXACT,
+                           C3_KAPPA_DEFAULT, dst, dbm, dmj, (c3_stream_t)s) == C3_E_INVAL);
+        HIP_OK(hipFree(dev_ev));
+        HIP_OK(hipFree(dbm));
+        HIP_OK(hipFree(dst));
+        HIP_OK(hipFree(dmj));
+        free(hev);
+    }
 
     /* argument errors return codes and launch nothing */
     {

@@ -7,6 +7,8 @@
   bytes changed in place between replays and the program's own eager work
   in between, must equal the eager result bit for bit.  The same holds for
   c3_timing_consensus (both of its execution paths).
+  A vote and localization over a 130-replica group are captured the same
+  way.
 * Streams.  Calls on different streams with disjoint outputs and
   workspaces may run concurrently: two signature + vote + localize passes
   over different replica sets, enqueued alternately on two streams, give
@@ -145,6 +147,65 @@ def test_graph_replays_timing_consensus(G, per_unit):
         if per_unit:
             want += [x.cpu().numpy() for x in r[1] + r[2]]
         _equal(got, want, ("timing replay", step))
+
+
+@pytest.mark.parametrize("mode", ["exact", "statistical"])
+def test_graph_replays_wide_group(mode):
+    """A 130-replica vote (three bitmap words per unit) and its localization
+    captured once; every replay, with the evidence changed in place, equals
+    the eager result."""
+    _case("graph wide", mode)
+    R, U = 130, 3000
+    rng = np.random.default_rng(130)
+    if mode == "exact":
+        ev = torch.from_numpy(np.repeat(rng.integers(-(2 ** 62), 2 ** 62, size=(U, 1)), R,
+                                        axis=1)).to(DEV)
+        m = c3.EXACT
+    else:
+        ev = torch.from_numpy(np.exp(rng.normal(0, 0.02, size=(U, R)))).to(DEV)
+        m = c3.STATISTICAL
+    W = c3.bitmap_words(R)
+    vote = (torch.empty(U, dtype=torch.uint8, device=DEV),
+            torch.empty((U, W), dtype=torch.int64, device=DEV),
+            torch.empty(U, dtype=torch.int32, device=DEV))
+    lists = (torch.zeros((U * 4, 80), dtype=torch.uint8, device=DEV),
+             torch.zeros(U, dtype=torch.int64, device=DEV),
+             torch.zeros(3, dtype=torch.int64, device=DEV))
+    lws = torch.empty(max(c3.localize_workspace_size(U), 256), dtype=torch.uint8, device=DEV)
+
+    def run(out_v, out_l, ws):
+        c3.consensus(ev, m, out=out_v)
+        c3.localize(*out_v, None, R=R, out_cap=U * 4, out=out_l, workspace=ws)
+
+    def snap(v, lo):
+        n_o, n_u = int(lo[2][0]), int(lo[2][1])
+        return [x.cpu().numpy().copy() for x in v] + [lo[0][:n_o].cpu().numpy().copy(),
+                                                      lo[1][:n_u].cpu().numpy().copy(),
+                                                      lo[2].cpu().numpy().copy()]
+
+    run(vote, lists, lws)
+    torch.cuda.synchronize()
+    s = torch.cuda.Stream()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        run(vote, lists, lws)
+    ref_v = tuple(torch.empty_like(x) for x in vote)
+    ref_l = tuple(torch.zeros_like(x) for x in lists)
+    ref_ws = torch.empty_like(lws)
+    for step in range(4):
+        # a different replica in a different word diverges at a few units
+        r = (37 * step + 60) % R
+        if mode == "exact":
+            ev[step::50, r] ^= 1 << step
+        else:
+            ev[step::50, r] *= 1.5
+        g.replay()
+        torch.cuda.synchronize()
+        got = snap(vote, lists)
+        run(ref_v, ref_l, ref_ws)
+        torch.cuda.synchronize()
+        _equal(got, snap(ref_v, ref_l), ("wide replay", mode, step))
+        assert int(lists[2][0]) > 0
 
 
 def test_two_streams_concurrently():
