@@ -196,17 +196,19 @@ __device__ __forceinline__ double quantile7_sorted(const V (&s)[N], int n, doubl
 
 // Everything after the first sort.  NC > 0 fixes the finite count at
 // compile time (every value finite and R == NMAX, the usual case), so every
-// order statistic is a plain register.
+// order statistic is a plain register and no replica needs a finiteness
+// test.
 template <int NMAX, int NC, typename V>
 __device__ __forceinline__ UnitVote statistical_tail(const V (&x)[NMAX], const V (&s)[NMAX],
                                                      uint64_t fin, uint64_t nonfin, int nf_rt,
                                                      double kappa) {
     const double inf = __builtin_huge_val();
     const int nf = NC > 0 ? NC : nf_rt;
+    auto finite = [&](int r) { return NC > 0 || ((fin >> r) & 1ull) != 0; };
     const double m = median_sorted<NMAX>(s, nf);
     double dev[NMAX];
 #pragma unroll
-    for (int r = 0; r < NMAX; ++r) dev[r] = ((fin >> r) & 1ull) ? fabs((double)x[r] - m) : inf;
+    for (int r = 0; r < NMAX; ++r) dev[r] = finite(r) ? fabs((double)x[r] - m) : inf;
     double d;
     if constexpr (NC > 0) {
         // m lies between the two middle sorted values, so the deviations of
@@ -246,17 +248,17 @@ __device__ __forceinline__ UnitVote statistical_tail(const V (&x)[NMAX], const V
         const double thr = kappa * d;
 #pragma unroll
         for (int r = 0; r < NMAX; ++r)
-            if (((fin >> r) & 1ull) && dev[r] > thr) B |= 1ull << r;
+            if (finite(r) && dev[r] > thr) B |= 1ull << r;
     }
     // lower-median replica: stable position (nf - 1) / 2 in (value, replica) order
     const V target = pick<NMAX>(s, (nf - 1) / 2);
     int want = (nf - 1) / 2;
 #pragma unroll
-    for (int r = 0; r < NMAX; ++r) want -= (((fin >> r) & 1ull) && x[r] < target) ? 1 : 0;
+    for (int r = 0; r < NMAX; ++r) want -= (finite(r) && x[r] < target) ? 1 : 0;
     int med = -1;
 #pragma unroll
     for (int r = 0; r < NMAX; ++r) {
-        if (((fin >> r) & 1ull) && x[r] == target) {
+        if (finite(r) && x[r] == target) {
             if (want == 0 && med < 0) med = r;
             --want;
         }
