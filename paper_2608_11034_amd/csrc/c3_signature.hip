@@ -240,10 +240,21 @@ __device__ inline LaneFold fold_lane(const uint8_t* tile, uint32_t len, uint32_t
             stats_fast<DT>(v[u], f.s, f.q, mf);
         }
     }
-    for (; k < nfull; k += 4) {
-        u32x4 v = load16_buf(rs, off, (uint32_t)k << 10);
-        nh16(v, K, block_beta(blk0 + (uint32_t)k), f.A, f.B);
-        stats_fast<DT>(v, f.s, f.q, mf);
+    if (k < nfull) {
+        // fewer than U blocks left for this wave: one more batch, all loads in
+        // flight together; the tests are wave-uniform (scalar branches).
+        u32x4 v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (k + 4 * u < nfull) v[u] = load16_buf(rs, off, (uint32_t)(k + 4 * u) << 10);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (k + 4 * u < nfull) {
+                nh16(v[u], K, block_beta(blk0 + (uint32_t)(k + 4 * u)), f.A, f.B);
+                stats_fast<DT>(v[u], f.s, f.q, mf);
+            }
+        }
     }
     const bool has_tail = tail != 0u && (nfull & 3) == wave && off < tail;
     if (has_tail) {
