@@ -177,6 +177,47 @@ def test_edge_shapes_every_record(dtype, chunk_bytes):
     compare_all_records(c3.records_numpy(rec), ref)
 
 
+@pytest.mark.parametrize("seed", range(8))
+def test_random_shapes_chunks_and_tiles(seed):
+    """Seeded random tensor counts, lengths and types, chunk sizes and tile
+    sizes: every record against the oracle.  Covers tiles whose blocks leave
+    a wave a partial batch, ragged tensor ends and multi-tile chunks in
+    combinations the fixed cases do not."""
+    rng = np.random.default_rng(1000 + seed)
+    chunk = int(1024 << rng.integers(0, 9))                # 1 KiB .. 256 KiB
+    tile = int(1024 << rng.integers(0, int(np.log2(chunk // 1024)) + 1))
+    dts = [torch.float32, torch.bfloat16, torch.float16, torch.uint8]
+    T = int(rng.integers(1, 7))
+    gen = torch.Generator(device=DEV)
+    gen.manual_seed(seed)
+    base = []
+    for _ in range(T):
+        dt = dts[int(rng.integers(0, 4))]
+        n = int(rng.integers(0, 300_000))
+        base.append(_special_tensor(dt, n, gen) if rng.random() < 0.3 else
+                    (torch.randint(0, 256, (n,), generator=gen, device=DEV, dtype=torch.uint8)
+                     if dt == torch.uint8 else torch.randn(n, generator=gen, device=DEV).to(dt)))
+    R = int(rng.integers(2, 6))
+    reps = [[t.clone() for t in base] for _ in range(R)]
+    for _ in range(3):                                     # a few byte faults
+        t = int(rng.integers(0, T))
+        if reps[0][t].numel():
+            r = int(rng.integers(0, R))
+            b = reps[r][t].view(torch.uint8)
+            b[int(rng.integers(0, b.numel()))] ^= int(rng.integers(1, 256))
+    _print_case("random shapes", seed, "chunk", chunk, "tile", tile, "T", T, "R", R,
+                [(str(t.dtype), t.numel()) for t in base])
+    plan = c3.SignaturePlan(reps, chunk, tile)
+    rec = plan.new_records()
+    plan.run(rec, plan.new_workspace())
+    torch.cuda.synchronize()
+    code = {torch.float32: workloads.F32, torch.bfloat16: workloads.BF16,
+            torch.float16: workloads.F16, torch.uint8: workloads.RAW}
+    metas = [(code[t.dtype], tuple(t.shape)) for t in base]
+    ref = oracle.signature([[workloads.host_bytes(t) for t in rep] for rep in reps], metas, chunk)
+    compare_all_records(c3.records_numpy(rec), ref)
+
+
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16, torch.float16])
 def test_absmax_finite_extremes_every_record(dtype):
     """Chunks without NaN or Inf (the kernel's unclassified path) whose largest
