@@ -199,22 +199,24 @@ __device__ inline void emit_units(const uint8_t* __restrict__ status,
 }
 
 // Small inputs: one workgroup of kSingleThreads walks the units in rounds of
-// kSingleThreads * kPerThread, carrying list offsets between rounds.  One
-// launch instead of three.  Each thread loads its units once (one-word
-// bitmaps stay in registers; wider ones are counted on load and read again
-// to emit); the three per-thread counts travel through a single scan packed
-// into one 64-bit word: outliers in the low 24 bits (a round holds at most
-// 1024 * 8 units * 256 replicas = 2^21), undecided and attributed units in
-// 20 bits each (at most 2^13 per round), so no field overflows.
+// kSingleThreads * kSinglePerThread, carrying list offsets between rounds.  One
+// launch instead of three.  Each thread loads its kSinglePerThread units
+// once (one-word bitmaps stay in registers; wider ones are counted on load
+// and read again to emit); the three per-thread counts travel through a
+// single scan packed into one 64-bit word: outliers in the low 24 bits (a
+// round holds at most 1024 * 4 units * 256 replicas = 2^20), undecided and
+// attributed units in 20 bits each (at most 2^12 per round), so no field
+// overflows.
 constexpr int kSingleThreads = 1024;
-constexpr int64_t kSingleMaxUnits = 4 * (int64_t)kSingleThreads * kPerThread;
+constexpr int kSinglePerThread = 4;  // 8 spilled registers at this block size
+constexpr int64_t kSingleMaxUnits = 8 * (int64_t)kSingleThreads * kSinglePerThread;
 constexpr int kOutBits = 24;
 constexpr int kUnitBits = 20;
 constexpr int64_t kOutMask = (1ll << kOutBits) - 1;
 constexpr int64_t kUnitMask = (1ll << kUnitBits) - 1;
-static_assert((int64_t)kSingleThreads * kPerThread * C3_MAX_PEERS <= kOutMask,
+static_assert((int64_t)kSingleThreads * kSinglePerThread * C3_MAX_PEERS <= kOutMask,
               "outlier field too narrow");
-static_assert((int64_t)kSingleThreads * kPerThread <= kUnitMask, "unit fields too narrow");
+static_assert((int64_t)kSingleThreads * kSinglePerThread <= kUnitMask, "unit fields too narrow");
 static_assert(kOutBits + 2 * kUnitBits <= 64, "fields exceed one word");
 
 template <bool WIDE>
@@ -225,12 +227,12 @@ __global__ void __launch_bounds__(kSingleThreads) localize_single_kernel(
     int64_t* __restrict__ undecided, int64_t und_cap, int64_t* __restrict__ counts) {
     __shared__ int64_t lds[kSingleThreads / 64];
     int64_t carry_o = 0, carry_u = 0, carry_a = 0;
-    for (int64_t base = 0; base < n_units; base += (int64_t)kSingleThreads * kPerThread) {
-        const int64_t u0 = base + (int64_t)threadIdx.x * kPerThread;
-        uint8_t st[kPerThread];
-        uint64_t bm[kPerThread];  // the word (one-word bitmaps) or the set-bit count
+    for (int64_t base = 0; base < n_units; base += (int64_t)kSingleThreads * kSinglePerThread) {
+        const int64_t u0 = base + (int64_t)threadIdx.x * kSinglePerThread;
+        uint8_t st[kSinglePerThread];
+        uint64_t bm[kSinglePerThread];  // the word (one-word bitmaps) or the set-bit count
 #pragma unroll
-        for (int i = 0; i < kPerThread; ++i) {
+        for (int i = 0; i < kSinglePerThread; ++i) {
             const int64_t u = u0 + i;
             st[i] = u < n_units ? status[u] : (uint8_t)C3_AGREE;
             if constexpr (WIDE)
@@ -240,7 +242,7 @@ __global__ void __launch_bounds__(kSingleThreads) localize_single_kernel(
         }
         int64_t o = 0, un = 0, at = 0;
 #pragma unroll
-        for (int i = 0; i < kPerThread; ++i) {
+        for (int i = 0; i < kSinglePerThread; ++i) {
             if (st[i] == C3_INCONCLUSIVE) {
                 ++un;
             } else if (bm[i]) {
@@ -254,7 +256,7 @@ __global__ void __launch_bounds__(kSingleThreads) localize_single_kernel(
         int64_t po = carry_o + (excl & kOutMask);
         int64_t pu = carry_u + ((excl >> kOutBits) & kUnitMask);
 #pragma unroll
-        for (int i = 0; i < kPerThread; ++i) {
+        for (int i = 0; i < kSinglePerThread; ++i) {
             const int64_t u = u0 + i;
             if (st[i] == C3_INCONCLUSIVE) {
                 if (pu < und_cap) undecided[pu] = u;
