@@ -20,6 +20,7 @@
 
 #include <type_traits>
 
+#include "../../include/c3.h"
 #include "c3_device.h"
 
 namespace c3 {
