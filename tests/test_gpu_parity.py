@@ -177,6 +177,27 @@ def test_edge_shapes_every_record(dtype, chunk_bytes):
     compare_all_records(c3.records_numpy(rec), ref)
 
 
+def test_largest_tile_and_long_lanes():
+    """The largest tile the ABI takes (16 MiB): each lane folds 64 KiB in one
+    fp64 run and a wave walks 4,096 blocks; 64 MiB chunks, ragged tensors,
+    one fault in the last block of a tile."""
+    _print_case("largest tile")
+    gen = torch.Generator(device=DEV)
+    gen.manual_seed(16)
+    base = [torch.randn(20 * (1 << 20) + 12345, generator=gen, device=DEV).to(torch.bfloat16),
+            torch.randn(3 * (1 << 20) + 7, generator=gen, device=DEV) * 1e3]
+    reps = [[t.clone() for t in base] for _ in range(3)]
+    reps[1][0].view(torch.uint8)[(16 << 20) - 3] ^= 0x40
+    plan = c3.SignaturePlan(reps, 64 << 20, 16 << 20)
+    rec = plan.new_records()
+    plan.run(rec, plan.new_workspace())
+    torch.cuda.synchronize()
+    metas = [(workloads.BF16, tuple(base[0].shape)), (workloads.F32, tuple(base[1].shape))]
+    ref = oracle.signature([[workloads.host_bytes(t) for t in rep] for rep in reps], metas, 64 << 20)
+    compare_all_records(c3.records_numpy(rec), ref)
+    assert (ref["sig"][1] != ref["sig"][0]).sum() == 1
+
+
 @pytest.mark.parametrize("seed", range(8))
 def test_random_shapes_chunks_and_tiles(seed):
     """Seeded random tensor counts, lengths and types, chunk sizes and tile
