@@ -19,10 +19,11 @@
 // than R / 2 replicas; those are the majority, the bitmap marks the others
 // and the majority index is the lowest majority replica.
 //
-// STATISTICAL (Sec. 5.4), in fp64: a value's stable rank among the finite
-// values (value, then replica index) gives every order statistic by one
-// ballot and one broadcast: the median, the median absolute deviation, the
-// type-7 quartiles and the range, in the fallback order MAD -> IQR / 2 ->
+// STATISTICAL (Sec. 5.4), in fp64: order statistics of the finite values in
+// the stable (value, then replica index) order -- from each value's rank in
+// the lane-per-replica kernel, from a sort across the wave in the wave
+// kernel -- give the median, the median absolute deviation, the type-7
+// quartiles and the range, in the fallback order MAD -> IQR / 2 ->
 // range / n_finite.  Non-finite values are outliers and take no part in m
 // or d.  No floating-point contraction is allowed in this file (the host
 // compiles it with -ffp-contract=off), so the decision rounds exactly as the
@@ -178,8 +179,8 @@ __global__ void __launch_bounds__(kVoteThreads) statistical_vote_small_kernel(
 // Wave per unit (EXACT above 16 replicas, STATISTICAL above 32).  Lane l
 // holds the values of replicas l, l + 64, l + 128 and l + 192 (NS =
 // ceil(R / 64) slots; slot s holds replica 64 s + l), so bitmap word s is the
-// ballot of slot s.  Every peer value reaches all lanes by readlane at a
-// wave-uniform index.
+// ballot of slot s.  The exact vote broadcasts candidate values by readlane
+// at a wave-uniform index; the statistical vote sorts the wave's keys.
 // ---------------------------------------------------------------------------
 constexpr int kWideUnitsPerBlock = kVoteThreads / 64;
 
@@ -279,63 +280,84 @@ __global__ void __launch_bounds__(kVoteThreads) exact_vote_wide_kernel(
     wide_write<NS>(u, any ? C3_ATTRIBUTED : C3_AGREE, ob, mj, status, bitmap, majority_idx);
 }
 
-// Stable rank of each slot's value among the finite values of the unit:
-// the number of finite peers j with y_j < x, or y_j == x and j before the
-// slot's replica.
-template <int NS>
-__device__ inline void wide_stable_rank(const double (&x)[NS], const uint64_t (&finb)[NS], int R,
-                                        int (&rank)[NS]) {
+// Bitonic sort of the wave's 64 * NP (value, replica) keys, ascending by
+// value, then replica: position p = 64 s + lane ends up holding the p-th
+// smallest key.  Keys are unique (the replica breaks ties), so the order is
+// the stable (value, replica) order.  Partners within a slot are 2^i lanes
+// apart (xor shuffles); partners 64 and more apart sit in the same lane.
+__device__ inline bool key_less(double av, int ai, double bv, int bi) {
+    return av < bv || (av == bv && ai < bi);
+}
+
+template <int NP>
+__device__ inline void wave_sort(double (&v)[NP], int (&id)[NP]) {
     const int lane = threadIdx.x & 63;
 #pragma unroll
-    for (int s = 0; s < NS; ++s) rank[s] = 0;
+    for (int k = 2; k <= 64 * NP; k <<= 1) {
 #pragma unroll
-    for (int sj = 0; sj < NS; ++sj) {
-        const int n = min(64, R - 64 * sj);
-        for (int l = 0; l < n; ++l) {
-            if (((finb[sj] >> l) & 1ull) == 0) continue;  // wave-uniform branch
-            const double y = readlane_f64(x[sj], l);
-            const int j = 64 * sj + l;
+        for (int j = k >> 1; j > 0; j >>= 1) {
+            if (j >= 64) {
 #pragma unroll
-            for (int s = 0; s < NS; ++s)
-                rank[s] += (y < x[s] || (y == x[s] && j < 64 * s + lane)) ? 1 : 0;
+                for (int s = 0; s < NP; ++s) {
+                    const int t = s ^ (j >> 6);
+                    if (t < s) continue;                 // each slot pair once
+                    const bool asc = ((64 * s) & k) == 0;
+                    const bool tl = key_less(v[t], id[t], v[s], id[s]);
+                    if (asc ? tl : !tl) {
+                        const double w = v[s];
+                        v[s] = v[t];
+                        v[t] = w;
+                        const int q = id[s];
+                        id[s] = id[t];
+                        id[t] = q;
+                    }
+                }
+            } else {
+#pragma unroll
+                for (int s = 0; s < NP; ++s) {
+                    const double ov = shfl_xor_f64(v[s], j);
+                    const int oi = (int)shfl_xor_u32((uint32_t)id[s], j);
+                    const bool lower = (lane & j) == 0;
+                    const bool asc = ((64 * s + lane) & k) == 0;
+                    const bool ol = key_less(ov, oi, v[s], id[s]);
+                    if (lower == asc ? ol : !ol) {
+                        v[s] = ov;
+                        id[s] = oi;
+                    }
+                }
+            }
         }
     }
 }
 
-// Order statistic k (0-based) of the finite values: the one value whose
-// stable rank is k.
-template <int NS>
-__device__ inline double wide_order_stat(const double (&x)[NS], const bool (&fin)[NS],
-                                         const int (&rank)[NS], int k) {
-    double v = 0.0;
+// The key at sorted position k (wave-uniform).
+template <int NP>
+__device__ inline double sorted_at(const double (&v)[NP], int k) {
+    double r = 0.0;
 #pragma unroll
-    for (int s = NS - 1; s >= 0; --s) {
-        const uint64_t b = ballot64(fin[s] && rank[s] == k);
-        if (b) v = readlane_f64(x[s], __builtin_ctzll(b));
-    }
-    return v;
+    for (int s = 0; s < NP; ++s)
+        if (s == (k >> 6)) r = readlane_f64(v[s], k & 63);
+    return r;
 }
 
-template <int NS>
-__device__ inline double wide_median(const double (&x)[NS], const bool (&fin)[NS],
-                                     const int (&rank)[NS], int nf) {
-    if (nf & 1) return wide_order_stat<NS>(x, fin, rank, (nf - 1) / 2);
-    const double a = wide_order_stat<NS>(x, fin, rank, nf / 2 - 1);
-    const double b = wide_order_stat<NS>(x, fin, rank, nf / 2);
+template <int NP>
+__device__ inline double sorted_median(const double (&v)[NP], int nf) {
+    if (nf & 1) return sorted_at<NP>(v, (nf - 1) / 2);
+    const double a = sorted_at<NP>(v, nf / 2 - 1);
+    const double b = sorted_at<NP>(v, nf / 2);
     return (a + b) * 0.5;
 }
 
 // Hyndman-Fan type 7, as quantile7 above.
-template <int NS>
-__device__ inline double wide_quantile7(const double (&x)[NS], const bool (&fin)[NS],
-                                        const int (&rank)[NS], int nf, double p) {
+template <int NP>
+__device__ inline double sorted_quantile7(const double (&v)[NP], int nf, double p) {
     const double h = (double)(nf - 1) * p;
     const double fl = floor(h);
     const int lo = (int)fl;
     const double frac = h - fl;
-    if (lo + 1 >= nf) return wide_order_stat<NS>(x, fin, rank, nf - 1);
-    const double a = wide_order_stat<NS>(x, fin, rank, lo);
-    const double b = wide_order_stat<NS>(x, fin, rank, lo + 1);
+    if (lo + 1 >= nf) return sorted_at<NP>(v, nf - 1);
+    const double a = sorted_at<NP>(v, lo);
+    const double b = sorted_at<NP>(v, lo + 1);
     const double diff = b - a;
     const double prod = frac * diff;
     return a + prod;
@@ -369,33 +391,53 @@ __global__ void __launch_bounds__(kVoteThreads) statistical_vote_wide_kernel(
         wide_write<NS>(u, C3_INCONCLUSIVE, B, -1, status, bitmap, majority_idx);
         return;
     }
-    int rank[NS], drank[NS];
-    wide_stable_rank<NS>(x, finb, R, rank);
-    const double m = wide_median<NS>(x, fin, rank, nf);
+    // sorted copies (NP slots: NS padded to a power of two); excluded values
+    // sort last as +inf
+    constexpr int NP = NS == 3 ? 4 : NS;
+    const double inf = __builtin_huge_val();
+    double sv[NP];
+    int si[NP];
+#pragma unroll
+    for (int s = 0; s < NP; ++s) {
+        sv[s] = s < NS && fin[s < NS ? s : 0] ? x[s < NS ? s : 0] : inf;
+        si[s] = 64 * s + lane;
+    }
+    wave_sort<NP>(sv, si);
+    const double m = sorted_median<NP>(sv, nf);
+    // lower-median replica: stable position (nf - 1) / 2
+    int mj = -1;
+    const int pm = (nf - 1) / 2;
+#pragma unroll
+    for (int s = 0; s < NP; ++s)
+        if (s == (pm >> 6)) mj = __builtin_amdgcn_readlane(si[s], pm & 63);
     double dev[NS];
 #pragma unroll
     for (int s = 0; s < NS; ++s) dev[s] = fin[s] ? fabs(x[s] - m) : 0.0;
-    wide_stable_rank<NS>(dev, finb, R, drank);
-    double d = wide_median<NS>(dev, fin, drank, nf);
+    double sd[NP];
+    int sdi[NP];
+#pragma unroll
+    for (int s = 0; s < NP; ++s) {
+        sd[s] = s < NS && fin[s < NS ? s : 0] ? dev[s < NS ? s : 0] : inf;
+        sdi[s] = 64 * s + lane;
+    }
+    wave_sort<NP>(sd, sdi);
+    double d = sorted_median<NP>(sd, nf);
     if (d == 0.0) {
-        const double q3 = wide_quantile7<NS>(x, fin, rank, nf, 0.75);
-        const double q1 = wide_quantile7<NS>(x, fin, rank, nf, 0.25);
+        const double q3 = sorted_quantile7<NP>(sv, nf, 0.75);
+        const double q1 = sorted_quantile7<NP>(sv, nf, 0.25);
         d = (q3 - q1) * 0.5;
     }
     if (d == 0.0) {
-        const double hi = wide_order_stat<NS>(x, fin, rank, nf - 1);
-        const double lo = wide_order_stat<NS>(x, fin, rank, 0);
+        const double hi = sorted_at<NP>(sv, nf - 1);
+        const double lo = sorted_at<NP>(sv, 0);
         d = (hi - lo) / (double)nf;
     }
     const double thr = kappa * d;
-    int mj = -1;
     bool any = false;
 #pragma unroll
-    for (int s = NS - 1; s >= 0; --s) {
+    for (int s = 0; s < NS; ++s) {
         const bool flag = d != 0.0 && fin[s] && dev[s] > thr;
         B[s] |= ballot64(flag);
-        const uint64_t medb = ballot64(fin[s] && rank[s] == (nf - 1) / 2);
-        if (medb) mj = 64 * s + __builtin_ctzll(medb);
         any = any || B[s] != 0;
     }
     wide_write<NS>(u, any ? C3_ATTRIBUTED : C3_AGREE, B, mj, status, bitmap, majority_idx);
