@@ -374,7 +374,9 @@ int c3_optimizer_check(const c3_optimizer_state_t *st, int64_t k, const c3_adamw
  *
  *   status [n_units] u8 (c3_verdict_t), bitmap [n_units][C3_BITMAP_WORDS(R)]
  *   u64 (8-byte aligned), majority_idx [n_units] i32 (-1 when Inconclusive);
- *   device.  R in 1..C3_MAX_PEERS (R = 1 gives Agree), n_units >= 0.
+ *   device.  R in 2..C3_MAX_PEERS, n_units >= 0.  R = 1 is C3_E_INVAL: a group
+ *   of one peer provides no comparison (Sec. 4), so no vote over it may
+ *   return Agree.
  */
 int c3_consensus(const void *evidence, int evidence_kind, int64_t replica_stride_bytes,
                  int64_t unit_stride_bytes, int R, int64_t n_units, int mode, double kappa,
@@ -389,7 +391,8 @@ size_t c3_localize_workspace_size(int64_t n_units);
  * i; Sec. 9: reports keep the peers and bitmaps).
  *
  *   status, bitmap, majority_idx  as c3_consensus writes them: bitmap is
- *              [n_units][C3_BITMAP_WORDS(R)] u64; R in 1..C3_MAX_PEERS.
+ *              [n_units][C3_BITMAP_WORDS(R)] u64; R in 2..C3_MAX_PEERS (R = 1:
+ *              C3_E_INVAL, as c3_consensus).
  *   outliers   device [out_cap]: one entry per set bitmap bit, ordered by
  *              (unit ascending, replica ascending).  With records (device
  *              [R][n_units], may be NULL) each entry carries the outlier's
@@ -419,6 +422,8 @@ size_t c3_timing_consensus_workspace_size(int R, int64_t G, int64_t T, int windo
  * protocol).  The results equal c3_consensus(fingerprints, EXACT) and
  * c3_consensus(times, STATISTICAL) per unit and c3_confirm on their bitmaps.
  *
+ *   R             ranks per group, 2..C3_MAX_REPLICAS (R = 1: C3_E_INVAL; a
+ *                 group of one rank provides no comparison, Sec. 4).
  *   fingerprints  device [T][G][R] u64, ranks innermost (8-byte aligned).
  *   times         device [T][G][R] fp32 (C3_EV_F32) or fp64 (C3_EV_F64).
  *   kappa         statistical threshold (> 0); window W >= 1 as c3_confirm.
@@ -456,6 +461,8 @@ size_t c3_confirm_workspace_size(int R, int64_t G, int64_t T);
  * straggler must recur across timing rounds before it is reported; Sec. 7:
  * a minority collective fingerprint is a protocol outlier).
  *
+ *   R         ranks per group, 2..C3_MAX_REPLICAS (R = 1: C3_E_INVAL, as
+ *             c3_consensus).
  *   fp_bitmap, time_bitmap  device [T][G] u64: the bitmaps c3_consensus
  *             produced for the fingerprint (EXACT) and timing (STATISTICAL)
  *             evidence of unit (t, g).

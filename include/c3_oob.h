@@ -168,7 +168,8 @@ typedef struct {
 } c3_hang_verdict_t;      /* 80 bytes */
 
 /* Exact C3 (Algorithm 1, Exact branch) over the R gathered records (peer i
- * = records[i], R in 1..64), evidence c3_progress_evidence: the most
+ * = records[i], R in 2..64; a single rank has no peer to compare with,
+ * Sec. 4), evidence c3_progress_evidence: the most
  * frequent record with 2 c* > R is the majority, the rest are outliers.
  * Their reasons compare coordinates with the majority record. */
 int c3_hang_classify(const c3_progress_t *records, int R, c3_hang_verdict_t *out);

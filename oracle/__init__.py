@@ -88,6 +88,11 @@ def _load():
     return _lib
 
 
+def _ok(rc):
+    if rc != 0:
+        raise ValueError(f"oracle call rejected its arguments ({rc})")
+
+
 def _p(a):
     return ctypes.c_void_p(a.ctypes.data) if a is not None and a.size else ctypes.c_void_p(0)
 
@@ -227,9 +232,14 @@ def bitmap_words(R: int) -> int:
     return (R + 63) // 64
 
 
+def _check_group(R: int):
+    # Sec. 4: a singleton group provides no comparison, so no vote over it
+    if not 2 <= R <= MAX_PEERS:
+        raise ValueError(f"R = {R} outside 2..{MAX_PEERS}")
+
+
 def _new_bitmap(U: int, R: int) -> np.ndarray:
-    if not 1 <= R <= MAX_PEERS:
-        raise ValueError(f"R = {R} outside 1..{MAX_PEERS}")
+    _check_group(R)
     return np.zeros(U, np.uint64) if R <= 64 else np.zeros((U, bitmap_words(R)), np.uint64)
 
 
@@ -256,7 +266,7 @@ def vote_exact(ev: np.ndarray, replica_axis: int = 0):
     st = np.zeros(U, np.uint8)
     bm = _new_bitmap(U, R)
     mj = np.zeros(U, np.int32)
-    _load().c3o_vote_exact(_p(ev), _ev_kind(ev), rs, us, R, U, _p(st), _p(bm), _p(mj))
+    _ok(_load().c3o_vote_exact(_p(ev), _ev_kind(ev), rs, us, R, U, _p(st), _p(bm), _p(mj)))
     return st, bm, mj
 
 
@@ -269,7 +279,7 @@ def vote_bytes(chunks):
     st = np.zeros(U, np.uint8)
     bm = _new_bitmap(U, R)
     mj = np.zeros(U, np.int32)
-    _load().c3o_vote_bytes(ptrs, _p(lens), R, U, _p(st), _p(bm), _p(mj))
+    _ok(_load().c3o_vote_bytes(ptrs, _p(lens), R, U, _p(st), _p(bm), _p(mj)))
     return st, bm, mj
 
 
@@ -285,16 +295,15 @@ def vote_statistical(ev: np.ndarray, kappa: float = KAPPA_DEFAULT, replica_axis:
     st = np.zeros(U, np.uint8)
     bm = _new_bitmap(U, R)
     mj = np.zeros(U, np.int32)
-    _load().c3o_vote_statistical(_p(ev), _ev_kind(ev), rs, us, R, U, ctypes.c_double(kappa),
-                                 _p(st), _p(bm), _p(mj))
+    _ok(_load().c3o_vote_statistical(_p(ev), _ev_kind(ev), rs, us, R, U, ctypes.c_double(kappa),
+                                     _p(st), _p(bm), _p(mj)))
     return st, bm, mj
 
 
 def localize(status, bitmap, majority_idx, R: int, out_cap=None, und_cap=None):
     """Outlier (unit, replica, majority replica) list and undecided units.
     bitmap: [U] (R <= 64) or [U, ceil(R / 64)] uint64."""
-    if not 1 <= R <= MAX_PEERS:
-        raise ValueError(f"R = {R} outside 1..{MAX_PEERS}")
+    _check_group(R)
     status = np.ascontiguousarray(status, np.uint8)
     U = status.size
     bitmap = np.ascontiguousarray(bitmap, np.uint64).reshape(U * bitmap_words(R))
@@ -308,8 +317,8 @@ def localize(status, bitmap, majority_idx, R: int, out_cap=None, und_cap=None):
     om = np.zeros(max(out_cap, 1), np.int32)
     und = np.zeros(max(und_cap, 1), np.int64)
     counts = np.zeros(3, np.int64)
-    _load().c3o_localize(_p(status), _p(bitmap), _p(majority_idx), R, U, _p(ou), _p(orr), _p(om),
-                         out_cap, _p(und), und_cap, _p(counts))
+    _ok(_load().c3o_localize(_p(status), _p(bitmap), _p(majority_idx), R, U, _p(ou), _p(orr), _p(om),
+                             out_cap, _p(und), und_cap, _p(counts)))
     n_o = min(int(counts[0]), out_cap)
     n_u = min(int(counts[1]), und_cap)
     return dict(unit=ou[:n_o], replica=orr[:n_o], majority=om[:n_o], undecided=und[:n_u],
@@ -318,6 +327,8 @@ def localize(status, bitmap, majority_idx, R: int, out_cap=None, und_cap=None):
 
 def confirm(fp_bitmap, time_bitmap, R: int, W: int = 16):
     """Per-rank temporal confirmation; bitmaps are [T, G] uint64; rank = r*G + g."""
+    if not 2 <= R <= 64:
+        raise ValueError(f"R = {R} outside 2..64")
     fp_bitmap = np.ascontiguousarray(fp_bitmap, np.uint64)
     time_bitmap = np.ascontiguousarray(time_bitmap, np.uint64)
     T, G = fp_bitmap.shape
@@ -325,7 +336,7 @@ def confirm(fp_bitmap, time_bitmap, R: int, W: int = 16):
     out = dict(flags=np.zeros(n, np.uint32), first_div=np.zeros(n, np.int32),
                div_count=np.zeros(n, np.uint32), slow_count=np.zeros(n, np.uint32),
                max_window=np.zeros(n, np.uint32), first_window=np.zeros(n, np.int32))
-    _load().c3o_confirm(_p(fp_bitmap), _p(time_bitmap), R, G, T, W,
-                        _p(out["flags"]), _p(out["first_div"]), _p(out["div_count"]),
-                        _p(out["slow_count"]), _p(out["max_window"]), _p(out["first_window"]))
+    _ok(_load().c3o_confirm(_p(fp_bitmap), _p(time_bitmap), R, G, T, W,
+                            _p(out["flags"]), _p(out["first_div"]), _p(out["div_count"]),
+                            _p(out["slow_count"]), _p(out["max_window"]), _p(out["first_window"])))
     return out

@@ -26,7 +26,9 @@
  *   - Sec. 5.4: statistical consensus (median, MAD -> IQR -> scaled range,
  *     kappa multiplier).
  *   - Sec. 4 (peer-group size): a two-member disagreement is group-scoped,
- *     i.e. no strict majority, i.e. Inconclusive.
+ *     i.e. no strict majority, i.e. Inconclusive; a group of one peer has
+ *     nothing to compare with, so every vote, localization and confirmation
+ *     below rejects R = 1 (returns -1) instead of certifying agreement.
  *   - Sec. 10 (protocol): stragglers are confirmed over repeated rounds.
  *
  * Parity status per function:
@@ -425,7 +427,7 @@ int c3o_vote_exact(const uint8_t *evidence, int kind, int64_t replica_stride,
 {
     int64_t u;
     const int W = bm_words(R);
-    if (R < 1 || R > O_MAX_R) return -1;
+    if (R < 2 || R > O_MAX_R) return -1;   /* a singleton compares nothing */
     for (u = 0; u < n_units; u++) {
         uint64_t e[O_MAX_R];
         uint64_t *B = bitmap + u * W;
@@ -465,7 +467,7 @@ int c3o_vote_bytes(const uint8_t *const *chunk_ptrs, const uint64_t *chunk_len,
 {
     int64_t u;
     const int W = bm_words(R);
-    if (R < 1 || R > O_MAX_R) return -1;
+    if (R < 2 || R > O_MAX_R) return -1;   /* a singleton compares nothing */
     for (u = 0; u < n_units; u++) {
         uint64_t *B = bitmap + u * W;
         int cnt[O_MAX_R], r, j, best = 0, arg = -1;
@@ -535,7 +537,7 @@ int c3o_vote_statistical(const uint8_t *evidence, int kind, int64_t replica_stri
 {
     int64_t u;
     const int W = bm_words(R);
-    if (R < 1 || R > O_MAX_R) return -1;
+    if (R < 2 || R > O_MAX_R) return -1;   /* a singleton compares nothing */
     for (u = 0; u < n_units; u++) {
         double tau[O_MAX_R], s[O_MAX_R], dev[O_MAX_R], devs[O_MAX_R], m, d, thr;
         int fin[O_MAX_R], r, nf = 0, k, lowmed;
@@ -610,7 +612,7 @@ int c3o_localize(const uint8_t *status,
     int64_t u, no = 0, nu = 0, na = 0;
     int r;
     const int W = bm_words(R);
-    if (R < 1 || R > O_MAX_R) return -1;
+    if (R < 2 || R > O_MAX_R) return -1;   /* a singleton compares nothing */
     for (u = 0; u < n_units; u++) {
         const uint64_t *B = bitmap + u * W;
         if (status[u] == O_INCONCLUSIVE) {
@@ -656,6 +658,7 @@ int c3o_confirm(const uint64_t *fp_bitmap /* [T][G] */, const uint64_t *time_bit
     int64_t g, t;
     int r;
     int64_t Wt = (int64_t)W < T ? (int64_t)W : T;
+    if (R < 2 || R > 64 || W < 1) return -1;   /* one-word bitmaps; no singleton */
     for (r = 0; r < R; r++) {
         for (g = 0; g < G; g++) {
             int64_t rank = (int64_t)r * G + g;

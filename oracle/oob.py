@@ -49,6 +49,8 @@ def classify(records):
     """records: list of dicts with step, op_id, fingerprint, flags.
     Returns (class, majority_idx, outliers, reasons)."""
     R = len(records)
+    if R < 2:
+        raise ValueError("a single rank has no peer to compare with (Sec. 4)")
     key = [(r["step"], r["op_id"], r["fingerprint"], r["flags"] & PENDING) for r in records]
     counts = [sum(1 for k in key if k == key[i]) for i in range(R)]
     best = max(range(R), key=lambda i: (counts[i], -i))

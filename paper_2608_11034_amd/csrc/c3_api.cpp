@@ -408,7 +408,9 @@ int c3_adamw_slice(const float* const* param, const float* const* grad, const fl
 int c3_consensus(const void* evidence, int evidence_kind, int64_t replica_stride_bytes,
                  int64_t unit_stride_bytes, int R, int64_t n_units, int mode, double kappa,
                  uint8_t* status, uint64_t* bitmap, int32_t* majority_idx, c3_stream_t stream) {
-    if (R < 1 || R > C3_MAX_PEERS || n_units < 0) return C3_E_INVAL;
+    // Sec. 4: a group of one peer provides no comparison, so a vote over it
+    // is an argument error, not an Agree that could certify anything
+    if (R < 2 || R > C3_MAX_PEERS || n_units < 0) return C3_E_INVAL;
     if (mode != C3_EXACT && mode != C3_STATISTICAL) return C3_E_INVAL;
     int vsize;
     switch (evidence_kind) {
@@ -441,7 +443,7 @@ int c3_localize(const uint8_t* status, const uint64_t* bitmap, const int32_t* ma
                 const c3_chunk_record_t* records, int R, int64_t n_units, c3_outlier_t* outliers,
                 int64_t out_cap, int64_t* undecided, int64_t und_cap, int64_t* counts, void* ws,
                 size_t ws_bytes, c3_stream_t stream) {
-    if (R < 1 || R > C3_MAX_PEERS || n_units < 0 || out_cap < 0 || und_cap < 0)
+    if (R < 2 || R > C3_MAX_PEERS || n_units < 0 || out_cap < 0 || und_cap < 0)
         return C3_E_INVAL;
     if (counts == nullptr) return C3_E_INVAL;
     if (n_units > 0 && (status == nullptr || bitmap == nullptr || majority_idx == nullptr))
@@ -594,7 +596,7 @@ static uint64_t timing_fallback_bytes(int R, int64_t G, int64_t T) {
 }
 
 size_t c3_timing_consensus_workspace_size(int R, int64_t G, int64_t T, int window) {
-    if (R < 1 || R > C3_MAX_REPLICAS || G < 0 || T < 0 || window < 1) return 0;
+    if (R < 2 || R > C3_MAX_REPLICAS || G < 0 || T < 0 || window < 1) return 0;
     if (T > 0x7FFFFFFF || G > ((int64_t)1 << 40) / (T > 0 ? T : 1)) return 0;
     const uint64_t b = timing_fused(R, window) ? (uint64_t)c3::timing_masks_bytes(R, G, T)
                                                : timing_fallback_bytes(R, G, T);
@@ -606,7 +608,7 @@ int c3_timing_consensus(const uint64_t* fingerprints, const void* times, int tim
                         uint64_t* fp_bitmap, int32_t* fp_majority, uint8_t* t_status,
                         uint64_t* t_bitmap, int32_t* t_majority, c3_rank_verdict_t* verdicts,
                         void* ws, size_t ws_bytes, c3_stream_t stream) {
-    if (R < 1 || R > C3_MAX_REPLICAS || G < 0 || T < 0 || window < 1) return C3_E_INVAL;
+    if (R < 2 || R > C3_MAX_REPLICAS || G < 0 || T < 0 || window < 1) return C3_E_INVAL;
     if (time_kind != C3_EV_F32 && time_kind != C3_EV_F64) return C3_E_INVAL;
     if (!(kappa > 0.0) || kappa > 1e300) return C3_E_INVAL;
     if (T > 0x7FFFFFFF || (int64_t)R * G > 0x7FFFFFFF) return C3_E_INVAL;
@@ -668,14 +670,14 @@ int c3_timing_consensus(const uint64_t* fingerprints, const void* times, int tim
 }
 
 size_t c3_confirm_workspace_size(int R, int64_t G, int64_t T) {
-    if (R < 1 || R > C3_MAX_REPLICAS || G < 0 || T < 0) return 0;
+    if (R < 2 || R > C3_MAX_REPLICAS || G < 0 || T < 0) return 0;
     return c3::confirm_ws_bytes(R, G, T);
 }
 
 int c3_confirm(const uint64_t* fp_bitmap, const uint64_t* time_bitmap, int R, int64_t G,
                int64_t T, int window, c3_rank_verdict_t* verdicts, void* ws, size_t ws_bytes,
                c3_stream_t stream) {
-    if (R < 1 || R > C3_MAX_REPLICAS || G < 0 || T < 0 || window < 1) return C3_E_INVAL;
+    if (R < 2 || R > C3_MAX_REPLICAS || G < 0 || T < 0 || window < 1) return C3_E_INVAL;
     if (T > 0x7FFFFFFF || (int64_t)R * G > 0x7FFFFFFF) return C3_E_INVAL;
     if ((int64_t)R * G == 0) return C3_OK;
     if (verdicts == nullptr || (T > 0 && (fp_bitmap == nullptr || time_bitmap == nullptr)))

@@ -290,7 +290,8 @@ uint64_t c3_progress_evidence(const c3_progress_t* p) {
 }
 
 int c3_hang_classify(const c3_progress_t* records, int R, c3_hang_verdict_t* out) {
-    if (records == nullptr || out == nullptr || R < 1 || R > C3_OOB_MAX_RANKS)
+    // a single rank has no peer to be compared with (Sec. 4)
+    if (records == nullptr || out == nullptr || R < 2 || R > C3_OOB_MAX_RANKS)
         return C3_OOB_E_INVAL;
     memset(out, 0, sizeof(*out));
     uint64_t e[C3_OOB_MAX_RANKS];

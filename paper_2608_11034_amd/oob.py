@@ -179,8 +179,8 @@ def _records_array(records):
 def classify(records) -> dict:
     """Exact C3 over gathered progress records (Progress or dicts)."""
     R = len(records)
-    if not 1 <= R <= MAX_RANKS:
-        raise OOBError("1..64 records")
+    if not 2 <= R <= MAX_RANKS:
+        raise OOBError("2..64 records (a single rank has no peer to compare with)")
     v = HangVerdict()
     _check(lib().c3_hang_classify(_records_array(records), R, ctypes.byref(v)), "c3_hang_classify")
     return {"class": CLASS_NAMES[v.cls], "cls": int(v.cls), "majority_idx": int(v.majority_idx),

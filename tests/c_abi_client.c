@@ -212,6 +212,10 @@ int main(void) {
               C3_E_INVAL);
         CHECK(c3_signature(ptrs, &meta, 1, R, 1000, rec, ws, ws_bytes, (c3_stream_t)s) ==
               C3_E_INVAL);
+        /* a group of one replica provides no comparison (Sec. 4): no vote */
+        CHECK(c3_consensus(&rec[0].sig, C3_EV_U64, C * (int64_t)sizeof(c3_chunk_record_t),
+                           (int64_t)sizeof(c3_chunk_record_t), 1, C, C3_EXACT,
+                           C3_KAPPA_DEFAULT, st, bm, mj, (c3_stream_t)s) == C3_E_INVAL);
         CHECK(c3_signature(ptrs, &meta, 1, R, CHUNK, rec, ws, 16, (c3_stream_t)s) ==
               C3_E_WORKSPACE);
     }

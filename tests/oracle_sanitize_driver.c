@@ -157,7 +157,7 @@ static void signature_cases(void) {
 
 static void vote_cases(void) {
     int R;
-    for (R = 1; R <= 64; R++) {
+    for (R = 2; R <= 64; R++) {
         const int64_t U = 97;
         uint64_t *ev = (uint64_t *)xmalloc(8 * (size_t)(U * R));
         uint32_t *ev32 = (uint32_t *)xmalloc(4 * (size_t)(U * R));
@@ -184,6 +184,8 @@ static void vote_cases(void) {
             }
             cl[u] = 8;
         }
+        /* a singleton group is refused before anything is read (Sec. 4) */
+        CHECK(c3o_vote_exact((const uint8_t *)ev, 0, 8, 8 * R, 1, U, st, bm, mj) == -1);
         CHECK(c3o_vote_exact((const uint8_t *)ev, 0, 8, 8 * R, R, U, st, bm, mj) == 0);
         CHECK(c3o_vote_exact((const uint8_t *)ev32, 1, 4, 4 * R, R, U, st, bm, mj) == 0);
         CHECK(c3o_vote_bytes((const uint8_t *const *)cp, cl, R, U, st, bm, mj) == 0);

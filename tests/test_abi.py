@@ -129,6 +129,28 @@ def test_argument_errors_return_before_gpu_work():
         assert isinstance(L.c3_status_string(code), bytes)
 
 
+def test_singleton_group_is_rejected_before_gpu_work():
+    """Sec. 4: one peer provides no comparison.  Every vote, localization
+    and confirmation entry point returns C3_E_INVAL for R = 1 (checked before
+    any HIP call), while signing one replica stays valid (records are per
+    replica; the tests of the emulated sharded protocol sign R = 1)."""
+    L = c3.lib()
+    null = ctypes.c_void_p(0)
+    p8 = ctypes.c_void_p(8)
+    for kind, mode in ((c3.EV_U64, c3.EXACT), (c3.EV_F32, c3.STATISTICAL)):
+        assert L.c3_consensus(p8, kind, 8, 8, 1, 10, mode, 1.0, p8, p8, p8, null) == -1
+        assert L.c3_consensus(p8, kind, 8, 8, 1, 0, mode, 1.0, null, null, null, null) == -1
+    assert L.c3_localize(p8, p8, p8, null, 1, 10, p8, 10, p8, 10, p8, ctypes.c_void_p(256),
+                         1 << 20, null) == -1
+    assert L.c3_confirm(p8, p8, 1, 4, 16, 16, p8, ctypes.c_void_p(256), 1 << 20, null) == -1
+    assert L.c3_confirm_workspace_size(1, 4, 16) == 0
+    assert L.c3_timing_consensus_workspace_size(1, 4, 16, 16) == 0
+    assert L.c3_timing_consensus(p8, p8, c3.EV_F32, 1, 4, 16, 1.0, 16, null, null, null, null,
+                                 null, null, p8, ctypes.c_void_p(256), 1 << 20, null) == -1
+    md = _metas([(c3.F32, (1000,))])
+    assert L.c3_signature_workspace_size(md, 1, 1, 1024) > 0
+
+
 def test_binding_has_no_cpu_fallback():
     import torch
     x = torch.zeros(1024)

@@ -410,7 +410,33 @@ def test_grid_size_and_tile_size_invariance():
 # ---------------------------------------------------------------------------
 # consensus, localize and confirm on synthetic evidence
 # ---------------------------------------------------------------------------
-@pytest.mark.parametrize("R", [1, 2, 3, 4, 5, 7, 8, 9, 16, 31, 33, 64])
+def test_singleton_group_vote_is_an_error():
+    """Sec. 4: one replica provides no comparison.  Through the C ABI on the
+    GPU, votes, localization, confirmation and the timing path return
+    C3_E_INVAL for R = 1 and write nothing; signing one replica is valid."""
+    _print_case("singleton group")
+    ev = torch.arange(10, dtype=torch.int64, device=DEV).reshape(10, 1)
+    st = torch.full((10,), 0xAB, dtype=torch.uint8, device=DEV)
+    bm = torch.zeros(10, dtype=torch.int64, device=DEV)
+    mj = torch.zeros(10, dtype=torch.int32, device=DEV)
+    for mode, x in ((c3.EXACT, ev), (c3.STATISTICAL, ev.float())):
+        with pytest.raises(c3.C3Error, match=r"\(-1\)"):
+            c3.consensus(x, mode, out=(st, bm, mj))
+    with pytest.raises(c3.C3Error, match=r"\(-1\)"):
+        c3.localize(st, bm, mj, None, R=1)
+    with pytest.raises(c3.C3Error):
+        c3.confirm(bm.reshape(10, 1), bm.reshape(10, 1), 1)
+    fp = torch.zeros((4, 3, 1), dtype=torch.int64, device=DEV)
+    with pytest.raises(c3.C3Error):
+        c3.timing_consensus(fp, fp.float())
+    torch.cuda.synchronize()
+    assert (st == 0xAB).all().item()
+    x = torch.randn(5000, device=DEV)
+    rec = c3.signature([[x]], 4096)
+    assert rec.shape[:2] == (1, 5)
+
+
+@pytest.mark.parametrize("R", [2, 3, 4, 5, 7, 8, 9, 16, 31, 33, 64])
 def test_exact_consensus_matches_oracle(R):
     _print_case("exact consensus", R)
     rng = np.random.default_rng(R)

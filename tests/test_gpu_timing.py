@@ -92,7 +92,7 @@ def _check(fp, tau, W, per_unit=True):
 CASES = [
     # R, G, T, W, f64
     (8, 64, 16, 16, False), (8, 65, 17, 16, False), (8, 130, 100, 16, True),
-    (3, 63, 40, 5, False), (4, 1, 1, 16, False), (1, 7, 33, 3, False), (2, 70, 31, 1, True),
+    (3, 63, 40, 5, False), (4, 1, 1, 16, False), (2, 7, 33, 3, False), (2, 70, 31, 1, True),
     (5, 64, 64, 64, False), (7, 66, 90, 64, True), (8, 20, 129, 63, False),
     (9, 64, 16, 16, False), (13, 33, 41, 16, True), (16, 64, 24, 8, False), (16, 3, 9, 64, False),
     (4, 66, 300, 1, False), (6, 9, 700, 2, True),   # several lanes per rank, short windows

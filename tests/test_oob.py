@@ -14,6 +14,7 @@
   Gloo group detect the silence, exchange records and must all reach the
   expected verdict.
 """
+import ctypes
 import itertools
 import multiprocessing as mp
 import os
@@ -204,7 +205,7 @@ def _labels_records(labels, rng):
     return out
 
 
-@pytest.mark.parametrize("R", [1, 2, 3, 4, 5, 6])
+@pytest.mark.parametrize("R", [2, 3, 4, 5, 6])
 def test_classify_matches_the_tuple_majority_definition(R):
     rng = random.Random(R)
     n = 0
@@ -224,6 +225,18 @@ def test_classify_matches_the_tuple_majority_definition(R):
         assert int(bm[0]) == v["bitmap"]
         assert {0: "group_stall", 1: "rank_divergence", 2: "inconclusive"}[int(st[0])] == v["class"]
     assert n > 0
+
+
+def test_single_rank_is_rejected():
+    """Sec. 4: a single rank has no peer to be compared with; the library, its
+    binding and the oracle all refuse to classify it."""
+    rec = [dict(step=3, op_id=1, fingerprint=0, flags=0)]
+    with pytest.raises(oob.OOBError):
+        oob.classify(rec)
+    with pytest.raises(ValueError):
+        ooob.classify(rec)
+    v = oob.HangVerdict()
+    assert oob.lib().c3_hang_classify(oob._records_array(rec), 1, ctypes.byref(v)) == -1
 
 
 def _parse_cases():

@@ -6,6 +6,7 @@ library routines, brute force over tiny inputs, and the byte-equality
 definition of the exact result.
 """
 import collections
+import ctypes
 import itertools
 import math
 import os
@@ -279,12 +280,16 @@ def test_exact_vote_paper_cases():
         labels = labels.split()
         code = {v: i + 100 for i, v in enumerate(sorted(set(labels)))}
         ev = np.array([[code[v] for v in labels]], np.uint64)
+        if status == "REJECTED":
+            with pytest.raises(ValueError):
+                oracle.vote_exact(ev, replica_axis=1)
+            continue
         st, bm, mj = oracle.vote_exact(ev, replica_axis=1)
         want_bits = 0 if bits == "-" else sum(1 << int(b) for b in bits.split())
         assert (int(st[0]), int(bm[0]), int(mj[0])) == (STATUS[status], want_bits, int(maj)), ln
 
 
-@pytest.mark.parametrize("R", [1, 2, 3, 4, 5, 6, 7])
+@pytest.mark.parametrize("R", [2, 3, 4, 5, 6, 7])
 def test_exact_vote_brute_force_all_label_vectors(R):
     ev = np.array(list(itertools.product(range(R), repeat=R)), dtype=np.uint64).reshape(-1, R)
     st, bm, mj = oracle.vote_exact(ev, replica_axis=1)
@@ -302,6 +307,39 @@ def test_exact_vote_brute_force_all_label_vectors(R):
     assert np.array_equal(mj, np.where(has, first, -1).astype(np.int32))
 
 
+def test_singleton_group_is_rejected():
+    """Sec. 4: a group of one peer provides no comparison.  The C functions
+    themselves return -1 (not only the Python wrappers), for every vote,
+    localization and confirmation."""
+    L = oracle._load()
+    ev = np.array([7, 8, 9], np.uint64)
+    f = np.array([1.0, 2.0, 3.0])
+    st, bm, mj = np.zeros(3, np.uint8), np.zeros(3, np.uint64), np.zeros(3, np.int32)
+    P = oracle._p
+    assert L.c3o_vote_exact(P(ev), oracle.EV_U64, 8, 8, 1, 3, P(st), P(bm), P(mj)) == -1
+    assert L.c3o_vote_statistical(P(f), oracle.EV_F64, 8, 8, 1, 3, ctypes.c_double(5.0),
+                                  P(st), P(bm), P(mj)) == -1
+    chunks = (ctypes.c_void_p * 3)(*[ev.ctypes.data + 8 * i for i in range(3)])
+    lens = np.full(3, 8, np.uint64)
+    assert L.c3o_vote_bytes(chunks, P(lens), 1, 3, P(st), P(bm), P(mj)) == -1
+    ou, orr, om, und, cnt = (np.zeros(3, np.int64), np.zeros(3, np.int32), np.zeros(3, np.int32),
+                             np.zeros(3, np.int64), np.zeros(3, np.int64))
+    assert L.c3o_localize(P(st), P(bm), P(mj), 1, 3, P(ou), P(orr), P(om), 3, P(und), 3,
+                          P(cnt)) == -1
+    out = [np.zeros(3, np.uint32), np.zeros(3, np.int32), np.zeros(3, np.uint32),
+           np.zeros(3, np.uint32), np.zeros(3, np.uint32), np.zeros(3, np.int32)]
+    assert L.c3o_confirm(P(bm), P(bm), 1, 3, 1, 16, *[P(a) for a in out]) == -1
+    for call in (lambda: oracle.vote_exact(ev.reshape(1, 3)),
+                 lambda: oracle.vote_statistical(f.reshape(1, 3)),
+                 lambda: oracle.localize(st, bm, mj, 1),
+                 lambda: oracle.confirm(bm.reshape(3, 1), bm.reshape(3, 1), 1)):
+        with pytest.raises(ValueError):
+            call()
+    # two peers are a group (Sec. 4): agreement certifies, disagreement is inconclusive
+    st2, bm2, mj2 = oracle.vote_exact(np.array([[5, 5], [5, 6]], np.uint64), replica_axis=1)
+    assert st2.tolist() == [oracle.AGREE, oracle.INCONCLUSIVE]
+
+
 def _mjrty(vals):
     # Boyer & Moore, "MJRTY - a fast majority vote algorithm" (1991)
     cand, k = None, 0
@@ -317,7 +355,7 @@ def _mjrty(vals):
 
 def test_exact_vote_agrees_with_mjrty():
     rng = np.random.default_rng(13)
-    for R in range(1, 65, 3):
+    for R in range(2, 65, 3):
         ev = rng.integers(0, 3, size=(400, R)).astype(np.uint64)
         ev[::3] = 1
         st, bm, mj = oracle.vote_exact(ev, replica_axis=1)
@@ -670,8 +708,9 @@ def test_confirm_needs_more_than_half_of_a_window():
     for flagged, want in ((8, 0), (9, 1)):
         tmb = np.zeros((T, 1), np.uint64)
         tmb[:flagged, 0] = 1
-        out = oracle.confirm(np.zeros((T, 1), np.uint64), tmb, 1, W)
+        out = oracle.confirm(np.zeros((T, 1), np.uint64), tmb, 2, W)
         assert int(out["flags"][0] & 1) == want and out["max_window"][0] == flagged
+        assert out["flags"][1] == 0 and out["max_window"][1] == 0   # replica 1 never flagged
 
 
 def test_empty_tensor_is_one_empty_chunk():
