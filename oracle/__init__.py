@@ -31,8 +31,9 @@ functions return bitmaps of shape [U] for R <= 64 and [U, ceil(R / 64)] above.
                        rotating slice and the check built on it (module
                        ``oracle.adamw``).
 
-Parity: the hash bits of C3SIG-1 are not fixed by the paper ("parity
-unpinned" for the exact bit pattern); they are pinned indirectly (see the
+Parity: the paper fixes no hash construction, so the bits of C3SIG-1 are
+this implementation's definition.  They are pinned by a restatement of that
+definition in Python integers and by frozen known-answer vectors (see the
 header of ``c3_oracle.c``).
 """
 import ctypes

@@ -36,14 +36,17 @@
  *   c3o_fmix64              pinned (bijectivity via an independently derived
  *                           inverse; avalanche); exact constants are the
  *                           published MurmurHash3 ones
- *   c3o_chunk_signature     hash bits: parity unpinned by the paper (the paper
- *                           fixes no construction).  Pinned indirectly:
- *                           byte-equality vote == signature vote, exhaustive
- *                           single-bit-flip detection, big-integer
- *                           recomputation on tiny inputs.
+ *   c3o_chunk_signature     hash bits: the paper fixes no construction, so the
+ *                           bits are C3SIG-1's definition.  Pinned by a
+ *                           restatement of that definition in Python integers
+ *                           (keys, NH fold and the whole fmix64 chain) and by
+ *                           frozen known-answer vectors; indirectly also by
+ *                           byte-equality vote == signature vote and
+ *                           exhaustive single-bit-flip detection.
  *                           stats: pinned against numpy / math.fsum.
- *   c3o_tensor_signature    pinned indirectly: its vote equals the byte-equality
- *                           vote over whole tensors
+ *   c3o_tensor_signature    pinned by the same restatement and vectors; its
+ *                           vote equals the byte-equality vote over whole
+ *                           tensors
  *   c3o_vote_exact          pinned (brute force over all label vectors, paper
  *                           cases, Boyer-Moore MJRTY; groups of 65-256 by
  *                           rows whose vote is fixed by construction)

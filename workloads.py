@@ -361,3 +361,16 @@ def make(k: int, device="cuda", scale="full"):
 def host_bytes(t: torch.Tensor) -> np.ndarray:
     """Raw bytes of a tensor as a contiguous host uint8 array."""
     return t.detach().contiguous().view(-1).view(torch.uint8).cpu().numpy()
+
+
+def lcg_bytes(seed: int, n: int) -> np.ndarray:
+    """n pattern bytes for known-answer vectors: the top byte of each state of
+    the 32-bit linear congruential generator x <- 1664525 x + 1013904223 mod
+    2^32 (the constants of Numerical Recipes' ranqd1), started at x = seed;
+    byte i comes from the state after i + 1 steps."""
+    out = np.empty(n, np.uint8)
+    x = seed & 0xFFFFFFFF
+    for i in range(n):
+        x = (1664525 * x + 1013904223) & 0xFFFFFFFF
+        out[i] = x >> 24
+    return out
