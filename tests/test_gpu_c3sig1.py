@@ -14,9 +14,11 @@ c3 = pytest.importorskip("paper_2608_11034_amd.c3")
 TORCH = {0: torch.float32, 1: torch.bfloat16, 2: torch.float16, 3: torch.uint8}
 
 
-def _device_tensor(t):
+def _device_tensor(t, device="cuda"):
     raw = torch.from_numpy(_tensor_bytes(t).copy())
-    return raw.view(TORCH[t["dtype"]]).reshape(t["shape"]).to("cuda")
+    if raw.numel() == 0:
+        return torch.empty(t["shape"], dtype=TORCH[t["dtype"]], device=device)
+    return raw.view(TORCH[t["dtype"]]).reshape(t["shape"]).to(device)
 
 
 @pytest.mark.parametrize("tile", [0, 1024])
