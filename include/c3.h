@@ -410,6 +410,29 @@ int c3_localize(const uint8_t *status, const uint64_t *bitmap, const int32_t *ma
                 int64_t out_cap, int64_t *undecided, int64_t und_cap, int64_t *counts, void *ws,
                 size_t ws_bytes, c3_stream_t stream);
 
+/* Largest n_units that c3_localize_noalloc accepts. */
+#define C3_LOCALIZE_NOALLOC_MAX_UNITS (1ll << 26)
+
+/*
+ * c3_localize_noalloc -- c3_localize for callers that cannot allocate device
+ * memory: code under HIP graph capture, tight serving loops and harnesses
+ * that forbid allocation.  Same arguments, outputs and errors as
+ * c3_localize, without the workspace: the segment counts and offsets it
+ * needs for more than 32,768 units live in a fixed 1 MiB device array that
+ * the library holds on every device it runs on until the process ends.  The
+ * call allocates nothing (no hipMalloc, no host allocation); the first call
+ * on a device looks up that device's copy of the array.
+ *   n_units    0..C3_LOCALIZE_NOALLOC_MAX_UNITS (2^26); more is C3_E_INVAL.
+ * Every call on one device shares that device's array: calls that overlap on
+ * one device (two streams, or two host threads) race and must be ordered by
+ * the caller.  Results are bit-identical to c3_localize's.
+ */
+int c3_localize_noalloc(const uint8_t *status, const uint64_t *bitmap,
+                        const int32_t *majority_idx, const c3_chunk_record_t *records, int R,
+                        int64_t n_units, c3_outlier_t *outliers, int64_t out_cap,
+                        int64_t *undecided, int64_t und_cap, int64_t *counts,
+                        c3_stream_t stream);
+
 /* Device workspace bytes c3_timing_consensus needs (256 at least; 0 if the
  * sizes are invalid). */
 size_t c3_timing_consensus_workspace_size(int R, int64_t G, int64_t T, int window);

@@ -10,6 +10,7 @@ Entry points (same names as the C ABI):
 * ``tensor_signature(records, T)``       -> per-tensor signatures [R, T]
 * ``consensus(evidence, mode, ...)``     -> status, bitmap, majority index
 * ``localize(status, bitmap, majority_idx, records, R)`` -> lists + counts
+* ``localize_noalloc(...)``              the same without a workspace
 * ``confirm(fp_bitmap, time_bitmap, R, window)`` -> per-rank verdicts
 * ``timing_consensus(fingerprints, times, window)`` -> verdicts (and per-unit
                                          results): both votes + confirmation
@@ -138,6 +139,8 @@ def lib():
         L.c3_localize_workspace_size.argtypes = [i64]
         L.c3_localize.restype = i32
         L.c3_localize.argtypes = [vp, vp, vp, vp, i32, i64, vp, i64, vp, i64, vp, vp, sz, vp]
+        L.c3_localize_noalloc.restype = i32
+        L.c3_localize_noalloc.argtypes = [vp, vp, vp, vp, i32, i64, vp, i64, vp, i64, vp, vp]
         L.c3_confirm_workspace_size.restype = sz
         L.c3_confirm_workspace_size.argtypes = [i32, i64, i64]
         L.c3_confirm.restype = i32
@@ -387,6 +390,40 @@ def localize(status, bitmap, majority_idx, records=None, R: int = None, out_cap:
                            _ptr(outliers), out_cap, _ptr(undecided), und_cap, _ptr(counts),
                            _ptr(ws), ws_bytes, _stream(stream))
     _check(rc, "c3_localize")
+    return outliers, undecided, counts
+
+
+LOCALIZE_NOALLOC_MAX_UNITS = 1 << 26
+
+
+def localize_noalloc(status, bitmap, majority_idx, records=None, R: int = None, out_cap: int = None,
+                     und_cap: int = None, stream=None, out=None):
+    """c3_localize_noalloc: localize without a workspace (the library's fixed
+    per-device scratch array; calls that overlap on one device race).  Same
+    results as ``localize``.  Pass ``out`` to allocate nothing here either."""
+    n_units = status.numel()
+    if R is None:
+        if records is None:
+            raise C3Error("R is required without records")
+        R = records.shape[0]
+    if 1 <= R <= MAX_PEERS and n_units > 0:
+        _check_out(bitmap, torch.int64, n_units * bitmap_words(R), "bitmap")
+        _check_out(majority_idx, torch.int32, n_units, "majority")
+    dev = status.device
+    out_cap = n_units * R if out_cap is None else out_cap
+    und_cap = n_units if und_cap is None else und_cap
+    if out is not None:
+        outliers, undecided, counts = out
+        out_cap = min(out_cap, outliers.shape[0])
+        und_cap = min(und_cap, undecided.numel())
+    else:
+        outliers = _empty((max(out_cap, 1), 80), torch.uint8, dev)
+        undecided = _empty((max(und_cap, 1),), torch.int64, dev)
+        counts = _empty((3,), torch.int64, dev)
+    rc = lib().c3_localize_noalloc(_ptr(status), _ptr(bitmap), _ptr(majority_idx), _ptr(records), R,
+                                   n_units, _ptr(outliers), out_cap, _ptr(undecided), und_cap,
+                                   _ptr(counts), _stream(stream))
+    _check(rc, "c3_localize_noalloc")
     return outliers, undecided, counts
 
 

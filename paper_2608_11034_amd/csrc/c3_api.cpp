@@ -435,6 +435,27 @@ int c3_consensus(const void* evidence, int evidence_kind, int64_t replica_stride
     return e == hipSuccess ? C3_OK : C3_E_HIP;
 }
 
+}  // extern "C"
+
+int c3::localize_check(const uint8_t* status, const uint64_t* bitmap, const int32_t* majority_idx,
+                       const c3_chunk_record_t* records, int R, int64_t n_units,
+                       const c3_outlier_t* outliers, int64_t out_cap, const int64_t* undecided,
+                       int64_t und_cap, const int64_t* counts) {
+    if (R < 2 || R > C3_MAX_PEERS || n_units < 0 || out_cap < 0 || und_cap < 0)
+        return C3_E_INVAL;
+    if (counts == nullptr) return C3_E_INVAL;
+    if (n_units > 0 && (status == nullptr || bitmap == nullptr || majority_idx == nullptr))
+        return C3_E_INVAL;
+    if ((out_cap > 0 && outliers == nullptr) || (und_cap > 0 && undecided == nullptr))
+        return C3_E_INVAL;
+    if (!aligned(bitmap, 8) || !aligned(majority_idx, 4) || !aligned(counts, 8) ||
+        !aligned(outliers, 8) || !aligned(undecided, 8) || !aligned(records, 8))
+        return C3_E_ALIGN;
+    return C3_OK;
+}
+
+extern "C" {
+
 size_t c3_localize_workspace_size(int64_t n_units) {
     return n_units < 0 ? 0 : c3::localize_ws_bytes(n_units);
 }
@@ -443,18 +464,11 @@ int c3_localize(const uint8_t* status, const uint64_t* bitmap, const int32_t* ma
                 const c3_chunk_record_t* records, int R, int64_t n_units, c3_outlier_t* outliers,
                 int64_t out_cap, int64_t* undecided, int64_t und_cap, int64_t* counts, void* ws,
                 size_t ws_bytes, c3_stream_t stream) {
-    if (R < 2 || R > C3_MAX_PEERS || n_units < 0 || out_cap < 0 || und_cap < 0)
-        return C3_E_INVAL;
-    if (counts == nullptr) return C3_E_INVAL;
-    if (n_units > 0 && (status == nullptr || bitmap == nullptr || majority_idx == nullptr))
-        return C3_E_INVAL;
-    if ((out_cap > 0 && outliers == nullptr) || (und_cap > 0 && undecided == nullptr))
-        return C3_E_INVAL;
+    const int rc = c3::localize_check(status, bitmap, majority_idx, records, R, n_units, outliers,
+                                      out_cap, undecided, und_cap, counts);
+    if (rc != C3_OK) return rc;
     if (ws == nullptr || !aligned(ws, 256) || ws_bytes < c3::localize_ws_bytes(n_units))
         return C3_E_WORKSPACE;
-    if (!aligned(bitmap, 8) || !aligned(majority_idx, 4) || !aligned(counts, 8) ||
-        !aligned(outliers, 8) || !aligned(undecided, 8) || !aligned(records, 8))
-        return C3_E_ALIGN;
     const hipError_t e = c3::launch_localize(status, bitmap, majority_idx, records, R, n_units,
                                              outliers, out_cap, undecided, und_cap, counts, ws,
                                              reinterpret_cast<hipStream_t>(stream));

@@ -72,6 +72,13 @@ hipError_t launch_consensus(const void* evidence, int kind, int64_t rstride, int
                             int64_t n_units, int mode, double kappa, uint8_t* status,
                             uint64_t* bitmap, int32_t* majority_idx, hipStream_t stream);
 
+// Argument checks shared by c3_localize and c3_localize_noalloc (everything
+// but the workspace); C3_OK or an error code.
+int localize_check(const uint8_t* status, const uint64_t* bitmap, const int32_t* majority_idx,
+                   const c3_chunk_record_t* records, int R, int64_t n_units,
+                   const c3_outlier_t* outliers, int64_t out_cap, const int64_t* undecided,
+                   int64_t und_cap, const int64_t* counts);
+
 size_t localize_ws_bytes(int64_t n_units);
 hipError_t launch_localize(const uint8_t* status, const uint64_t* bitmap,
                            const int32_t* majority_idx, const c3_chunk_record_t* records, int R,

@@ -14,6 +14,8 @@
 // A thread owns kPerThread consecutive units, so list order is (unit
 // ascending, replica ascending) by construction.  A unit's bitmap is W =
 // ceil(R / 64) words, bit b of word w naming replica 64 w + b.
+#include <mutex>
+
 #include "c3_device.h"
 #include "c3_internal.h"
 
@@ -328,3 +330,73 @@ hipError_t launch_localize(const uint8_t* status, const uint64_t* bitmap,
 }
 
 }  // namespace c3
+
+// ---------------------------------------------------------------------------
+// c3_localize_noalloc: c3_localize with its workspace (the per-segment
+// counts and offsets of the three-pass compaction) in a fixed device array
+// instead of a caller buffer, for callers that cannot allocate.  Every call
+// on one device shares that device's copy of the array; the count kernel
+// writes every segment entry before the scan and emit kernels read it, so
+// nothing has to start at zero, and calls that overlap on one device race.
+// ---------------------------------------------------------------------------
+constexpr size_t kNoallocScratchBytes = 1u << 20;
+static_assert((C3_LOCALIZE_NOALLOC_MAX_UNITS + c3::kSegUnits - 1) / c3::kSegUnits *
+                      (int64_t)sizeof(c3::SegCount) + 256 <= (int64_t)kNoallocScratchBytes,
+              "scratch too small for the largest accepted input");
+
+// In host code `scratch` names a host-side stand-in; its device address on
+// each GPU is taken once with hipGetSymbolAddress and only that is used.
+static __device__ __align__(256) unsigned char scratch[kNoallocScratchBytes];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of `scratch` on the device `stream` belongs to, looked up
+// with that device current on the first call for the device.
+hipError_t scratch_address(hipStream_t stream, void** out) {
+    int dev = 0;
+    if (hipStreamGetDevice(stream, &dev) != hipSuccess) {
+        (void)hipGetLastError();
+        hipError_t e = hipGetDevice(&dev);
+        if (e != hipSuccess) return e;
+    }
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (g_scratch_ptr[dev] == nullptr) {
+        int cur = 0;
+        hipError_t e = hipGetDevice(&cur);
+        if (e != hipSuccess) return e;
+        if (cur != dev && (e = hipSetDevice(dev)) != hipSuccess) return e;
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        const hipError_t e2 = cur != dev ? hipSetDevice(cur) : hipSuccess;
+        if (e != hipSuccess) return e;
+        if (e2 != hipSuccess) return e2;
+        if (p == nullptr) return hipErrorInvalidSymbol;
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return hipSuccess;
+}
+
+}  // namespace
+
+extern "C" int c3_localize_noalloc(const uint8_t* status, const uint64_t* bitmap,
+                                   const int32_t* majority_idx, const c3_chunk_record_t* records,
+                                   int R, int64_t n_units, c3_outlier_t* outliers,
+                                   int64_t out_cap, int64_t* undecided, int64_t und_cap,
+                                   int64_t* counts, c3_stream_t stream) {
+    const int rc = c3::localize_check(status, bitmap, majority_idx, records, R, n_units, outliers,
+                                      out_cap, undecided, und_cap, counts);
+    if (rc != C3_OK) return rc;
+    if (n_units > C3_LOCALIZE_NOALLOC_MAX_UNITS) return C3_E_INVAL;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    void* ws = nullptr;
+    if (scratch_address(s, &ws) != hipSuccess) return C3_E_HIP;
+    const hipError_t e = c3::launch_localize(status, bitmap, majority_idx, records, R, n_units,
+                                             outliers, out_cap, undecided, und_cap, counts, ws, s);
+    return e == hipSuccess ? C3_OK : C3_E_HIP;
+}

@@ -151,6 +151,19 @@ def test_singleton_group_is_rejected_before_gpu_work():
     assert L.c3_signature_workspace_size(md, 1, 1, 1024) > 0
 
 
+def test_localize_noalloc_argument_errors_return_before_gpu_work():
+    L = c3.lib()
+    null = ctypes.c_void_p(0)
+    p8 = ctypes.c_void_p(8)
+    big = c3.LOCALIZE_NOALLOC_MAX_UNITS + 1
+    assert L.c3_localize_noalloc(p8, p8, p8, null, 8, big, p8, 10, p8, 10, p8, null) == -1
+    assert L.c3_localize_noalloc(p8, p8, p8, null, 1, 10, p8, 10, p8, 10, p8, null) == -1
+    assert L.c3_localize_noalloc(p8, p8, p8, null, 257, 10, p8, 10, p8, 10, p8, null) == -1
+    assert L.c3_localize_noalloc(p8, p8, p8, null, 8, 10, p8, 10, p8, 10, null, null) == -1
+    assert L.c3_localize_noalloc(p8, ctypes.c_void_p(4), p8, null, 8, 10, p8, 10, p8, 10, p8,
+                                 null) == -2
+
+
 def test_binding_has_no_cpu_fallback():
     import torch
     x = torch.zeros(1024)
