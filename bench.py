@@ -68,20 +68,59 @@ def measured_traffic(workload: str):
 
 
 def host_cpu():
-    """Host CPU model and the number of cores this process may run on."""
-    model = "unknown"
+    """Host CPU model (the kernel's model string, and lscpu's when it says
+    more), the CPU family/model/stepping numbers, and the cores this process
+    may run on."""
+    import subprocess
+    info = {}
     try:
         for ln in open("/proc/cpuinfo"):
-            if ln.startswith("model name"):
-                model = ln.split(":", 1)[1].strip()
+            k, _, v = ln.partition(":")
+            k = k.strip()
+            if k in ("model name", "cpu family", "model", "stepping") and k not in info:
+                info[k] = v.strip()
+            if not ln.strip() and info:
                 break
     except OSError:
         pass
-    return {"model": model, "cores_available": len(os.sched_getaffinity(0))}
+    model = info.get("model name", "unknown")
+    try:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for ln in out.splitlines():
+            if ln.startswith("Model name:"):
+                lm = ln.split(":", 1)[1].strip()
+                if len(lm) > len(model):
+                    model = lm
+    except (OSError, subprocess.SubprocessError):
+        pass
+    return {"model": model, "family_model_stepping": [info.get("cpu family"), info.get("model"),
+                                                      info.get("stepping")],
+            "cores_available": len(os.sched_getaffinity(0))}
 
 
-def cpu_baseline(w, budget_s: float):
-    """Oracle over the first chunks of every replica: bounded sample, one thread."""
+def records_match(g, ref):
+    """GPU records [R, C] against the oracle's: bit-exact signature, counts,
+    ids and absmax; fp64 sums within |d| <= max(1e-6 |ref|, 1e-12
+    sqrt(n_finite sumsq)), sums of squares within 1e-6 relative.  Returns
+    the number of records that differ."""
+    import numpy as np
+    exact = ((g["sig"] == ref["sig"]) & (g["n_elems"] == ref["n_elems"]) &
+             (g["nan_count"] == ref["nan"]) & (g["inf_count"] == ref["inf"]) &
+             (g["tensor"] == ref["tensor"]) & (g["chunk_in_tensor"] == ref["chunk"]) &
+             (g["absmax"] == ref["absmax"]))
+    n_fin = ref["n_elems"].astype(np.float64) - ref["nan"] - ref["inf"]
+    floor = 1e-12 * np.sqrt(np.maximum(n_fin, 0) * np.maximum(ref["sumsq"], 0))
+    s_ok = np.abs(g["sum"] - ref["sum"]) <= np.maximum(1e-6 * np.abs(ref["sum"]), floor)
+    q_ok = np.abs(g["sumsq"] - ref["sumsq"]) <= 1e-6 * np.abs(ref["sumsq"])
+    return int((~(exact & s_ok & q_ok)).sum())
+
+
+def cpu_baseline(w, budget_s: float, gpu=None):
+    """Oracle over the first chunks of every replica: bounded sample, one
+    thread pinned to one host core.  With `gpu` (records [R, C] and the
+    per-chunk status, bitmap and majority of the timed steps, as numpy), the
+    oracle's records, votes and lists of the sample are compared with the
+    GPU's for the same chunks."""
     import numpy as np
     import oracle
     import workloads
@@ -97,17 +136,42 @@ def cpu_baseline(w, budget_s: float):
         metas.append((d, shape))
         nbytes += nb
     T = len(metas)
-    reps = [[workloads.host_bytes(w.replicas[r][t]) for t in range(T)] for r in range(w.R)]
     t0 = time.perf_counter()
-    rec = oracle.signature(reps, metas, w.chunk_bytes)
-    st, bm, mj = oracle.vote_exact(rec["sig"])
-    oracle.localize(st, bm, mj, w.R)
-    dt = time.perf_counter() - t0
+    reps = [[workloads.host_bytes(w.replicas[r][t]) for t in range(T)] for r in range(w.R)]
+    d2h = time.perf_counter() - t0
+    affinity = os.sched_getaffinity(0)
+    core = min(affinity)
+    os.sched_setaffinity(0, {core})
+    try:
+        t0 = time.perf_counter()
+        rec = oracle.signature(reps, metas, w.chunk_bytes)
+        st, bm, mj = oracle.vote_exact(rec["sig"])
+        loc = oracle.localize(st, bm, mj, w.R)
+        dt = time.perf_counter() - t0
+    finally:
+        os.sched_setaffinity(0, affinity)
     sample_bytes = nbytes * w.R
-    return {"value": sample_bytes / dt / 1e9, "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "sample": f"first {T} tensors of all {w.R} replicas ({sample_bytes} bytes, "
-                      f"{rec['sig'].shape[1]} chunks), signature+vote+localize, {dt:.1f} s",
-            "seconds": dt, "host": host_cpu()}
+    Cs = rec["sig"].shape[1]
+    out = {"value": sample_bytes / dt / 1e9, "unit": "GB/s", "cores": 1, "kind": "oracle",
+           "sample": f"first {T} tensors of all {w.R} replicas ({sample_bytes} bytes, "
+                     f"{Cs} chunks), signature+vote+localize, {dt:.1f} s on host core {core}",
+           "seconds": dt, "d2h_seconds": round(d2h, 3),
+           "d2h_GBps": round(sample_bytes / d2h / 1e9, 2) if d2h > 0 else None,
+           "host": host_cpu()}
+    if gpu is not None:
+        bad = records_match(gpu["records"][:, :Cs], rec)
+        votes_ok = (np.array_equal(gpu["status"][:Cs], st) and
+                    np.array_equal(gpu["bitmap"][:Cs], bm) and np.array_equal(gpu["maj"][:Cs], mj))
+        o = gpu["outliers"]
+        sel = o["chunk"] < Cs
+        lists_ok = (o["chunk"][sel].tolist() == loc["unit"].tolist() and
+                    o["replica"][sel].tolist() == loc["replica"].tolist() and
+                    o["majority_replica"][sel].tolist() == loc["majority"].tolist())
+        out["parity"] = {"ok": bad == 0 and votes_ok and lists_ok,
+                         "records_compared": int(w.R * Cs), "records_differing": bad,
+                         "chunks_compared": int(Cs), "votes_equal": bool(votes_ok),
+                         "outlier_list_equal": bool(lists_ok)}
+    return out
 
 
 def main():
@@ -162,16 +226,19 @@ def main():
         c3.localize(status, bitmap, maj, rec, out=(outl, und, cnt), workspace=lws)
 
     def timed(staged):
-        e0 = torch.cuda.Event(enable_timing=True)
-        e1 = torch.cuda.Event(enable_timing=True)
+        """Mean ms per step over the K steps, the per-step median and
+        minimum (an event between consecutive steps), and the wall time."""
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
         torch.cuda.synchronize()
         t0 = time.perf_counter()
-        e0.record()
-        for _ in range(args.steps):
+        evs[0].record()
+        for i in range(args.steps):
             step(staged)
-        e1.record()
+            evs[i + 1].record()
         torch.cuda.synchronize()
-        return e0.elapsed_time(e1) / args.steps, time.perf_counter() - t0
+        per = sorted(evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps))
+        mean = evs[0].elapsed_time(evs[-1]) / args.steps
+        return mean, per[len(per) // 2], per[0], time.perf_counter() - t0
 
     args.warmup = warm_up(torch, step, args.warmup)
     log(f"[bench] warmup {args.warmup} steps")
@@ -179,10 +246,10 @@ def main():
     log(f"[bench] outliers={counts[0]} undecided={counts[1]} attributed_chunks={counts[2]}")
 
     log(f"[bench] timing {args.steps} steps")
-    ms_per_step, wall = timed(staged=False)
+    ms_per_step, step_med, step_min, wall = timed(staged=False)
     value = total / (ms_per_step * 1e-3) / 1e9
     # the same steps when the plan staged by the previous call is reused
-    ms_staged, _ = timed(staged=True)
+    ms_staged, _, _, _ = timed(staged=True)
 
     # dominant kernel: the streaming signature kernel, events recorded by the
     # library on the launch stream immediately around it
@@ -201,6 +268,29 @@ def main():
     k_med, k_min = k_all[len(k_all) // 2], k_all[0]
     achieved = total / (k_ms * 1e-3) / 1e9
 
+    # the read ceiling of the same access pattern: the library's read probe
+    # (256 KiB tiles, 16 loads in flight per lane, nothing computed) over a
+    # buffer of the same size, capped at 32 GiB, timed the same way
+    log("[bench] timing the read probe")
+    probe_bytes = min(total, 32 << 30) // 1024 * 1024
+    probe_buf = torch.empty(probe_bytes, dtype=torch.uint8, device=dev)
+    probe_cs = torch.empty(-(-probe_bytes // (256 << 10)), dtype=torch.int64, device=dev)
+    for _ in range(3):
+        c3.read_probe(probe_buf, 0, checksum=probe_cs)
+    pevs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+            for _ in range(args.steps)]
+    for a, b in pevs:
+        a.record()
+        b.record()
+    torch.cuda.synchronize()
+    for a, b in pevs:
+        c3.read_probe(probe_buf, 0, checksum=probe_cs, ev_begin=a, ev_end=b)
+    torch.cuda.synchronize()
+    p_all = sorted(a.elapsed_time(b) for a, b in pevs)
+    p_ms = sum(p_all) / len(p_all)
+    achievable = probe_bytes / (p_ms * 1e-3) / 1e9
+    del probe_buf, probe_cs
+
     if args.copy_calibration:
         log("[bench] copy calibration: 1 GiB device copy x3")
         src = torch.empty(1 << 30, dtype=torch.uint8, device=dev).fill_(1)
@@ -211,11 +301,19 @@ def main():
         del src, dst
 
     cpu = None
+    parity = None
     if not args.no_cpu_baseline:
         log("[bench] CPU oracle baseline on a bounded sample")
-        cpu = cpu_baseline(w, args.cpu_budget)
-        log(f"[bench] oracle {cpu['value']:.3f} GB/s over {cpu['seconds']:.1f} s")
+        # the timed steps' own outputs (every step rewrites the same buffers)
+        import numpy as np
+        gpu = {"records": c3.records_numpy(rec), "status": status.cpu().numpy(),
+               "bitmap": bitmap.cpu().numpy().view(np.uint64), "maj": maj.cpu().numpy(),
+               "outliers": c3.outliers_numpy(outl, cnt)}
+        cpu = cpu_baseline(w, args.cpu_budget, gpu)
+        log(f"[bench] oracle {cpu['value']:.3f} GB/s over {cpu['seconds']:.1f} s; "
+            f"parity {cpu['parity']}")
         cpu.pop("seconds")
+        parity = cpu.pop("parity")
 
     traffic = measured_traffic(w.name)
     out = {
@@ -226,12 +324,15 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 4),
+        "ms_per_step_median": round(step_med, 4),
+        "ms_per_step_min": round(step_min, 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "u64+f64",
         "data": "synthetic",
         "pct_of_hbm_peak": round(100.0 * value / HBM_PEAK_GBS, 2),
+        "parity": parity,
         "config": {"workload": w.name, "R": w.R, "tensors_per_replica": len(w.metas),
                    "bytes_per_replica": w.bytes_per_replica, "replica_bytes_total": total,
                    "chunk_bytes": w.chunk_bytes, "chunks": C,
@@ -241,7 +342,13 @@ def main():
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": traffic, "kernel": "signature_kernel",
                      "kernel_ms": round(k_ms, 4), "kernel_ms_median": round(k_med, 4),
-                     "kernel_ms_min": round(k_min, 4), "algorithmic_bytes_per_launch": total},
+                     "kernel_ms_min": round(k_min, 4), "algorithmic_bytes_per_launch": total,
+                     "achievable": {"GBps": round(achievable, 2), "kernel": "read_probe_kernel",
+                                    "bytes_per_launch": probe_bytes, "ms": round(p_ms, 4),
+                                    "ms_median": round(p_all[len(p_all) // 2], 4),
+                                    "ms_min": round(p_all[0], 4),
+                                    "frac_of_peak": round(achievable / HBM_PEAK_GBS, 4)},
+                     "frac_of_achievable": round(achieved / achievable, 4)},
         "cpu_baseline": cpu,
         "wall_s_timed": round(wall, 3),
         "ms_per_step_plan_reused": round(ms_staged, 4),
@@ -445,8 +552,8 @@ def bench_optimizer(args, torch, workloads, c3, dev):
     sws = plan.new_workspace()
     plan.run(rec, sws)
     # the staged plan is reused (no fetch kernel); the library records the
-    # first event right before the first signature kernel and the last one
-    # after the last partial combine
+    # first event right before the first signature kernel, and the last one
+    # is recorded again after the loop, behind the last partial combine
     k_sig = batch_ms(lambda i, a, b: plan.run(rec, sws, plan_staged=True, ev_begin=a, ev_end=b))
     del head_src, head_dst
     adamw_bytes = R * n * 28                 # read p, g, m, v; write p', m', v'

@@ -166,10 +166,11 @@ typedef struct {
 
 /* Optional launch controls for c3_signature_ex.
  *   ev_kernel_begin / ev_kernel_end: if non-NULL, recorded on the stream
- *     immediately before the streaming signature kernel (after the plan is
- *     staged) and after the pass ends: the streaming kernel, plus the combine
- *     of tile partials when a chunk spans several tiles.  Either may be
- *     given alone, so a run of calls can be timed as a whole.
+ *     immediately before the first streaming signature kernel (after the
+ *     plan is staged) and immediately after the last one, before the
+ *     combine of tile partials that chunks spanning several tiles need.
+ *     Either may be given alone, so a run of calls can be timed as a
+ *     whole.
  *   grid_blocks: workgroups of the streaming kernel; 0 chooses one per tile.
  *     Results do not depend on it.
  *   flags: C3_OPT_PLAN_STAGED -- the workspace still holds the plan that a
@@ -566,6 +567,29 @@ int c3_ckpt_save(c3_ckpt_state_t *st, int outcome, int64_t checkpoint_id, int ma
  * replay found SDC, then verified. */
 int c3_ckpt_retrieve(const c3_ckpt_state_t *st, int outcome, int machines_accessible,
                      int full_catalog_sdc, int64_t *checkpoint_id);
+
+/* ---------------------------------------------------------------------- */
+/* Measurement aid (not part of the method).                              */
+/* ---------------------------------------------------------------------- */
+
+/*
+ * c3_read_probe -- reads `bytes` of device memory once with the streaming
+ * signature kernel's access pattern (one 256-thread workgroup per tile,
+ * 1 KiB blocks round-robin over its four waves, 128-bit non-temporal loads,
+ * 16 in flight per lane) and nothing else, so the signature pass can be set
+ * against the read rate this pattern reaches on the same device.
+ *   buf        device, 16-byte aligned; bytes a multiple of 1024 (whole
+ *              1 KiB blocks, so every load lies inside the buffer; 0: nothing).
+ *   tile_bytes power of two in [1 KiB, 16 MiB]; 0 = the signature kernel's
+ *              default tile (256 KiB).
+ *   checksum   device [ceil(bytes / tile_bytes)] u64, 8-byte aligned: the
+ *              xor of the little-endian 64-bit words of each tile.
+ *   ev_begin, ev_end  optional events recorded on the stream immediately
+ *              around the probe kernel.
+ * Errors: C3_E_INVAL, C3_E_ALIGN, C3_E_HIP.
+ */
+int c3_read_probe(const void *buf, uint64_t bytes, uint64_t tile_bytes, uint64_t *checksum,
+                  c3_event_t ev_begin, c3_event_t ev_end, c3_stream_t stream);
 
 /* Static description of a status code. */
 const char *c3_status_string(int code);

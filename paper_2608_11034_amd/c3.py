@@ -156,6 +156,8 @@ def lib():
         L.c3_timing_consensus.restype = i32
         L.c3_timing_consensus.argtypes = [vp, vp, i32, i32, i64, i64, dbl, i32, vp, vp, vp, vp, vp,
                                           vp, vp, vp, sz, vp]
+        L.c3_read_probe.restype = i32
+        L.c3_read_probe.argtypes = [vp, u64, u64, vp, vp, vp, vp]
         L.c3_job_outcome.restype = i32
         L.c3_job_outcome.argtypes = [i64, i64, i64]
         L.c3_ckpt_init.restype = i32
@@ -620,6 +622,29 @@ class OptimizerBoundaryCheck:
         _check(rc, "c3_optimizer_check")
         return (self.records, self.status, self.bitmap, self.majority, self.outliers,
                 self.undecided, self.counts)
+
+
+# ---------------------------------------------------------------------------
+# measurement aid
+# ---------------------------------------------------------------------------
+def read_probe(buf: torch.Tensor, tile_bytes: int = 0, checksum=None, ev_begin=None,
+               ev_end=None, stream=None):
+    """c3_read_probe over the bytes of ``buf``: one read with the signature
+    kernel's access pattern.  Returns the per-tile xor checksums [n_tiles]
+    (int64 bit patterns)."""
+    _dev_tensor(buf, "buf")
+    nbytes = buf.numel() * buf.element_size()
+    tb = tile_bytes or 256 * 1024
+    n_tiles = -(-nbytes // tb)
+    if checksum is None:
+        checksum = _empty((max(n_tiles, 1),), torch.int64, buf.device)
+    elif checksum.numel() < n_tiles:
+        raise C3Error("checksum holds fewer values than tiles")
+    rc = lib().c3_read_probe(_ptr(buf), nbytes, tile_bytes, _ptr(checksum),
+                             ev_begin.cuda_event if ev_begin is not None else None,
+                             ev_end.cuda_event if ev_end is not None else None, _stream(stream))
+    _check(rc, "c3_read_probe")
+    return checksum[:n_tiles]
 
 
 # ---------------------------------------------------------------------------

@@ -353,13 +353,12 @@ int signature_impl(const void* const* ptrs, const c3_tensor_meta_t* metas, int T
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     const bool staged = opts != nullptr && (opts->flags & C3_OPT_PLAN_STAGED) != 0;
     if (!staged && stage_to_device(ws, buf.data(), buf.size(), s) != hipSuccess) return C3_E_HIP;
-    // the end event follows the whole pass: the streaming kernels and, for
-    // tiled plans, the combine of their partials
-    hipError_t e = c3::launch_signature(
+    // the events bracket the streaming kernels only: the end event is
+    // recorded before the combine of tile partials of multi-tile chunks
+    const hipError_t e = c3::launch_signature(
         static_cast<const SigPlan*>(ws), p.h, p.groups, records, opts ? opts->grid_blocks : 0,
-        true, s, opts ? reinterpret_cast<hipEvent_t>(opts->ev_kernel_begin) : nullptr, nullptr);
-    if (e == hipSuccess && opts != nullptr && opts->ev_kernel_end != nullptr)
-        e = hipEventRecord(reinterpret_cast<hipEvent_t>(opts->ev_kernel_end), s);
+        true, s, opts ? reinterpret_cast<hipEvent_t>(opts->ev_kernel_begin) : nullptr,
+        opts ? reinterpret_cast<hipEvent_t>(opts->ev_kernel_end) : nullptr);
     return e == hipSuccess ? C3_OK : C3_E_HIP;
 }
 
@@ -680,6 +679,24 @@ int c3_timing_consensus(const uint64_t* fingerprints, const void* times, int tim
         e = c3::launch_consensus(times, time_kind, tsize, (int64_t)tsize * R, R, (int64_t)n,
                                  C3_STATISTICAL, kappa, ts, tb, tm, s);
     if (e == hipSuccess) e = c3::launch_confirm(fb, tb, R, G, T, window, verdicts, cws, s);
+    return e == hipSuccess ? C3_OK : C3_E_HIP;
+}
+
+int c3_read_probe(const void* buf, uint64_t bytes, uint64_t tile_bytes, uint64_t* checksum,
+                  c3_event_t ev_begin, c3_event_t ev_end, c3_stream_t stream) {
+    if (tile_bytes == 0) tile_bytes = c3::kDefaultTileMax;
+    if (tile_bytes < 1024 || tile_bytes > (1ull << 24) || (tile_bytes & (tile_bytes - 1)) != 0 ||
+        bytes % 1024 != 0 || bytes > (1ull << 46))
+        return C3_E_INVAL;
+    if (bytes == 0) return C3_OK;
+    if (buf == nullptr || checksum == nullptr) return C3_E_INVAL;
+    if (!aligned(buf, 16) || !aligned(checksum, 8)) return C3_E_ALIGN;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    hipError_t e = hipSuccess;
+    if (ev_begin != nullptr) e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev_begin), s);
+    if (e == hipSuccess) e = c3::launch_read_probe(buf, bytes, tile_bytes, checksum, s);
+    if (e == hipSuccess && ev_end != nullptr)
+        e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev_end), s);
     return e == hipSuccess ? C3_OK : C3_E_HIP;
 }
 

@@ -76,4 +76,39 @@ __device__ inline double shfl_f64(double v, int src) {
 
 __device__ inline uint64_t ballot64(bool p) { return __ballot(p); }
 
+// ---------------------------------------------------------------------------
+// 128-bit streaming loads
+// ---------------------------------------------------------------------------
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef const __attribute__((address_space(1))) u32x4 gu32x4;
+
+// 128-bit streaming load from global memory, non-temporal (read once).
+__device__ inline u32x4 load16(const u32x4* p) {
+    return __builtin_nontemporal_load((gu32x4*)p);
+}
+
+// Raw buffer resource over the `len` bytes at `base` (stride 0, untyped
+// 32-bit data format in the descriptor's last word, as gfx9 buffer loads
+// require).  Callers load only whole 16-byte segments of whole 1 KiB blocks
+// that lie inside `len`, so nothing depends on the hardware range check.
+// Tiles are at most 16 MiB, so `len` fits the 32-bit record count.  Base and
+// length are taken from the first lane: the resource must sit in scalar
+// registers even when the compiler cannot prove them uniform.
+constexpr int kRawBufferWord3 = 0x00020000;
+
+__device__ inline __amdgpu_buffer_rsrc_t tile_resource(const uint8_t* base, uint32_t len) {
+    const uint64_t a = reinterpret_cast<uint64_t>(base);
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)a);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(a >> 32));
+    const int n = __builtin_amdgcn_readfirstlane((int)len);
+    void* b = reinterpret_cast<void*>(((uint64_t)hi << 32) | lo);
+    return __builtin_amdgcn_make_buffer_rsrc(b, (short)0, n, kRawBufferWord3);
+}
+
+// 128-bit non-temporal buffer load at voffset + soffset bytes.
+__device__ inline u32x4 load16_buf(__amdgpu_buffer_rsrc_t rs, uint32_t voff, uint32_t soff) {
+    constexpr int kNonTemporal = 2;
+    return __builtin_amdgcn_raw_buffer_load_b128(rs, (int)voff, (int)soff, kNonTemporal);
+}
+
 }  // namespace c3

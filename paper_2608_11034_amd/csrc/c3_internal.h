@@ -86,6 +86,11 @@ hipError_t launch_localize(const uint8_t* status, const uint64_t* bitmap,
                            int64_t* undecided, int64_t und_cap, int64_t* counts, void* ws,
                            hipStream_t stream);
 
+// Read-only probe over `bytes` (a multiple of 1024) in tiles of tile_bytes;
+// writes the xor of each tile's 64-bit words to checksum[tile].
+hipError_t launch_read_probe(const void* buf, uint64_t bytes, uint64_t tile_bytes,
+                             uint64_t* checksum, hipStream_t stream);
+
 size_t confirm_ws_bytes(int R, int64_t G, int64_t T);
 hipError_t launch_confirm(const uint64_t* fp_bitmap, const uint64_t* time_bitmap, int R, int64_t G,
                           int64_t T, int window, c3_rank_verdict_t* verdicts, void* ws,

@@ -40,40 +40,9 @@
 
 namespace c3 {
 
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef const __attribute__((address_space(1))) u32x4 gu32x4;
-
 struct LaneKeys {
     uint32_t k0, k1, k2, k3, k4, k5;
 };
-
-// 128-bit streaming load from global memory, non-temporal (read once).
-__device__ inline u32x4 load16(const u32x4* p) {
-    return __builtin_nontemporal_load((gu32x4*)p);
-}
-
-// Raw buffer resource over the `len` bytes at `base` (stride 0, untyped
-// 32-bit data format in the descriptor's last word, as gfx9 buffer loads
-// require); loads past `len` return zero.  Tiles are at most 16 MiB, so `len`
-// fits the 32-bit record count.  The plan is read with vector loads (the
-// kernel also writes through it), so base and length are taken from the first
-// lane: the resource must sit in scalar registers.
-constexpr int kRawBufferWord3 = 0x00020000;
-
-__device__ inline __amdgpu_buffer_rsrc_t tile_resource(const uint8_t* base, uint32_t len) {
-    const uint64_t a = reinterpret_cast<uint64_t>(base);
-    const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)a);
-    const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(a >> 32));
-    const int n = __builtin_amdgcn_readfirstlane((int)len);
-    void* b = reinterpret_cast<void*>(((uint64_t)hi << 32) | lo);
-    return __builtin_amdgcn_make_buffer_rsrc(b, (short)0, n, kRawBufferWord3);
-}
-
-// 128-bit non-temporal buffer load at voffset + soffset bytes.
-__device__ inline u32x4 load16_buf(__amdgpu_buffer_rsrc_t rs, uint32_t voff, uint32_t soff) {
-    constexpr int kNonTemporal = 2;
-    return __builtin_amdgcn_raw_buffer_load_b128(rs, (int)voff, (int)soff, kNonTemporal);
-}
 
 // beta of block b (wave-uniform, so it stays in a scalar register)
 __device__ inline uint32_t block_beta(uint32_t b) { return b * kBlockMul; }

@@ -164,6 +164,19 @@ def test_localize_noalloc_argument_errors_return_before_gpu_work():
                                  null) == -2
 
 
+def test_read_probe_argument_errors_return_before_gpu_work():
+    L = c3.lib()
+    null = ctypes.c_void_p(0)
+    p16 = ctypes.c_void_p(256)
+    assert L.c3_read_probe(p16, 4096, 3000, p16, null, null, null) == -1      # tile not 2^k
+    assert L.c3_read_probe(p16, 4080, 1024, p16, null, null, null) == -1      # bytes % 1024
+    assert L.c3_read_probe(p16, 4096, 512, p16, null, null, null) == -1       # tile < 1 KiB
+    assert L.c3_read_probe(p16, 4096, 1 << 25, p16, null, null, null) == -1   # tile > 16 MiB
+    assert L.c3_read_probe(ctypes.c_void_p(8), 4096, 0, p16, null, null, null) == -2
+    assert L.c3_read_probe(null, 0, 0, null, null, null, null) == 0           # nothing to read
+    assert L.c3_read_probe(null, 4096, 0, p16, null, null, null) == -1
+
+
 def test_binding_has_no_cpu_fallback():
     import torch
     x = torch.zeros(1024)

@@ -15,7 +15,7 @@ import torch
 
 import oracle
 import workloads
-from parity import compare_all_records, compare_record
+from parity import compare_all_records
 
 pytestmark = pytest.mark.gpu
 
@@ -592,18 +592,49 @@ def test_confirm_pair_across_segments(W, R):
 # ---------------------------------------------------------------------------
 # full sizes, benchmark launch configuration
 # ---------------------------------------------------------------------------
-def _chunk_range(w, c):
+def _oracle_records_streamed(w, workers=None):
+    """Oracle records [R, C] of a full-size workload, every (replica, chunk):
+    one (replica, tensor) is copied to the host at a time (8 GB at most for
+    the Adam shard) and its chunks are signed by a pool of host threads (the
+    oracle is plain C called through ctypes, which releases the GIL)."""
+    from concurrent.futures import ThreadPoolExecutor
+    import os
+    workers = workers or max(1, min(16, len(os.sched_getaffinity(0))))
+    C = oracle.num_chunks(w.metas, w.chunk_bytes)
+    out = dict(sig=np.zeros((w.R, C), np.uint64), n_elems=np.zeros((w.R, C), np.uint64),
+               nan=np.zeros((w.R, C), np.uint32), inf=np.zeros((w.R, C), np.uint32),
+               absmax=np.zeros((w.R, C), np.float64), sum=np.zeros((w.R, C), np.float64),
+               sumsq=np.zeros((w.R, C), np.float64), tensor=np.zeros((w.R, C), np.uint32),
+               chunk=np.zeros((w.R, C), np.uint32))
     bases = _chunk_bases(w.metas, w.chunk_bytes)
-    t = int(np.searchsorted(bases, c, side="right") - 1)
-    k = c - int(bases[t])
-    d, shape = w.metas[t]
-    nb = int(np.prod(shape, dtype=np.int64)) * workloads.ELEM_SIZE[d]
-    lo = k * w.chunk_bytes
-    return t, k, lo, min(nb, lo + w.chunk_bytes)
+    oracle.keys()                                   # load the library before the threads
+    with ThreadPoolExecutor(workers) as pool:
+        for r in range(w.R):
+            for t, (d, shape) in enumerate(w.metas):
+                host = workloads.host_bytes(w.replicas[r][t])
+                nb = host.size
+                nc = int(bases[t + 1] - bases[t])
+
+                def one(k, host=host, d=d, shape=shape, nb=nb):
+                    lo = k * w.chunk_bytes
+                    return k, oracle.chunk_signature(host[lo:min(nb, lo + w.chunk_bytes)], d,
+                                                     list(shape), k)
+                for k, ref in pool.map(one, range(nc)):
+                    c = int(bases[t]) + k
+                    for f in ("sig", "n_elems", "nan", "inf", "absmax", "sum", "sumsq"):
+                        out[f][r, c] = ref[f]
+                    out["tensor"][r, c] = t
+                    out["chunk"][r, c] = k
+                del host
+    return out
 
 
-@pytest.mark.parametrize("k", [2, 3, 4])
+@pytest.mark.parametrize("k", [1, 2, 3, 4])
 def test_full_config_parity(k):
+    """Every configuration at its full size, in the benchmark's launch
+    configuration: every record of every replica against the oracle, the
+    votes and lists against the oracle's on those records, the planted faults
+    exactly, and signature equality equal to byte equality on every chunk."""
     _print_case("full config", k)
     torch.cuda.empty_cache()
     w = workloads.make(k, device=DEV, scale="full")
@@ -613,6 +644,11 @@ def test_full_config_parity(k):
     want_out, want_und = _expected(w)
     assert set(zip(g["outliers"]["replica"].tolist(), g["outliers"]["chunk"].tolist())) == want_out
     assert set(g["undecided"].tolist()) == want_und
+    if k == 1:
+        # the workload's stated answer: replica 2, the chunk of the flipped element
+        f = w.faults[0]
+        assert [(int(c), int(r)) for c, r in zip(g["outliers"]["chunk"], g["outliers"]["replica"])] \
+            == [(f.byte_offset // w.chunk_bytes, 2)]
     # signature equality <=> byte equality with replica 0, every chunk
     bases = _chunk_bases(w.metas, w.chunk_bytes)
     for r in range(1, w.R):
@@ -631,18 +667,27 @@ def test_full_config_parity(k):
                 eq.append(bool(torch.equal(a[nfull * w.chunk_bytes:], b[nfull * w.chunk_bytes:])))
             same[int(bases[t]): int(bases[t + 1])] = eq
         assert np.array_equal(same, g["records"]["sig"][r] == g["records"]["sig"][0]), r
-    # sampled chunks against the oracle, all replicas
-    rng = np.random.default_rng(1000 + k)
-    sample = sorted({c for _, c in want_out} | set(want_und) | {0, C - 1} |
-                    set(rng.integers(0, C, 12).tolist()))
-    for c in sample:
-        t, kk, lo, hi = _chunk_range(w, c)
-        d, shape = w.metas[t]
-        for r in range(w.R):
-            data = w.replicas[r][t].view(-1).view(torch.uint8)[lo:hi].cpu().numpy()
-            ref = oracle.chunk_signature(data, d, shape, kk)
-            compare_record(g["records"][r, c], ref, where=f"replica {r} chunk {c}")
-    del w, g
+    # every record of every replica against the oracle
+    print("CASE full config", k, "oracle over", w.total_bytes, "bytes", flush=True)
+    ref = _oracle_records_streamed(w)
+    compare_all_records(g["records"], ref)
+    # votes and lists against the oracle's on the oracle's own records
+    ost, obm, omj = oracle.vote_exact(ref["sig"])
+    assert np.array_equal(g["status"], ost) and np.array_equal(g["bitmap"], obm)
+    assert np.array_equal(g["maj"], omj)
+    loc = oracle.localize(ost, obm, omj, w.R)
+    assert g["counts"].tolist() == loc["counts"].tolist()
+    assert g["outliers"]["chunk"].tolist() == loc["unit"].tolist()
+    assert g["outliers"]["replica"].tolist() == loc["replica"].tolist()
+    assert g["outliers"]["majority_replica"].tolist() == loc["majority"].tolist()
+    assert g["undecided"].tolist() == loc["undecided"].tolist()
+    for i, (c, r, m) in enumerate(zip(loc["unit"], loc["replica"], loc["majority"])):
+        o = g["outliers"][i]
+        for z, rr in ((0, r), (1, m)):
+            assert int(o["nan_count"][z]) == int(ref["nan"][rr, c])
+            assert int(o["inf_count"][z]) == int(ref["inf"][rr, c])
+            assert float(o["absmax"][z]) == float(ref["absmax"][rr, c])
+    del w, g, ref
     torch.cuda.empty_cache()
 
 
