@@ -1,7 +1,6 @@
-"""Builds libc3.so, the gfx950 HIP library behind include/c3.h,
+"""Builds libc3.so, the gfx950 HIP library behind include/c3.h, and
 libc3_oob.so, the host-only hang-localization library behind
-include/c3_oob.h (g++, no HIP: observer processes never touch a GPU), and
-c3_abi_client, a plain C program that uses libc3.so through the C ABI only.
+include/c3_oob.h (g++, no HIP: observer processes never touch a GPU).
 
 hipcc compiles every source of csrc/ for gfx950 only:
   -O3, no floating-point contraction (the statistical vote and the AdamW
@@ -51,30 +50,6 @@ def build_oob(verbose: bool = False) -> str:
     return OOB_LIB
 
 
-ABI_CLIENT_SRC = os.path.join(HERE, "..", "tests", "c_abi_client.c")
-ABI_CLIENT = os.path.join(HERE, "c3_abi_client")
-CC = os.environ.get("CC", "gcc")
-ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
-
-
-def build_abi_client(verbose: bool = False):
-    """A plain C client of libc3.so (C99, gcc, no HIP compiler), linked next
-    to the library; the GPU tests run it.  Skipped when the test sources are
-    not present."""
-    if not os.path.exists(ABI_CLIENT_SRC):
-        return None
-    cmd = [CC, "-std=c99", "-O2", "-Wall", "-Wextra", "-Werror", "-D__HIP_PLATFORM_AMD__",
-           "-I", os.path.join(ROCM, "include"), "-I", os.path.join(HERE, "..", "include"),
-           ABI_CLIENT_SRC, "-o", ABI_CLIENT + ".tmp", "-L", HERE, "-lc3",
-           "-L", os.path.join(ROCM, "lib"), "-lamdhip64", "-lm",
-           "-Wl,-rpath,$ORIGIN", "-Wl,-rpath," + os.path.join(ROCM, "lib")]
-    if verbose:
-        print(" ".join(cmd), flush=True)
-    subprocess.run(cmd, check=True)
-    os.replace(ABI_CLIENT + ".tmp", ABI_CLIENT)
-    return ABI_CLIENT
-
-
 def build(verbose: bool = False, extra=None) -> str:
     cmd = [HIPCC] + FLAGS + (extra or []) + ["-I", os.path.join(HERE, "..", "include")] + \
         sources() + ["-o", LIB + ".tmp"]
@@ -83,7 +58,6 @@ def build(verbose: bool = False, extra=None) -> str:
     subprocess.run(cmd, check=True)
     os.replace(LIB + ".tmp", LIB)
     build_oob(verbose)
-    build_abi_client(verbose)
     return LIB
 
 
