@@ -1,14 +1,19 @@
 """Benchmark of the C3 hot path on one MI355X.
 
-One step = c3_signature + c3_consensus (exact, on the signatures) +
-c3_localize over R replica copies resident in HBM.  Default workload: R = 8
+One step = c3_check: signature, exact vote on the signatures and
+localization over R replica copies resident in HBM, in one call (the line
+also reports the same outputs from the three separate calls c3_signature +
+c3_consensus + c3_localize).  Default workload: R = 8
 replicas of 1,073,807,360 bf16 parameters in layer-shaped tensors (16 layers
 of a 2048/8192 transformer), chunk 1 MiB, with seeded faults on one replica.
 
 Prints ONE JSON line on stdout (progress goes to stderr):
   value      replica GB/s fingerprinted + localized (R * S bytes / step time)
   roofline   the streaming signature kernel against MI355X HBM peak, timed
-             with HIP events the library records around that kernel
+             with HIP events the library records around that kernel, and
+             the read probe of the same access pattern as "achievable"
+  parity     the oracle's records, votes and lists of the CPU sample
+             against the GPU's
   cpu_baseline  the CPU oracle (single thread) on a bounded sample
 
 Flags: --gpus N (only 1: the path runs on one GPU), --steps K, --warmup W
@@ -209,36 +214,50 @@ def main():
     torch.cuda.synchronize()
     total = w.total_bytes
     plan = c3.SignaturePlan(w.replicas, w.chunk_bytes, args.tile)
-    rec = plan.new_records()
-    ws = plan.new_workspace()
     C = plan.C
-    status = torch.empty(C, dtype=torch.uint8, device=dev)
-    bitmap = torch.empty(C, dtype=torch.int64, device=dev)
-    maj = torch.empty(C, dtype=torch.int32, device=dev)
-    outl = torch.empty((C * w.R, 80), dtype=torch.uint8, device=dev)
-    und = torch.empty(C, dtype=torch.int64, device=dev)
-    cnt = torch.empty(3, dtype=torch.int64, device=dev)
+    outs = plan.new_check_outputs()
+    rec, status, bitmap, maj, outl, und, cnt = outs
+    cws = torch.empty(plan.check_workspace_size(), dtype=torch.uint8, device=dev)
+    ws = plan.new_workspace()
     lws = torch.empty(c3.localize_workspace_size(C), dtype=torch.uint8, device=dev)
 
     def step(staged=False):
+        # c3_check: signature, exact vote and localization in one call
+        plan.run_check(outs, cws, grid_blocks=args.grid, plan_staged=staged)
+
+    def step_three_calls(staged=False):
+        # the same outputs from c3_signature + c3_consensus + c3_localize
         plan.run(rec, ws, grid_blocks=args.grid, plan_staged=staged)
         c3.consensus(rec, c3.EXACT, out=(status, bitmap, maj))
         c3.localize(status, bitmap, maj, rec, out=(outl, und, cnt), workspace=lws)
 
-    def timed(staged):
-        """Mean ms per step over the K steps, the per-step median and
-        minimum (an event between consecutive steps), and the wall time."""
-        evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    def timed(staged, fn=step):
+        """Mean ms per step over K back-to-back steps between one pair of
+        events, and the wall time."""
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
+        e0.record()
+        for _ in range(args.steps):
+            fn(staged)
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / args.steps, time.perf_counter() - t0
+
+    def per_step(fn=step):
+        """Median and minimum ms of single steps: K more steps with an event
+        between consecutive ones.  Each event record idles the GPU a few
+        microseconds, so these include one event; the mean above has none."""
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+        torch.cuda.synchronize()
         evs[0].record()
         for i in range(args.steps):
-            step(staged)
+            fn(False)
             evs[i + 1].record()
         torch.cuda.synchronize()
         per = sorted(evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps))
-        mean = evs[0].elapsed_time(evs[-1]) / args.steps
-        return mean, per[len(per) // 2], per[0], time.perf_counter() - t0
+        return per[len(per) // 2], per[0]
 
     args.warmup = warm_up(torch, step, args.warmup)
     log(f"[bench] warmup {args.warmup} steps")
@@ -246,10 +265,17 @@ def main():
     log(f"[bench] outliers={counts[0]} undecided={counts[1]} attributed_chunks={counts[2]}")
 
     log(f"[bench] timing {args.steps} steps")
-    ms_per_step, step_med, step_min, wall = timed(staged=False)
+    ms_per_step, wall = timed(staged=False)
     value = total / (ms_per_step * 1e-3) / 1e9
+    step_med, step_min = per_step()
     # the same steps when the plan staged by the previous call is reused
-    ms_staged, _, _, _ = timed(staged=True)
+    ms_staged, _ = timed(staged=True)
+    # the three separate calls, for comparison (same outputs)
+    for _ in range(5):
+        step_three_calls()
+    ms_three, _ = timed(staged=False, fn=step_three_calls)
+    med_three, _ = per_step(fn=step_three_calls)
+    step()                       # leave c3_check's outputs for the parity check
 
     # dominant kernel: the streaming signature kernel, events recorded by the
     # library on the launch stream immediately around it
@@ -261,7 +287,7 @@ def main():
         b.record()
     torch.cuda.synchronize()
     for a, b in evs:
-        plan.run(rec, ws, ev_begin=a, ev_end=b, grid_blocks=args.grid)
+        plan.run_check(outs, cws, ev_begin=a, ev_end=b, grid_blocks=args.grid)
     torch.cuda.synchronize()
     k_all = sorted(a.elapsed_time(b) for a, b in evs)
     k_ms = sum(k_all) / len(k_all)
@@ -353,6 +379,10 @@ def main():
         "wall_s_timed": round(wall, 3),
         "ms_per_step_plan_reused": round(ms_staged, 4),
         "value_plan_reused": round(total / (ms_staged * 1e-3) / 1e9, 2),
+        "step": "c3_check (signature + exact vote + localize in one call)",
+        "ms_per_step_three_calls": round(ms_three, 4),
+        "ms_per_step_three_calls_median": round(med_three, 4),
+        "value_three_calls": round(total / (ms_three * 1e-3) / 1e9, 2),
     }
     print(json.dumps(out), flush=True)
 

@@ -16,10 +16,11 @@
  *
  * Common conventions
  *   - Device pointers are plain HIP device addresses owned by the caller.
- *     The library allocates no device memory.  Its only state between calls
- *     is a 2 MiB ring of pinned host memory per device (allocated on first
- *     use, kept until the process ends) through which c3_signature stages
- *     its plan, so that staging never makes the host wait for the GPU.
+ *     The library allocates no device memory.  Its state between calls is
+ *     a 4 MiB ring of pinned host memory per device (allocated on first
+ *     use, kept until the process ends) through which c3_signature and
+ *     c3_check stage their plans, so that staging never makes the host wait
+ *     for the GPU, and the fixed scratch array of c3_localize_noalloc.
  *   - Host arrays passed in (pointer tables, tensor metadata) are consumed
  *     before the call returns; the caller may free them immediately.
  *   - Every call enqueues work on `stream` and returns without waiting; its
@@ -238,6 +239,40 @@ int c3_signature(const void *const *ptrs, const c3_tensor_meta_t *metas, int T, 
 int c3_signature_ex(const void *const *ptrs, const c3_tensor_meta_t *metas, int T, int R,
                     uint64_t chunk_bytes, c3_chunk_record_t *records, void *ws, size_t ws_bytes,
                     c3_stream_t stream, const c3_launch_opts_t *opts);
+
+/* Device workspace bytes c3_check needs for this plan (tile_bytes as in
+ * c3_launch_opts_t; 0 = default).  0 on invalid arguments or R < 2. */
+size_t c3_check_workspace_size(const c3_tensor_meta_t *metas, int T, int R, uint64_t chunk_bytes,
+                               uint64_t tile_bytes);
+
+/*
+ * c3_check -- the whole exact check of Algorithm 1 over R co-resident
+ * replicas in one call: the evidence of every chunk (Sec. 5.2, as
+ * c3_signature), the strict-majority vote of every chunk on the signatures
+ * (Sec. 5.3, as c3_consensus in C3_EXACT mode with replica stride C * 64 and
+ * unit stride 64) and the outlier and undecided lists (Sec. 5.1, as
+ * c3_localize with the records).  Every output is bit-identical to what those
+ * three calls write.
+ *   ptrs, metas, T, chunk_bytes, records  as c3_signature.
+ *   R           2..C3_MAX_PEERS (R = 1: C3_E_INVAL, Sec. 4).
+ *   status, bitmap, majority_idx  device [C], [C][C3_BITMAP_WORDS(R)] u64
+ *               (8-byte aligned), [C] i32 (4-byte aligned), as c3_consensus.
+ *   outliers, out_cap, undecided, und_cap, counts  as c3_localize.
+ *   ws, ws_bytes  device workspace of c3_check_workspace_size(...) bytes,
+ *               256-byte aligned, not used by another call at the same time.
+ *   opts        as c3_signature_ex (may be NULL): the events bracket the
+ *               streaming kernels; C3_OPT_PLAN_STAGED skips staging when a
+ *               previous c3_signature_ex or c3_check call staged the same
+ *               plan into this workspace.
+ * For R <= 16 the tile partials are combined, the chunks voted and (for up
+ * to 8,192 chunks) the lists written by one kernel after the streaming pass;
+ * larger groups run the separate steps.  Errors as the three calls.
+ */
+int c3_check(const void *const *ptrs, const c3_tensor_meta_t *metas, int T, int R,
+             uint64_t chunk_bytes, c3_chunk_record_t *records, uint8_t *status, uint64_t *bitmap,
+             int32_t *majority_idx, c3_outlier_t *outliers, int64_t out_cap, int64_t *undecided,
+             int64_t und_cap, int64_t *counts, void *ws, size_t ws_bytes, c3_stream_t stream,
+             const c3_launch_opts_t *opts);
 
 /*
  * c3_tensor_signature -- one signature per (replica, tensor), the paper's own

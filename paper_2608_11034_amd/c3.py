@@ -7,6 +7,7 @@ the tensors are not on a GPU the functions raise.
 Entry points (same names as the C ABI):
 
 * ``signature(replicas, chunk_bytes)``  -> records [R, C] (64-byte rows)
+* ``check(replicas, chunk_bytes)``      -> records, votes and lists in one call
 * ``tensor_signature(records, T)``       -> per-tensor signatures [R, T]
 * ``consensus(evidence, mode, ...)``     -> status, bitmap, majority index
 * ``localize(status, bitmap, majority_idx, records, R)`` -> lists + counts
@@ -131,6 +132,11 @@ def lib():
         L.c3_signature.argtypes = [vp, vp, i32, i32, u64, vp, vp, sz, vp]
         L.c3_signature_ex.restype = i32
         L.c3_signature_ex.argtypes = [vp, vp, i32, i32, u64, vp, vp, sz, vp, vp]
+        L.c3_check_workspace_size.restype = sz
+        L.c3_check_workspace_size.argtypes = [vp, i32, i32, u64, u64]
+        L.c3_check.restype = i32
+        L.c3_check.argtypes = [vp, vp, i32, i32, u64, vp, vp, vp, vp, vp, i64, vp, i64, vp, vp, sz,
+                               vp, vp]
         L.c3_tensor_signature.restype = i32
         L.c3_tensor_signature.argtypes = [vp, i32, i64, i32, vp, vp]
         L.c3_consensus.restype = i32
@@ -294,6 +300,59 @@ class SignaturePlan:
                                    _stream(stream), ctypes.byref(opts))
         _check(rc, "c3_signature")
         return records
+
+
+    # -- the whole exact check in one call (c3_check) ----------------------
+    def check_workspace_size(self) -> int:
+        n = lib().c3_check_workspace_size(self.metas, self.T, self.R, self.chunk_bytes,
+                                          self.tile_bytes)
+        if n == 0:
+            raise C3Error("invalid check plan")
+        return int(n)
+
+    def new_check_outputs(self, out_cap: int = None, und_cap: int = None):
+        """Device outputs of run_check: records [R, C, 64], status [C], bitmap
+        [C] (or [C, words] above 64 replicas), majority [C], outliers
+        [out_cap, 80], undecided [und_cap], counts [3]."""
+        C, R, dev = self.C, self.R, self.device
+        W = bitmap_words(R)
+        out_cap = C * R if out_cap is None else out_cap
+        und_cap = C if und_cap is None else und_cap
+        return (self.new_records(), _empty((C,), torch.uint8, dev),
+                _empty((C,) if W == 1 else (C, W), torch.int64, dev), _empty((C,), torch.int32, dev),
+                _empty((max(out_cap, 1), 80), torch.uint8, dev), _empty((max(und_cap, 1),), torch.int64, dev),
+                _empty((3,), torch.int64, dev))
+
+    def run_check(self, outputs, workspace, stream=None, ev_begin=None, ev_end=None,
+                  grid_blocks=0, plan_staged=False, out_cap: int = None, und_cap: int = None):
+        """Launch c3_check into `outputs` (as new_check_outputs returns them)."""
+        rec, st, bm, mj, outl, und, cnt = outputs
+        C, R = self.C, self.R
+        _check_out(rec, torch.uint8, R * C * 64, "records")
+        _check_out(st, torch.uint8, C, "status")
+        _check_out(bm, torch.int64, C * bitmap_words(R), "bitmap")
+        _check_out(mj, torch.int32, C, "majority")
+        _check_out(cnt, torch.int64, 3, "counts")
+        out_cap = outl.shape[0] if out_cap is None else min(out_cap, outl.shape[0])
+        und_cap = und.numel() if und_cap is None else min(und_cap, und.numel())
+        opts = LaunchOpts(ev_begin.cuda_event if ev_begin is not None else None,
+                          ev_end.cuda_event if ev_end is not None else None,
+                          int(grid_blocks), OPT_PLAN_STAGED if plan_staged else 0,
+                          self.tile_bytes)
+        rc = lib().c3_check(self.ptrs, self.metas, self.T, R, self.chunk_bytes, _ptr(rec), _ptr(st),
+                            _ptr(bm), _ptr(mj), _ptr(outl), out_cap, _ptr(und), und_cap, _ptr(cnt),
+                            _ptr(workspace), workspace.numel(), _stream(stream), ctypes.byref(opts))
+        _check(rc, "c3_check")
+        return outputs
+
+
+def check(replicas, chunk_bytes: int, stream=None, tile_bytes: int = 0):
+    """c3_check: records, status, bitmap, majority, outliers, undecided and
+    counts of R replica lists of T device tensors, in one call."""
+    plan = SignaturePlan(replicas, chunk_bytes, tile_bytes)
+    outs = plan.new_check_outputs()
+    ws = _empty((plan.check_workspace_size(),), torch.uint8, plan.device)
+    return plan.run_check(outs, ws, stream=stream)
 
 
 def signature(replicas, chunk_bytes: int, stream=None, grid_blocks: int = 0, tile_bytes: int = 0):

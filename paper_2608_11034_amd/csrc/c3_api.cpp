@@ -5,9 +5,12 @@
 #include <math.h>
 #include <string.h>
 
+#include <algorithm>
 #include <atomic>
+#include <chrono>
 #include <functional>
 #include <mutex>
+#include <thread>
 #include <vector>
 
 #include "c3_internal.h"
@@ -140,6 +143,8 @@ int make_plan(const c3_tensor_meta_t* metas, int T, int R, uint64_t chunk_bytes,
     off = align_up(off + 4ull * (uint64_t)T, 256);
     h.off_gtile = off;
     off = align_up(off + 8ull * (uint64_t)(T + 1), 256);
+    h.off_chunk_tensor = off;
+    off = align_up(off + 4ull * (uint64_t)h.C, 256);
     h.off_partials = off;
     if (!h.direct) off += sizeof(c3::TilePartial) * (uint64_t)h.tiles_per_replica * (uint64_t)R;
     h.total_bytes = align_up(off, 256);
@@ -151,15 +156,19 @@ inline bool aligned(const void* p, uintptr_t a) { return ((uintptr_t)p & (a - 1)
 // ---------------------------------------------------------------------------
 // Plan staging.  A copy from pageable host memory makes the host wait for the
 // stream before it returns, and a copy-engine transfer costs a cross-engine
-// synchronization on each side.  Plans are therefore written into a small
-// ring of pinned host slots per device (allocated on first use, kept until
-// the process ends) and pulled into the workspace by a kernel on the caller's
-// stream; a slot is reused only after the kernel that read it has completed.
-// Plans larger than a slot (256 KB, about 1,500 tensors at R = 8) fall back
-// to a pageable copy.  The buffer holds whole 16-byte words, so the
-// staged size is rounded up to 16.
+// synchronization on each side.  Plans are therefore written into a ring of
+// pinned host slots per device (allocated on first use, kept until the
+// process ends) and pulled into the workspace by a kernel on the caller's
+// stream.  A slot is reused only after the kernel that read it has
+// completed: the plan fetch kernel stores the slot's sequence number into a
+// pinned coherent word when it is done, which costs nothing on the stream
+// (an event recorded per call idled the GPU about 6 us per call); kernels
+// that copy a plan as a side job (the optimizer check's replay) record an
+// event instead.  A plan larger than a slot (256 KB, about 1,500 tensors at
+// R = 8) falls back to a pageable copy.  The buffer
+// holds whole 16-byte words, so the staged size is rounded up to 16.
 // ---------------------------------------------------------------------------
-constexpr int kStageSlots = 8;
+constexpr int kStageSlots = 16;
 constexpr size_t kStageSlotBytes = 256 * 1024;
 constexpr int kMaxDevices = 64;
 
@@ -168,35 +177,48 @@ struct Stager {
     bool ready = false;
     bool failed = false;
     unsigned char* host = nullptr;
+    uint64_t* seen = nullptr;                 // [kStageSlots][kFetchBlocks], written by the fetch kernel
+    uint64_t issued[kStageSlots] = {};        // sequence of the last fetch from each slot
+    int blocks[kStageSlots] = {};             // its workgroups, each of which signals
     hipEvent_t ev[kStageSlots] = {};
-    bool pending[kStageSlots] = {};
+    bool ev_pending[kStageSlots] = {};
+    uint64_t seq = 0;
     int next = 0;
 };
 
 Stager g_stagers[kMaxDevices];
 
 // Copies `bytes` of `src` to device `dst` on `s`; returns a HIP error code.
-// `enqueue(h)` launches the kernel that copies the staged bytes from the
-// pinned slot h to dst (with whatever else it does); when staging falls back
-// to a pageable copy, that copy is enqueued first and enqueue(nullptr)
-// after it.
+// `enqueue(h, seen, seq)` launches the kernel that copies the staged bytes
+// from the pinned slot h to dst (with whatever else it does); if it can
+// store `seq` into `seen` when done (plan_fetch_kernel) it returns true in
+// `signals`, else an event marks the slot.  When staging falls back to a
+// pageable copy, that copy is enqueued first and enqueue(nullptr, ...) after
+// it.
+using Enqueue = std::function<hipError_t(const void*, uint64_t*, uint64_t, bool&)>;
+
 hipError_t stage_to_device(void* dst, const void* src, size_t bytes, hipStream_t s,
-                           const std::function<hipError_t(const void*)>& enqueue) {
+                           const Enqueue& enqueue) {
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return e;
+    bool unused = false;
     auto pageable = [&]() {
         hipError_t e2 = hipMemcpyAsync(dst, src, bytes, hipMemcpyHostToDevice, s);
-        return e2 != hipSuccess ? e2 : enqueue(nullptr);
+        return e2 != hipSuccess ? e2 : enqueue(nullptr, nullptr, 0, unused);
     };
     if (dev < 0 || dev >= kMaxDevices || bytes > kStageSlotBytes) return pageable();
     Stager& st = g_stagers[dev];
     std::lock_guard<std::mutex> lock(st.mu);
     if (!st.ready && !st.failed) {
         if (hipHostMalloc(reinterpret_cast<void**>(&st.host), kStageSlots * kStageSlotBytes,
-                          hipHostMallocDefault) != hipSuccess) {
+                          hipHostMallocDefault) != hipSuccess ||
+            hipHostMalloc(reinterpret_cast<void**>(&st.seen),
+                          kStageSlots * c3::kFetchBlocks * sizeof(uint64_t),
+                          hipHostMallocCoherent) != hipSuccess) {
             st.failed = true;
         } else {
+            for (int i = 0; i < kStageSlots * c3::kFetchBlocks; ++i) st.seen[i] = 0;
             for (int i = 0; i < kStageSlots && !st.failed; ++i)
                 if (hipEventCreateWithFlags(&st.ev[i], hipEventDisableTiming) != hipSuccess)
                     st.failed = true;
@@ -205,20 +227,55 @@ hipError_t stage_to_device(void* dst, const void* src, size_t bytes, hipStream_t
     }
     if (!st.ready) return pageable();
     const int slot = st.next;
+    if (st.ev_pending[slot]) {
+        if ((e = hipEventSynchronize(st.ev[slot])) != hipSuccess) return e;
+        st.ev_pending[slot] = false;
+    }
+    // The fetch from this slot kStageSlots calls ago may still be queued
+    // when the host runs far ahead of the GPU: wait for it, which keeps the
+    // host that many calls ahead (a pageable copy instead would wait for the
+    // whole stream and leave the GPU idle between calls).  After a minute
+    // without progress the pageable copy is taken after all.
+    uint64_t* seen = st.seen + (size_t)slot * c3::kFetchBlocks;
+    auto consumed = [&]() {
+        for (int b = 0; b < st.blocks[slot]; ++b)
+            if (__atomic_load_n(&seen[b], __ATOMIC_ACQUIRE) < st.issued[slot]) return false;
+        return true;
+    };
+    if (!consumed()) {
+        const auto t0 = std::chrono::steady_clock::now();
+        unsigned nap = 1;
+        while (!consumed()) {
+            if (std::chrono::steady_clock::now() - t0 > std::chrono::seconds(60)) return pageable();
+            std::this_thread::sleep_for(std::chrono::microseconds(nap));
+            if (nap < 256) nap *= 2;
+        }
+    }
     st.next = (st.next + 1) % kStageSlots;
-    if (st.pending[slot] && (e = hipEventSynchronize(st.ev[slot])) != hipSuccess) return e;
     unsigned char* h = st.host + (size_t)slot * kStageSlotBytes;
     memcpy(h, src, bytes);
-    if ((e = enqueue(h)) != hipSuccess) return e;
-    if ((e = hipEventRecord(st.ev[slot], s)) != hipSuccess) return e;
-    st.pending[slot] = true;
+    const uint64_t seq = ++st.seq;
+    bool signals = false;
+    if ((e = enqueue(h, seen, seq, signals)) != hipSuccess) return e;
+    if (signals) {
+        st.issued[slot] = seq;
+        st.blocks[slot] = c3::plan_fetch_blocks(bytes);
+    } else {
+        st.issued[slot] = 0;
+        st.blocks[slot] = 0;
+        if ((e = hipEventRecord(st.ev[slot], s)) != hipSuccess) return e;
+        st.ev_pending[slot] = true;
+    }
     return hipSuccess;
 }
 
 hipError_t stage_to_device(void* dst, const void* src, size_t bytes, hipStream_t s) {
-    return stage_to_device(dst, src, bytes, s, [&](const void* h) {
-        return h != nullptr ? c3::launch_plan_fetch(h, dst, bytes, s) : hipSuccess;
-    });
+    return stage_to_device(dst, src, bytes, s,
+                           [&](const void* h, uint64_t* seen, uint64_t seq, bool& signals) {
+                               if (h == nullptr) return hipSuccess;
+                               signals = true;
+                               return c3::launch_plan_fetch(h, dst, bytes, s, seen, seq);
+                           });
 }
 
 }  // namespace
@@ -289,6 +346,9 @@ int prepare_signature(const void* const* ptrs, const c3_tensor_meta_t* metas, in
     memcpy(buf.data() + p.h.off_tmeta, p.tinfo.data(), sizeof(TensorInfo) * (size_t)T);
     memcpy(buf.data() + p.h.off_order, p.order.data(), 4ull * T);
     memcpy(buf.data() + p.h.off_gtile, p.gtile.data(), 8ull * (T + 1));
+    int32_t* ct = reinterpret_cast<int32_t*>(buf.data() + p.h.off_chunk_tensor);
+    for (int t = 0; t < T; ++t)
+        for (int64_t c = p.chunk_base[t]; c < p.chunk_base[t + 1]; ++c) ct[c] = t;
     return C3_OK;
 }
 
@@ -376,6 +436,76 @@ int c3_signature(const void* const* ptrs, const c3_tensor_meta_t* metas, int T, 
                  uint64_t chunk_bytes, c3_chunk_record_t* records, void* ws, size_t ws_bytes,
                  c3_stream_t stream) {
     return c3_signature_ex(ptrs, metas, T, R, chunk_bytes, records, ws, ws_bytes, stream, nullptr);
+}
+
+}  // extern "C"
+
+// c3_check's workspace: the signature plan and partials, then the lists'
+// staging area (fused tail) or the localization workspace.
+static uint64_t check_ws_bytes(const SigPlan& h, int R) {
+    return align_up(h.total_bytes, 256) +
+           std::max<uint64_t>(align_up(c3::localize_ws_bytes(h.C), 256),
+                              c3::check_stage_bytes(R, h.C));
+}
+
+extern "C" {
+
+size_t c3_check_workspace_size(const c3_tensor_meta_t* metas, int T, int R, uint64_t chunk_bytes,
+                               uint64_t tile_bytes) {
+    Plan p;
+    if (make_plan(metas, T, R, chunk_bytes, tile_bytes, p) != C3_OK || R < 2) return 0;
+    return (size_t)check_ws_bytes(p.h, R);
+}
+
+int c3_check(const void* const* ptrs, const c3_tensor_meta_t* metas, int T, int R,
+             uint64_t chunk_bytes, c3_chunk_record_t* records, uint8_t* status, uint64_t* bitmap,
+             int32_t* majority_idx, c3_outlier_t* outliers, int64_t out_cap, int64_t* undecided,
+             int64_t und_cap, int64_t* counts, void* ws, size_t ws_bytes, c3_stream_t stream,
+             const c3_launch_opts_t* opts) {
+    if (R < 2) return C3_E_INVAL;  // a singleton group provides no comparison (Sec. 4)
+    const uint64_t tile = opts ? opts->tile_bytes : 0;
+    Plan p;
+    std::vector<unsigned char> buf;
+    // the signature's checks and plan; its workspace is the front of ws
+    int rc = prepare_signature(ptrs, metas, T, R, chunk_bytes, records, ws, ws_bytes, tile, p, buf);
+    if (rc != C3_OK) return rc;
+    const uint64_t sig_ws = align_up(p.h.total_bytes, 256);
+    if (ws_bytes < check_ws_bytes(p.h, R)) return C3_E_WORKSPACE;
+    if (status == nullptr || bitmap == nullptr || majority_idx == nullptr) return C3_E_INVAL;
+    if (!aligned(bitmap, 8) || !aligned(majority_idx, 4)) return C3_E_ALIGN;
+    rc = c3::localize_check(status, bitmap, majority_idx, records, R, p.h.C, outliers, out_cap,
+                            undecided, und_cap, counts);
+    if (rc != C3_OK) return rc;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    const bool staged = opts != nullptr && (opts->flags & C3_OPT_PLAN_STAGED) != 0;
+    if (!staged && stage_to_device(ws, buf.data(), buf.size(), s) != hipSuccess) return C3_E_HIP;
+    const SigPlan* dplan = static_cast<const SigPlan*>(ws);
+    // Up to 16 replicas: the streaming kernels, then one tail kernel that
+    // combines partials, votes and (for up to 8,192 chunks) lists in its
+    // last workgroup.  Larger groups: the separate steps.
+    const bool fused = c3::check_group_bound(R) != 0;
+    hipError_t e = c3::launch_signature(
+        dplan, p.h, p.groups, records, opts ? opts->grid_blocks : 0, !fused, s,
+        opts ? reinterpret_cast<hipEvent_t>(opts->ev_kernel_begin) : nullptr,
+        opts ? reinterpret_cast<hipEvent_t>(opts->ev_kernel_end) : nullptr);
+    if (e != hipSuccess) return C3_E_HIP;
+    void* lws = static_cast<unsigned char*>(ws) + sig_ws;
+    if (fused) {
+        const bool lists = c3::check_stage_bytes(R, p.h.C) != 0;
+        e = c3::launch_check_tail(dplan, p.h, records, status, bitmap, majority_idx, outliers,
+                                  out_cap, undecided, und_cap, counts, lists ? lws : nullptr, s);
+        if (e == hipSuccess && !lists)
+            e = c3::launch_localize(status, bitmap, majority_idx, records, R, p.h.C, outliers,
+                                    out_cap, undecided, und_cap, counts, lws, s);
+    } else {
+        e = c3::launch_consensus(&records[0].sig, C3_EV_U64, p.h.C * (int64_t)sizeof(c3_chunk_record_t),
+                                 (int64_t)sizeof(c3_chunk_record_t), R, p.h.C, C3_EXACT, 1.0, status,
+                                 bitmap, majority_idx, s);
+        if (e == hipSuccess)
+            e = c3::launch_localize(status, bitmap, majority_idx, records, R, p.h.C, outliers,
+                                    out_cap, undecided, und_cap, counts, lws, s);
+    }
+    return e == hipSuccess ? C3_OK : C3_E_HIP;
 }
 
 int c3_tensor_signature(const c3_chunk_record_t* records, int R, int64_t C, int T, uint64_t* out,
@@ -582,7 +712,9 @@ int c3_optimizer_check(const c3_optimizer_state_t* st, int64_t k, const c3_adamw
     // plan into the workspace; the streaming signature kernel; one workgroup
     // that combines tile partials into records, votes and writes the lists.
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    hipError_t e = stage_to_device(ws, buf.data(), buf.size(), s, [&](const void* h) {
+    hipError_t e = stage_to_device(ws, buf.data(), buf.size(), s,
+                                   [&](const void* h, uint64_t*, uint64_t, bool& signals) {
+        signals = false;
         return c3::launch_adamw_slice(aptrs, ac, R, vec4, off, n, out->updated, S, s, h,
                                       h != nullptr ? ws : nullptr, h != nullptr ? buf.size() : 0);
     });

@@ -31,9 +31,27 @@ hipError_t launch_small_tail(const SigPlan* dplan, c3_chunk_record_t* records, u
                              int64_t out_cap, int64_t* undecided, int64_t und_cap, int64_t* counts,
                              hipStream_t stream);
 
+// Tail of c3_check for R <= 16 (check_group_bound(R) != 0): records from
+// partials and exact votes in one kernel; with stage_ws (check_stage_bytes(R,
+// C) bytes, 256-byte aligned; C up to 8,192) also the lists of c3_localize,
+// staged per segment by that kernel and placed by a one-workgroup kernel.
+int check_group_bound(int R);
+uint64_t check_stage_bytes(int R, int64_t C);
+hipError_t launch_check_tail(const SigPlan* dplan, const SigPlan& hplan, c3_chunk_record_t* records,
+                             uint8_t* status, uint64_t* bitmap, int32_t* majority,
+                             c3_outlier_t* outliers, int64_t out_cap, int64_t* undecided,
+                             int64_t und_cap, int64_t* counts, void* stage_ws,
+                             hipStream_t stream);
+
 // Copies `bytes` (rounded up to 16) from pinned, device-visible host memory
-// to device memory with a kernel on `stream`.
-hipError_t launch_plan_fetch(const void* host_src, void* dst, size_t bytes, hipStream_t stream);
+// to device memory with a kernel of plan_fetch_blocks(bytes) workgroups on
+// `stream`; with `seen` (pinned coherent host memory, kFetchBlocks words)
+// workgroup b then stores `seq` into seen[b], which tells the host that its
+// part of the source may be reused.
+constexpr int kFetchBlocks = 32;
+int plan_fetch_blocks(size_t bytes);
+hipError_t launch_plan_fetch(const void* host_src, void* dst, size_t bytes, hipStream_t stream,
+                             uint64_t* seen = nullptr, uint64_t seq = 0);
 
 hipError_t launch_tensor_signature(const c3_chunk_record_t* records, int R, int64_t C, int T,
                                    uint64_t* out, hipStream_t stream);

@@ -18,6 +18,7 @@
 
 #include "c3_device.h"
 #include "c3_internal.h"
+#include "c3_localize_block.h"
 
 namespace c3 {
 
@@ -28,13 +29,6 @@ constexpr int64_t kSegUnits = (int64_t)kLocThreads * kPerThread;
 struct SegCount {
     int64_t n_out, n_und, n_att;
 };
-
-// Set bits of unit u's bitmap.
-__device__ inline int unit_popcount(const uint64_t* bitmap, int W, int64_t u) {
-    int n = 0;
-    for (int w = 0; w < W; ++w) n += __builtin_popcountll(bitmap[u * W + w]);
-    return n;
-}
 
 __device__ inline void thread_counts(const uint8_t* status, const uint64_t* bitmap, int W,
                                      int64_t u0, int64_t n_units, int64_t& o, int64_t& un,
@@ -56,28 +50,6 @@ __device__ inline void thread_counts(const uint8_t* status, const uint64_t* bitm
     }
 }
 
-// Inclusive prefix sum over the NT threads of a workgroup (fixed order).
-template <int NT = kLocThreads>
-__device__ inline int64_t block_inclusive_scan(int64_t v, int64_t* lds_wave, int64_t& total) {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    int64_t x = v;
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        const int64_t y = (int64_t)shfl_u64((uint64_t)x, lane >= d ? lane - d : lane);
-        if (lane >= d) x += y;
-    }
-    if (lane == 63) lds_wave[wave] = x;
-    __syncthreads();
-    int64_t before = 0;
-    total = 0;
-    for (int w = 0; w < NT / 64; ++w) {
-        if (w < wave) before += lds_wave[w];
-        total += lds_wave[w];
-    }
-    __syncthreads();
-    return x + before;
-}
-
 __global__ void __launch_bounds__(kLocThreads) localize_count_kernel(
     const uint8_t* __restrict__ status, const uint64_t* __restrict__ bitmap, int W,
     int64_t n_units, SegCount* __restrict__ seg) {
@@ -86,9 +58,9 @@ __global__ void __launch_bounds__(kLocThreads) localize_count_kernel(
     int64_t o, un, at;
     thread_counts(status, bitmap, W, u0, n_units, o, un, at);
     int64_t to, tu, ta;
-    block_inclusive_scan(o, lds[0], to);
-    block_inclusive_scan(un, lds[1], tu);
-    block_inclusive_scan(at, lds[2], ta);
+    block_inclusive_scan<kLocThreads>(o, lds[0], to);
+    block_inclusive_scan<kLocThreads>(un, lds[1], tu);
+    block_inclusive_scan<kLocThreads>(at, lds[2], ta);
     if (threadIdx.x == 0) seg[blockIdx.x] = SegCount{to, tu, ta};
 }
 
@@ -102,9 +74,9 @@ __global__ void __launch_bounds__(kLocThreads) localize_scan_kernel(SegCount* __
         const int64_t s = base + threadIdx.x;
         SegCount c = s < n_seg ? seg[s] : SegCount{0, 0, 0};
         int64_t to, tu, ta;
-        const int64_t io = block_inclusive_scan(c.n_out, lds[0], to);
-        const int64_t iu = block_inclusive_scan(c.n_und, lds[1], tu);
-        block_inclusive_scan(c.n_att, lds[2], ta);
+        const int64_t io = block_inclusive_scan<kLocThreads>(c.n_out, lds[0], to);
+        const int64_t iu = block_inclusive_scan<kLocThreads>(c.n_und, lds[1], tu);
+        block_inclusive_scan<kLocThreads>(c.n_att, lds[2], ta);
         if (s < n_seg) seg[s] = SegCount{carry_o + io - c.n_out, carry_u + iu - c.n_und, 0};
         carry_o += to;
         carry_u += tu;
@@ -125,35 +97,6 @@ __device__ inline void emit_units(const uint8_t* __restrict__ status,
                                   c3_outlier_t* __restrict__ outliers, int64_t out_cap,
                                   int64_t* __restrict__ undecided, int64_t und_cap);
 
-// One outlier entry: unit, replica, majority replica and both summaries
-// (zeros when no record table is given).
-__device__ inline void write_outlier(c3_outlier_t* dst, int64_t u, int r, int32_t mj,
-                                     const c3_chunk_record_t* __restrict__ records, int R,
-                                     int64_t n_units) {
-    c3_outlier_t e;
-    e.chunk = u;
-    e.replica = r;
-    e.majority_replica = mj;
-    for (int z = 0; z < 2; ++z) {
-        const int rr = z == 0 ? r : mj;
-        if (records != nullptr && rr >= 0 && rr < R) {
-            const c3_chunk_record_t& rec = records[(int64_t)rr * n_units + u];
-            e.nan_count[z] = rec.nan_count;
-            e.inf_count[z] = rec.inf_count;
-            e.absmax[z] = rec.absmax;
-            e.sum[z] = rec.sum;
-            e.sumsq[z] = rec.sumsq;
-        } else {
-            e.nan_count[z] = 0;
-            e.inf_count[z] = 0;
-            e.absmax[z] = 0.0;
-            e.sum[z] = 0.0;
-            e.sumsq[z] = 0.0;
-        }
-    }
-    *dst = e;
-}
-
 __global__ void __launch_bounds__(kLocThreads) localize_emit_kernel(
     const uint8_t* __restrict__ status, const uint64_t* __restrict__ bitmap,
     const int32_t* __restrict__ majority_idx, const c3_chunk_record_t* __restrict__ records, int R,
@@ -164,8 +107,8 @@ __global__ void __launch_bounds__(kLocThreads) localize_emit_kernel(
     int64_t o, un, at;
     thread_counts(status, bitmap, W, u0, n_units, o, un, at);
     int64_t to, tu;
-    int64_t po = block_inclusive_scan(o, lds[0], to) - o + seg[blockIdx.x].n_out;
-    int64_t pu = block_inclusive_scan(un, lds[1], tu) - un + seg[blockIdx.x].n_und;
+    int64_t po = block_inclusive_scan<kLocThreads>(o, lds[0], to) - o + seg[blockIdx.x].n_out;
+    int64_t pu = block_inclusive_scan<kLocThreads>(un, lds[1], tu) - un + seg[blockIdx.x].n_und;
     emit_units(status, bitmap, majority_idx, records, R, W, n_units, u0, po, pu, outliers, out_cap,
                undecided, und_cap);
 }
@@ -200,26 +143,11 @@ __device__ inline void emit_units(const uint8_t* __restrict__ status,
     }
 }
 
-// Small inputs: one workgroup of kSingleThreads walks the units in rounds of
-// kSingleThreads * kSinglePerThread, carrying list offsets between rounds.  One
-// launch instead of three.  Each thread loads its kSinglePerThread units
-// once (one-word bitmaps stay in registers; wider ones are counted on load
-// and read again to emit); the three per-thread counts travel through a
-// single scan packed into one 64-bit word: outliers in the low 24 bits (a
-// round holds at most 1024 * 4 units * 256 replicas = 2^20), undecided and
-// attributed units in 20 bits each (at most 2^12 per round), so no field
-// overflows.
+// Small inputs: one workgroup of kSingleThreads (localize_block, shared with
+// the fused check) walks the units in rounds, one launch instead of three.
 constexpr int kSingleThreads = 1024;
 constexpr int kSinglePerThread = 4;  // 8 spilled registers at this block size
 constexpr int64_t kSingleMaxUnits = 8 * (int64_t)kSingleThreads * kSinglePerThread;
-constexpr int kOutBits = 24;
-constexpr int kUnitBits = 20;
-constexpr int64_t kOutMask = (1ll << kOutBits) - 1;
-constexpr int64_t kUnitMask = (1ll << kUnitBits) - 1;
-static_assert((int64_t)kSingleThreads * kSinglePerThread * C3_MAX_PEERS <= kOutMask,
-              "outlier field too narrow");
-static_assert((int64_t)kSingleThreads * kSinglePerThread <= kUnitMask, "unit fields too narrow");
-static_assert(kOutBits + 2 * kUnitBits <= 64, "fields exceed one word");
 
 template <bool WIDE>
 __global__ void __launch_bounds__(kSingleThreads) localize_single_kernel(
@@ -227,65 +155,9 @@ __global__ void __launch_bounds__(kSingleThreads) localize_single_kernel(
     const int32_t* __restrict__ majority_idx, const c3_chunk_record_t* __restrict__ records, int R,
     int W, int64_t n_units, c3_outlier_t* __restrict__ outliers, int64_t out_cap,
     int64_t* __restrict__ undecided, int64_t und_cap, int64_t* __restrict__ counts) {
-    __shared__ int64_t lds[kSingleThreads / 64];
-    int64_t carry_o = 0, carry_u = 0, carry_a = 0;
-    for (int64_t base = 0; base < n_units; base += (int64_t)kSingleThreads * kSinglePerThread) {
-        const int64_t u0 = base + (int64_t)threadIdx.x * kSinglePerThread;
-        uint8_t st[kSinglePerThread];
-        uint64_t bm[kSinglePerThread];  // the word (one-word bitmaps) or the set-bit count
-#pragma unroll
-        for (int i = 0; i < kSinglePerThread; ++i) {
-            const int64_t u = u0 + i;
-            st[i] = u < n_units ? status[u] : (uint8_t)C3_AGREE;
-            if constexpr (WIDE)
-                bm[i] = u < n_units ? (uint64_t)unit_popcount(bitmap, W, u) : 0ull;
-            else
-                bm[i] = u < n_units ? bitmap[u] : 0ull;
-        }
-        int64_t o = 0, un = 0, at = 0;
-#pragma unroll
-        for (int i = 0; i < kSinglePerThread; ++i) {
-            if (st[i] == C3_INCONCLUSIVE) {
-                ++un;
-            } else if (bm[i]) {
-                ++at;
-                o += WIDE ? (int64_t)bm[i] : __builtin_popcountll(bm[i]);
-            }
-        }
-        const int64_t packed = o | (un << kOutBits) | (at << (kOutBits + kUnitBits));
-        int64_t tot;
-        const int64_t excl = block_inclusive_scan<kSingleThreads>(packed, lds, tot) - packed;
-        int64_t po = carry_o + (excl & kOutMask);
-        int64_t pu = carry_u + ((excl >> kOutBits) & kUnitMask);
-#pragma unroll
-        for (int i = 0; i < kSinglePerThread; ++i) {
-            const int64_t u = u0 + i;
-            if (st[i] == C3_INCONCLUSIVE) {
-                if (pu < und_cap) undecided[pu] = u;
-                ++pu;
-                continue;
-            }
-            if (!bm[i]) continue;
-            const int32_t mj = majority_idx[u];
-            for (int w = 0; w < (WIDE ? W : 1); ++w) {
-                uint64_t b = WIDE ? bitmap[u * W + w] : bm[i];
-                while (b) {
-                    const int r = 64 * w + __builtin_ctzll(b);
-                    b &= b - 1;
-                    if (po < out_cap) write_outlier(&outliers[po], u, r, mj, records, R, n_units);
-                    ++po;
-                }
-            }
-        }
-        carry_o += tot & kOutMask;
-        carry_u += (tot >> kOutBits) & kUnitMask;
-        carry_a += (tot >> (kOutBits + kUnitBits)) & kUnitMask;
-    }
-    if (threadIdx.x == 0) {
-        counts[0] = carry_o;
-        counts[1] = carry_u;
-        counts[2] = carry_a;
-    }
+    localize_block<WIDE, kSingleThreads, kSinglePerThread>(status, bitmap, majority_idx, records, R,
+                                                           W, n_units, outliers, out_cap,
+                                                           undecided, und_cap, counts);
 }
 
 size_t localize_ws_bytes(int64_t n_units) {

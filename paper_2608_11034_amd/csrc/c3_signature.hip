@@ -36,6 +36,7 @@
 // classifies every element.  Healthy data never takes that path.
 #include "c3_device.h"
 #include "c3_internal.h"
+#include "c3_localize_block.h"
 #include "c3_vote_row.h"
 
 namespace c3 {
@@ -412,7 +413,7 @@ __device__ inline void combine_chunk(const SigPlan* __restrict__ plan, int64_t r
     const int64_t* chunk_base = reinterpret_cast<const int64_t*>(pb + plan->off_chunk_base);
     const TensorInfo* tinfo = reinterpret_cast<const TensorInfo*>(pb + plan->off_tmeta);
     const TilePartial* partials = reinterpret_cast<const TilePartial*>(pb + plan->off_partials);
-    const int t = find_segment(chunk_base, plan->T, c);
+    const int t = reinterpret_cast<const int32_t*>(pb + plan->off_chunk_tensor)[c];
     const uint64_t k = (uint64_t)(c - chunk_base[t]);
     const uint64_t nbytes = tinfo[t].nbytes;
     const int64_t tiles_t = tile_base[t + 1] - tile_base[t];
@@ -537,20 +538,312 @@ hipError_t launch_small_tail(const SigPlan* dplan, c3_chunk_record_t* records, u
     return hipGetLastError();
 }
 
-// Copies the staged plan from pinned host memory into the workspace on the
-// compute queue (no copy engine, so no cross-engine synchronization).
-__global__ void __launch_bounds__(256) plan_fetch_kernel(const u32x4* __restrict__ src,
-                                                         u32x4* __restrict__ dst, int64_t n16) {
-    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n16; i += (int64_t)gridDim.x * 256)
-        dst[i] = src[i];
+// ---------------------------------------------------------------------------
+// Tail of c3_check: the records of every (replica, chunk) from their tile
+// partials (finalize_kernel's combine) or as the streaming kernel wrote
+// them, the exact vote of every chunk (exact_vote_row, the rule of
+// c3_consensus) and the lists of c3_localize, in two launches.
+// check_vote_kernel:
+//   - a workgroup of kCheckThreads threads takes CPB = kCheckThreads / N
+//     consecutive chunks (a segment), one thread per (chunk, replica slot),
+//     so the R records of a chunk are combined in parallel and meet in LDS;
+//   - one thread per chunk votes;
+//   - with a staging area, the first wave scans the segment's outlier and
+//     undecided counts (CPB <= 64 units: one wave) and writes the segment's
+//     entries, summaries taken from the records in LDS, into the segment's
+//     slots of the staging area, with the three counts.
+// check_lists_kernel (one workgroup): scans the segments' counts in segment
+// order and copies every staged entry to its place in the caller's lists.
+// Segments are in chunk order and entries in (chunk, replica) order inside
+// a segment, so the lists come out in c3_localize's order.
+// ---------------------------------------------------------------------------
+constexpr int kCheckThreads = 256;
+constexpr int kCheckMaxListUnits = 8192;   // chunks whose lists go through the staging area
+constexpr int kCheckMaxSegments = kCheckMaxListUnits / (kCheckThreads / 16);
+// per step of 64 segments: outliers < 64 * kCheckThreads * 8 / 2, units <= 64 * 64
+static_assert(64ll * kCheckThreads * 4 < (1ll << 24) && 64 * 64 < (1 << 20), "packed counts");
+
+struct CheckStage {
+    int32_t* seg_counts;      // [n_seg][4]: outliers, undecided, attributed units
+    c3_outlier_t* out;        // [n_seg][out_per_seg]
+    int64_t* und;             // [n_seg][CPB]
+    int32_t out_per_seg;
+    int32_t cpb;
+};
+
+// Inclusive prefix sum over the 64 lanes of a wave.
+__device__ inline uint64_t wave_inclusive_scan(uint64_t x, int lane) {
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const uint64_t y = shfl_u64(x, lane >= d ? lane - d : lane);
+        if (lane >= d) x += y;
+    }
+    return x;
 }
 
-hipError_t launch_plan_fetch(const void* host_src, void* dst, size_t bytes, hipStream_t stream) {
+__device__ inline void outlier_from(c3_outlier_t& o, int64_t u, int r, int mj,
+                                    const c3_chunk_record_t& a, const c3_chunk_record_t& b) {
+    o.chunk = u;
+    o.replica = r;
+    o.majority_replica = mj;
+    o.nan_count[0] = a.nan_count;
+    o.nan_count[1] = b.nan_count;
+    o.inf_count[0] = a.inf_count;
+    o.inf_count[1] = b.inf_count;
+    o.absmax[0] = a.absmax;
+    o.absmax[1] = b.absmax;
+    o.sum[0] = a.sum;
+    o.sum[1] = b.sum;
+    o.sumsq[0] = a.sumsq;
+    o.sumsq[1] = b.sumsq;
+}
+
+template <int N>
+__global__ void __launch_bounds__(kCheckThreads) check_vote_kernel(
+    const SigPlan* __restrict__ plan, c3_chunk_record_t* __restrict__ records,
+    uint8_t* __restrict__ status, uint64_t* __restrict__ bitmap, int32_t* __restrict__ majority,
+    CheckStage stage) {
+    constexpr int CPB = kCheckThreads / N;
+    static_assert(CPB <= 64, "a segment's units must fit one wave");
+    __shared__ c3_chunk_record_t rec[CPB][N];
+    __shared__ UnitVote votes[CPB];
+    const int R = plan->R;
+    const int64_t C = plan->C;
+    const int slot = threadIdx.x % N;
+    const int cu = threadIdx.x / N;
+    const int64_t c = (int64_t)blockIdx.x * CPB + cu;
+    if (slot < R && c < C) {
+        c3_chunk_record_t* dst = &records[(int64_t)slot * C + c];
+        if (plan->direct) {
+            rec[cu][slot] = *dst;
+        } else {
+            c3_chunk_record_t r;
+            combine_chunk(plan, slot, c, &r);
+            *dst = r;
+            rec[cu][slot] = r;
+        }
+    }
+    __syncthreads();
+    if ((int)threadIdx.x < CPB) {
+        const int64_t u = (int64_t)blockIdx.x * CPB + threadIdx.x;
+        if (u < C) {
+            uint64_t e[N];
+#pragma unroll
+            for (int r = 0; r < N; ++r) e[r] = r < R ? rec[threadIdx.x][r].sig : 0ull;
+            const UnitVote v = exact_vote_row<N>(e, R);
+            status[u] = v.status;
+            bitmap[u] = v.bitmap;
+            majority[u] = v.majority;
+            votes[threadIdx.x] = v;
+        }
+    }
+    if (stage.seg_counts == nullptr) return;
+    __syncthreads();
+    if (threadIdx.x < 64) {
+        // this segment's entries, in (chunk, replica) order, into its slots
+        const int lane = threadIdx.x;
+        const int64_t u = (int64_t)blockIdx.x * CPB + lane;
+        const bool valid = lane < CPB && u < C;
+        UnitVote v{0ull, -1, (uint8_t)C3_AGREE};
+        if (valid) v = votes[lane];
+        const uint64_t n_o =
+            valid && v.status != C3_INCONCLUSIVE ? (uint64_t)__builtin_popcountll(v.bitmap) : 0ull;
+        const uint64_t n_u = valid && v.status == C3_INCONCLUSIVE ? 1ull : 0ull;
+        const uint64_t packed = n_o | (n_u << 32);
+        const uint64_t incl = wave_inclusive_scan(packed, lane);
+        uint64_t po = (uint32_t)(incl - packed);
+        const uint64_t pu = (incl - packed) >> 32;
+        c3_outlier_t* so = stage.out + (int64_t)blockIdx.x * stage.out_per_seg;
+        for (uint64_t b = n_o ? v.bitmap : 0ull; b != 0ull; b &= b - 1ull) {
+            const int r = __builtin_ctzll(b);
+            c3_outlier_t o;
+            outlier_from(o, u, r, v.majority, rec[lane][r], rec[lane][v.majority]);
+            so[po++] = o;
+        }
+        if (n_u) stage.und[(int64_t)blockIdx.x * CPB + (int64_t)pu] = u;
+        const uint64_t tot = shfl_u64(incl, 63);
+        const uint64_t n_att = (uint64_t)__builtin_popcountll(ballot64(n_o != 0ull));
+        if (lane == 0) {
+            int32_t* sc = stage.seg_counts + 4 * (int64_t)blockIdx.x;
+            sc[0] = (int32_t)(uint32_t)tot;
+            sc[1] = (int32_t)(tot >> 32);
+            sc[2] = (int32_t)n_att;
+        }
+    }
+}
+
+__global__ void __launch_bounds__(kCheckThreads) check_lists_kernel(
+    CheckStage stage, int n_seg, c3_outlier_t* __restrict__ outliers, int64_t out_cap,
+    int64_t* __restrict__ undecided, int64_t und_cap, int64_t* __restrict__ counts) {
+    __shared__ int64_t seg_off[2][kCheckMaxSegments];
+    __shared__ int32_t seg_n[2][kCheckMaxSegments];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    if (wave == 0) {
+        // segment offsets in segment order: one wave, 64 segments per step,
+        // the three counts packed into one word (outliers 24 bits, undecided
+        // and attributed 20 bits each: a step of 64 segments holds at most
+        // 64 * 256 * 8 outliers and 64 * 64 units)
+        int64_t carry_o = 0, carry_u = 0, carry_a = 0;
+        for (int base = 0; base < n_seg; base += 64) {
+            const int sgi = base + lane;
+            uint64_t o = 0, un = 0, at = 0;
+            if (sgi < n_seg) {
+                const int32_t* sc = stage.seg_counts + 4 * (int64_t)sgi;
+                o = (uint32_t)sc[0];
+                un = (uint32_t)sc[1];
+                at = (uint32_t)sc[2];
+            }
+            const uint64_t packed = o | (un << 24) | (at << 44);
+            const uint64_t incl = wave_inclusive_scan(packed, lane);
+            const uint64_t excl = incl - packed;
+            if (sgi < n_seg) {
+                seg_off[0][sgi] = carry_o + (int64_t)(excl & 0xFFFFFFull);
+                seg_off[1][sgi] = carry_u + (int64_t)((excl >> 24) & 0xFFFFFull);
+                seg_n[0][sgi] = (int32_t)o;
+                seg_n[1][sgi] = (int32_t)un;
+            }
+            const uint64_t tot = shfl_u64(incl, 63);
+            carry_o += (int64_t)(tot & 0xFFFFFFull);
+            carry_u += (int64_t)((tot >> 24) & 0xFFFFFull);
+            carry_a += (int64_t)((tot >> 44) & 0xFFFFFull);
+        }
+        if (lane == 0) {
+            counts[0] = carry_o;
+            counts[1] = carry_u;
+            counts[2] = carry_a;
+        }
+    }
+    __syncthreads();
+    for (int sgi = wave; sgi < n_seg; sgi += kCheckThreads / 64) {
+        const c3_outlier_t* so = stage.out + (int64_t)sgi * stage.out_per_seg;
+        for (int j = lane; j < seg_n[0][sgi]; j += 64) {
+            const int64_t d = seg_off[0][sgi] + j;
+            if (d < out_cap) outliers[d] = so[j];
+        }
+        for (int j = lane; j < seg_n[1][sgi]; j += 64) {
+            const int64_t d = seg_off[1][sgi] + j;
+            if (d < und_cap) undecided[d] = stage.und[(int64_t)sgi * stage.cpb + j];
+        }
+    }
+}
+
+int check_group_bound(int R) { return R <= 4 ? 4 : R <= 8 ? 8 : R <= 16 ? 16 : 0; }
+
+// Staging bytes for the fused lists of C chunks at group bound N (0 when
+// the tail leaves the lists to a separate localization).
+static uint64_t check_stage_parts(int N, int64_t C, uint64_t& cnt_b, uint64_t& out_b,
+                                  uint64_t& und_b, int& out_per_seg) {
+    const int64_t cpb = kCheckThreads / N;
+    const int64_t n_seg = (C + cpb - 1) / cpb;
+    // a strict majority holds more than R / 2 replicas, so a chunk has at
+    // most ceil(R / 2) - 1 < N / 2 outliers
+    out_per_seg = (int)(cpb * (N / 2));
+    cnt_b = (uint64_t)n_seg * 16;
+    out_b = (uint64_t)n_seg * out_per_seg * sizeof(c3_outlier_t);
+    und_b = (uint64_t)n_seg * cpb * 8;
+    return ((cnt_b + 255) / 256 + (out_b + 255) / 256 + (und_b + 255) / 256) * 256;
+}
+
+uint64_t check_stage_bytes(int R, int64_t C) {
+    const int N = check_group_bound(R);
+    if (N == 0 || C > kCheckMaxListUnits) return 0;
+    uint64_t a, b, c;
+    int o;
+    return check_stage_parts(N, C, a, b, c, o);
+}
+
+hipError_t launch_check_tail(const SigPlan* dplan, const SigPlan& hplan, c3_chunk_record_t* records,
+                             uint8_t* status, uint64_t* bitmap, int32_t* majority,
+                             c3_outlier_t* outliers, int64_t out_cap, int64_t* undecided,
+                             int64_t und_cap, int64_t* counts, void* stage_ws,
+                             hipStream_t stream) {
+    const int N = check_group_bound(hplan.R);
+    if (N == 0 || hplan.C <= 0) return hipErrorInvalidValue;
+    const int64_t cpb = kCheckThreads / N;
+    const int64_t blocks = (hplan.C + cpb - 1) / cpb;
+    if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
+    CheckStage st{nullptr, nullptr, nullptr, 0, (int32_t)cpb};
+    if (stage_ws != nullptr) {
+        if (hplan.C > kCheckMaxListUnits) return hipErrorInvalidValue;
+        uint64_t cnt_b, out_b, und_b;
+        check_stage_parts(N, hplan.C, cnt_b, out_b, und_b, st.out_per_seg);
+        unsigned char* w = static_cast<unsigned char*>(stage_ws);
+        st.seg_counts = reinterpret_cast<int32_t*>(w);
+        w += (cnt_b + 255) / 256 * 256;
+        st.out = reinterpret_cast<c3_outlier_t*>(w);
+        w += (out_b + 255) / 256 * 256;
+        st.und = reinterpret_cast<int64_t*>(w);
+    }
+    switch (N) {
+        case 4:
+            hipLaunchKernelGGL(check_vote_kernel<4>, dim3((unsigned)blocks), dim3(kCheckThreads), 0,
+                               stream, dplan, records, status, bitmap, majority, st);
+            break;
+        case 8:
+            hipLaunchKernelGGL(check_vote_kernel<8>, dim3((unsigned)blocks), dim3(kCheckThreads), 0,
+                               stream, dplan, records, status, bitmap, majority, st);
+            break;
+        default:
+            hipLaunchKernelGGL(check_vote_kernel<16>, dim3((unsigned)blocks), dim3(kCheckThreads), 0,
+                               stream, dplan, records, status, bitmap, majority, st);
+            break;
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || stage_ws == nullptr) return e;
+    hipLaunchKernelGGL(check_lists_kernel, dim3(1), dim3(kCheckThreads), 0, stream, st,
+                       (int)blocks, outliers, out_cap, undecided, und_cap, counts);
+    return hipGetLastError();
+}
+
+// Copies the staged plan from pinned host memory into the workspace on the
+// compute queue (no copy engine, so no cross-engine synchronization): up to
+// kFetchBlocks workgroups, four 16-byte loads per thread in flight, so a plan
+// of up to 128 KiB is one round trip over the host link.  With `seen`, thread
+// 0 of workgroup b then stores `seq` into seen[b] (system scope, pinned
+// coherent host memory): every load of that workgroup has completed, since
+// each thread stored what it loaded before the barrier, so the host may
+// reuse the slot once every used word reads `seq`.
+constexpr int kFetchThreads = 256;
+constexpr int kFetchLoads = 4;
+
+__global__ void __launch_bounds__(kFetchThreads) plan_fetch_kernel(const u32x4* __restrict__ src,
+                                                                   u32x4* __restrict__ dst,
+                                                                   int64_t n16, uint64_t* seen,
+                                                                   uint64_t seq) {
+    const int64_t stride = (int64_t)gridDim.x * kFetchThreads;
+    for (int64_t i0 = (int64_t)blockIdx.x * kFetchThreads + threadIdx.x; i0 < n16;
+         i0 += stride * kFetchLoads) {
+        u32x4 v[kFetchLoads];
+#pragma unroll
+        for (int k = 0; k < kFetchLoads; ++k) {
+            const int64_t i = i0 + (int64_t)k * stride;
+            if (i < n16) v[k] = src[i];
+        }
+#pragma unroll
+        for (int k = 0; k < kFetchLoads; ++k) {
+            const int64_t i = i0 + (int64_t)k * stride;
+            if (i < n16) dst[i] = v[k];
+        }
+    }
+    __syncthreads();
+    if (threadIdx.x == 0 && seen != nullptr)
+        __hip_atomic_store(seen + blockIdx.x, seq, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
+int plan_fetch_blocks(size_t bytes) {
     const int64_t n16 = (int64_t)((bytes + 15) / 16);
-    const int64_t blocks = (n16 + 255) / 256 < 64 ? (n16 + 255) / 256 : 64;
-    if (n16 == 0) return hipSuccess;
-    hipLaunchKernelGGL(plan_fetch_kernel, dim3((unsigned)blocks), dim3(256), 0, stream,
-                       static_cast<const u32x4*>(host_src), static_cast<u32x4*>(dst), n16);
+    const int64_t per = (int64_t)kFetchThreads * kFetchLoads;
+    const int64_t b = (n16 + per - 1) / per;
+    return b < 1 ? 1 : b > kFetchBlocks ? kFetchBlocks : (int)b;
+}
+
+hipError_t launch_plan_fetch(const void* host_src, void* dst, size_t bytes, hipStream_t stream,
+                             uint64_t* seen, uint64_t seq) {
+    const int64_t n16 = (int64_t)((bytes + 15) / 16);
+    if (n16 == 0 && seen == nullptr) return hipSuccess;
+    hipLaunchKernelGGL(plan_fetch_kernel, dim3((unsigned)plan_fetch_blocks(bytes)),
+                       dim3(kFetchThreads), 0, stream, static_cast<const u32x4*>(host_src),
+                       static_cast<u32x4*>(dst), n16, seen, seq);
     return hipGetLastError();
 }
 

@@ -29,6 +29,7 @@ struct SigPlan {
     uint64_t off_tmeta;         // TensorInfo [T]
     uint64_t off_order;         // i32  [T] tensor ids grouped by dtype (stable)
     uint64_t off_gtile;         // i64  [T+1] tile prefix in that order
+    uint64_t off_chunk_tensor;  // i32  [C] tensor of each chunk
     uint64_t off_partials;      // TilePartial [R * tiles_per_replica]
     uint64_t total_bytes;
 };

@@ -177,6 +177,23 @@ def test_read_probe_argument_errors_return_before_gpu_work():
     assert L.c3_read_probe(null, 4096, 0, p16, null, null, null) == -1
 
 
+def test_check_argument_errors_return_before_gpu_work():
+    L = c3.lib()
+    md = _metas([(c3.F32, (1000,))])
+    ptrs = (ctypes.c_void_p * 4)(16, 32, 48, 64)
+    null = ctypes.c_void_p(0)
+    p8, ws = ctypes.c_void_p(64), ctypes.c_void_p(256)
+    need = L.c3_check_workspace_size(md, 1, 2, 1024, 0)
+    assert need > L.c3_signature_workspace_size(md, 1, 2, 1024)
+    assert L.c3_check_workspace_size(md, 1, 1, 1024, 0) == 0              # a group of one
+    args = lambda R, wsb, bm=p8: (ptrs, md, 1, R, 1024, p8, p8, bm, p8, p8, 10, p8, 10, p8, ws,
+                                  wsb, null, null)
+    assert L.c3_check(*args(1, need)) == -1                               # R = 1
+    assert L.c3_check(*args(2, need - 256)) == -4                         # workspace too small
+    assert L.c3_check(*args(2, need, ctypes.c_void_p(68))) == -2          # misaligned bitmap
+    assert L.c3_check(*args(257, need)) == -1                             # R > 256
+
+
 def test_binding_has_no_cpu_fallback():
     import torch
     x = torch.zeros(1024)

@@ -1,0 +1,196 @@
+"""c3_check (signature, exact vote and localization in one call) against the
+three separate calls it replaces and against the oracle, through the C ABI:
+every record, status, bitmap word, majority index, list entry and count bit
+for bit.  Covers the fused tail (R <= 16, lists in the last workgroup up to
+8,192 chunks, a separate localization above), the separate steps of larger
+groups, repeated calls on a staged plan (the done counter must return to
+zero), truncated lists and graph replay."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads
+from parity import compare_all_records
+
+pytestmark = pytest.mark.gpu
+
+c3 = pytest.importorskip("paper_2608_11034_amd.c3")
+DEV = "cuda"
+CODE = {torch.float32: workloads.F32, torch.bfloat16: workloads.BF16,
+        torch.float16: workloads.F16, torch.uint8: workloads.RAW}
+
+
+def _case(*a):
+    print("CASE", *a, flush=True)
+
+
+def _host(outs):
+    rec, st, bm, mj, outl, und, cnt = outs
+    torch.cuda.synchronize()
+    c = cnt.cpu().numpy()
+    return dict(records=c3.records_numpy(rec), status=st.cpu().numpy(),
+                bitmap=bm.cpu().numpy().view(np.uint64), maj=mj.cpu().numpy(),
+                outliers=outl[:min(int(c[0]), outl.shape[0])].cpu().numpy(),
+                undecided=und.cpu().numpy()[:min(int(c[1]), und.numel())], counts=c)
+
+
+def _three_calls(reps, chunk, tile=0, out_cap=None, und_cap=None):
+    plan = c3.SignaturePlan(reps, chunk, tile)
+    rec = plan.new_records()
+    plan.run(rec, plan.new_workspace())
+    st, bm, mj = c3.consensus(rec, c3.EXACT)
+    outl, und, cnt = c3.localize(st, bm, mj, rec, out_cap=out_cap, und_cap=und_cap)
+    return _host((rec, st, bm, mj, outl, und, cnt))
+
+
+def _check(reps, chunk, tile=0, out_cap=None, und_cap=None):
+    plan = c3.SignaturePlan(reps, chunk, tile)
+    outs = plan.new_check_outputs(out_cap, und_cap)
+    ws = torch.empty(plan.check_workspace_size(), dtype=torch.uint8, device=DEV)
+    plan.run_check(outs, ws)
+    return _host(outs)
+
+
+def _same(a, b):
+    for f in a["records"].dtype.names:
+        assert np.array_equal(a["records"][f], b["records"][f]), f
+    for k in ("status", "bitmap", "maj", "undecided", "counts"):
+        assert np.array_equal(a[k], b[k]), k
+    assert a["outliers"].tobytes() == b["outliers"].tobytes()
+
+
+def _vs_oracle(g, reps, chunk):
+    metas = [(CODE[t.dtype], tuple(t.shape)) for t in reps[0]]
+    ref = oracle.signature([[workloads.host_bytes(t) for t in rep] for rep in reps], metas, chunk)
+    compare_all_records(g["records"], ref)
+    ost, obm, omj = oracle.vote_exact(ref["sig"])
+    assert np.array_equal(g["status"], ost) and np.array_equal(g["maj"], omj)
+    assert np.array_equal(g["bitmap"].reshape(obm.shape), obm)
+    loc = oracle.localize(ost, obm, omj, len(reps))
+    assert g["counts"].tolist() == loc["counts"].tolist()
+    o = g["outliers"].reshape(-1).view(c3.OUTLIER_DTYPE) if g["outliers"].size else \
+        np.zeros(0, c3.OUTLIER_DTYPE)
+    assert len(o) == len(loc["unit"])
+    assert [int(x) for x in o["chunk"]] == loc["unit"].tolist()
+    assert [int(x) for x in o["replica"]] == loc["replica"].tolist()
+    assert g["undecided"].tolist() == loc["undecided"].tolist()
+
+
+@pytest.mark.parametrize("k", [1, 2, 3, 4])
+def test_small_configs_equal_three_calls_and_oracle(k):
+    _case("check small config", k)
+    w = workloads.make(k, device=DEV, scale="small")
+    g = _check(w.replicas, w.chunk_bytes)
+    _same(g, _three_calls(w.replicas, w.chunk_bytes))
+    _vs_oracle(g, w.replicas, w.chunk_bytes)
+    assert g["counts"][0] + g["counts"][1] > 0
+
+
+def _random_reps(seed, R, n_max=300_000, T_max=6, chunk=None):
+    rng = np.random.default_rng(seed)
+    chunk = chunk or int(1024 << rng.integers(0, 9))
+    tile = int(1024 << rng.integers(0, int(np.log2(chunk // 1024)) + 1))
+    gen = torch.Generator(device=DEV)
+    gen.manual_seed(seed)
+    dts = list(CODE)
+    base = []
+    for _ in range(int(rng.integers(1, T_max + 1))):
+        dt = dts[int(rng.integers(0, 4))]
+        n = int(rng.integers(0, n_max))
+        base.append(torch.randint(0, 256, (n,), generator=gen, device=DEV, dtype=torch.uint8)
+                    if dt == torch.uint8 else torch.randn(n, generator=gen, device=DEV).to(dt))
+    reps = [[t.clone() for t in base] for _ in range(R)]
+    for _ in range(max(3, R // 2)):                       # byte faults, some in shared chunks
+        t = int(rng.integers(0, len(base)))
+        if reps[0][t].numel():
+            pos = int(rng.integers(0, reps[0][t].numel() * reps[0][t].element_size()))
+            for r in rng.choice(R, size=int(rng.integers(1, max(2, R // 2 + 1))), replace=False):
+                reps[int(r)][t].view(torch.uint8)[pos] ^= 0x5A
+    return reps, chunk, tile
+
+
+@pytest.mark.parametrize("seed,R", [(0, 2), (1, 3), (2, 4), (3, 5), (4, 8), (5, 13), (6, 16),
+                                    (7, 17), (8, 40), (9, 130)])
+def test_random_plans_equal_three_calls_and_oracle(seed, R):
+    reps, chunk, tile = _random_reps(2000 + seed, R, n_max=200_000 if R < 40 else 40_000)
+    _case("check random", seed, R, chunk, tile)
+    g = _check(reps, chunk, tile)
+    _same(g, _three_calls(reps, chunk, tile))
+    _vs_oracle(g, reps, chunk)
+
+
+@pytest.mark.parametrize("n_chunks,R", [(8192, 8), (8193, 8), (40_000, 4), (9000, 16)])
+def test_many_chunks_take_the_separate_localization(n_chunks, R):
+    """Above 8,192 chunks the tail kernel votes and a separate localization
+    lists; above 32,768 that localization is the three-pass one."""
+    _case("check many chunks", n_chunks, R)
+    gen = torch.Generator(device=DEV)
+    gen.manual_seed(n_chunks)
+    base = torch.randint(0, 256, (n_chunks * 1024 - 100,), generator=gen, device=DEV,
+                         dtype=torch.uint8)
+    reps = [[base.clone()] for _ in range(R)]
+    rng = np.random.default_rng(n_chunks)
+    for pos in rng.integers(0, base.numel(), 50):
+        reps[int(rng.integers(0, R))][0][int(pos)] ^= 1
+    g = _check(reps, 1024)
+    _same(g, _three_calls(reps, 1024))
+    assert g["counts"][0] >= 40
+
+
+def test_truncated_lists():
+    w = workloads.make(3, device=DEV, scale="small")
+    _case("check truncated")
+    g = _check(w.replicas, w.chunk_bytes, out_cap=2, und_cap=0)
+    _same(g, _three_calls(w.replicas, w.chunk_bytes, out_cap=2, und_cap=0))
+    assert g["counts"][0] > 2 and len(g["outliers"]) == 2
+
+
+def test_repeated_calls_on_a_staged_plan():
+    """Five calls on one staged plan with the bytes changed between calls:
+    the last workgroup of each call must find the counter at zero again."""
+    _case("check repeated staged")
+    w = workloads.make(3, device=DEV, scale="small")
+    plan = c3.SignaturePlan(w.replicas, w.chunk_bytes)
+    outs = plan.new_check_outputs()
+    ws = torch.empty(plan.check_workspace_size(), dtype=torch.uint8, device=DEV)
+    plan.run_check(outs, ws)
+    for i in range(5):
+        b = w.replicas[i % w.R][i % len(w.metas)].view(-1).view(torch.uint8)
+        b[(i * 7919) % b.numel()] ^= 0x10
+        plan.run_check(outs, ws, plan_staged=True)
+        _same(_host(outs), _three_calls(w.replicas, w.chunk_bytes))
+
+
+def test_graph_replay_equals_eager():
+    _case("check graph")
+    w = workloads.make(2, device=DEV, scale="small")
+    plan = c3.SignaturePlan(w.replicas, w.chunk_bytes)
+    outs = plan.new_check_outputs()
+    ws = torch.empty(plan.check_workspace_size(), dtype=torch.uint8, device=DEV)
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        plan.run_check(outs, ws, stream=s)
+    s.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        plan.run_check(outs, ws, stream=s, plan_staged=True)
+    for i in range(3):
+        b = w.replicas[1][0].view(-1).view(torch.uint8)
+        b[1000 * (i + 1)] ^= 0x04
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        _same(_host(outs), _three_calls(w.replicas, w.chunk_bytes))
+
+
+def test_argument_errors():
+    w = workloads.make(1, device=DEV, scale="small")
+    plan = c3.SignaturePlan(w.replicas, w.chunk_bytes)
+    outs = plan.new_check_outputs()
+    ws = torch.empty(plan.check_workspace_size(), dtype=torch.uint8, device=DEV)
+    with pytest.raises(c3.C3Error, match=r"\(-4\)"):
+        plan.run_check(outs, ws[: plan.ws_bytes])              # room for the signature only
+    one = c3.SignaturePlan([w.replicas[0]], w.chunk_bytes)
+    with pytest.raises(c3.C3Error, match=r"\(-1\)"):
+        one.run_check(one.new_check_outputs(), ws)             # a group of one
