@@ -387,6 +387,35 @@ __device__ __forceinline__ void pass_load(const char* __restrict__ base, int64_t
     }
 }
 
+// The same loads when the whole step lies inside the T x G array: the
+// step's first row (t0, g0) is a uniform address and every lane adds its
+// loop-invariant 32-bit offset (pass_lane_offsets), so no load spends vector
+// instructions on its address.
+template <int CP>
+__device__ __forceinline__ void pass_lane_offsets(int64_t G, int ng, int lane,
+                                                  uint32_t (&off)[CP]) {
+    constexpr int RB = 16 * CP;
+#pragma unroll
+    for (int j = 0; j < CP; ++j) {
+        const int b = 1024 * j + 16 * lane;
+        const int row = b / RB;
+        const int ti = row / kPassGroups;
+        int gi = row % kPassGroups;
+        gi = gi < ng ? gi : 0;                      // groups past the end re-read group g0
+        off[j] = (uint32_t)(((int64_t)ti * G + gi) * RB + (b % RB));
+    }
+}
+
+template <int CP>
+__device__ __forceinline__ void pass_load_full(const char* __restrict__ base, int64_t G,
+                                               int64_t g0, int64_t t0, const uint32_t (&off)[CP],
+                                               vu32x4 (&g)[CP]) {
+    constexpr int RB = 16 * CP;
+    const char* step = base + (t0 * G + g0) * RB;
+#pragma unroll
+    for (int j = 0; j < CP; ++j) g[j] = *reinterpret_cast<const vu32x4*>(step + off[j]);
+}
+
 template <int NMAX, int KIND, bool SHORT>
 __global__ void __launch_bounds__(PassShape<NMAX>::threads) timing_pass_kernel(
     const char* __restrict__ fp, const char* __restrict__ tp, int64_t G, int64_t T, double kappa,
@@ -398,7 +427,9 @@ __global__ void __launch_bounds__(PassShape<NMAX>::threads) timing_pass_kernel(
     constexpr int SEGW = R * kPassGroups;                        // mask words per segment
     __shared__ vu32x4 stage[NW][64 * CPF];
     extern __shared__ uint32_t pass_masks[];                     // [2][n_seg][R][kPassGroups]
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63;
+    // the wave index, uniform across the wave (keeps the step addresses scalar)
+    const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
     const int64_t g0 = (int64_t)blockIdx.x * kPassGroups;
     const int ng = G - g0 < kPassGroups ? (int)(G - g0) : kPassGroups;
     const int64_t n_seg = (T + kSegIters - 1) / kSegIters;
@@ -415,19 +446,27 @@ __global__ void __launch_bounds__(PassShape<NMAX>::threads) timing_pass_kernel(
     // order, so waiting for loads issued after the stores would wait for
     // the stores too.  The last step re-reads its own rows (L2 hits) rather
     // than branch around the prefetch.
+    uint32_t off_f[CPF], off_t[CPT];
+    pass_lane_offsets<CPF>(G, ng, lane, off_f);
+    pass_lane_offsets<CPT>(G, ng, lane, off_t);
+    auto load_step = [&](int64_t t0, vu32x4 (&gf)[CPF], vu32x4 (&gt)[CPT]) {
+        if (t0 + kPassIters <= T) {               // uniform: a whole step
+            pass_load_full<CPF>(fp, G, g0, t0, off_f, gf);
+            pass_load_full<CPT>(tp, G, g0, t0, off_t, gt);
+        } else {                                  // the last, partial step
+            pass_load<CPF>(fp, G, T, g0, ng, t0, lane, gf);
+            pass_load<CPT>(tp, G, T, g0, ng, t0, lane, gt);
+        }
+    };
     vu32x4 gf[CPF], gt[CPT];
-    if (wave < n_steps) {
-        pass_load<CPF>(fp, G, T, g0, ng, (int64_t)wave * kPassIters, lane, gf);
-        pass_load<CPT>(tp, G, T, g0, ng, (int64_t)wave * kPassIters, lane, gt);
-    }
+    if (wave < n_steps) load_step((int64_t)wave * kPassIters, gf, gt);
     for (int64_t st = wave; st < n_steps; st += NW) {
         const int64_t t0 = st * kPassIters;
         vu32x4 vf[CPF], vt[CPT];
         stage_swap<CPF>(stage[wave], lane, gf, vf);
         stage_swap<CPT>(stage[wave], lane, gt, vt);
         const int64_t tn = (st + NW < n_steps ? st + NW : st) * kPassIters;
-        pass_load<CPF>(fp, G, T, g0, ng, tn, lane, gf);
-        pass_load<CPT>(tp, G, T, g0, ng, tn, lane, gt);
+        load_step(tn, gf, gt);
         const int64_t t = t0 + ti;
         if (t >= T || gi >= ng) continue;
         uint64_t ef[NMAX], et[NMAX];
@@ -449,7 +488,8 @@ __global__ void __launch_bounds__(PassShape<NMAX>::threads) timing_pass_kernel(
             }
         }
         const UnitVote vfp = exact_vote_row<NMAX>(ef, R);
-        const UnitVote vtm = statistical_vote_row<NMAX, KIND>(et, R, kappa);
+        // only the bitmaps reach the masks: no lower-median replica
+        const UnitVote vtm = statistical_vote_row<NMAX, KIND, false>(et, R, kappa);
         const uint32_t bit = 1u << (t & (kSegIters - 1));
         const int64_t w0 = (t / kSegIters) * SEGW + gi;
         for (uint64_t b = vfp.bitmap; b != 0ull; b &= b - 1ull)
@@ -535,6 +575,8 @@ static bool pass_applies(const void* fp, const void* times, int time_kind, int R
     if (((uintptr_t)fp & 15) != 0 || ((uintptr_t)times & 15) != 0 || (R * tsize) % 16 != 0)
         return false;
     if (T < 1 || Wt > 64) return false;
+    // the lanes' offsets within a step are 32-bit
+    if ((int64_t)kPassIters * G * R * 8 >= ((int64_t)1 << 31)) return false;
     const int64_t n_seg = (T + kSegIters - 1) / kSegIters;
     const int64_t bytes = 2 * n_seg * R * kPassGroups * 4;
     if (bytes > kPassMaskLds) return false;

@@ -198,18 +198,17 @@ __device__ __forceinline__ double quantile7_sorted(const V (&s)[N], int n, doubl
 // Everything after the first sort.  NC > 0 fixes the finite count at
 // compile time (every value finite and R == NMAX, the usual case), so every
 // order statistic is a plain register and no replica needs a finiteness
-// test.
-template <int NMAX, int NC, typename V>
+// test.  Without MAJ the lower-median replica is not computed (majority is
+// -1); callers that keep only the bitmap skip that work.
+template <int NMAX, int NC, typename V, bool MAJ>
 __device__ __forceinline__ UnitVote statistical_tail(const V (&x)[NMAX], const V (&s)[NMAX],
                                                      uint64_t fin, uint64_t nonfin, int nf_rt,
                                                      double kappa) {
-    const double inf = __builtin_huge_val();
     const int nf = NC > 0 ? NC : nf_rt;
     auto finite = [&](int r) { return NC > 0 || ((fin >> r) & 1ull) != 0; };
     const double m = median_sorted<NMAX>(s, nf);
-    double dev[NMAX];
-#pragma unroll
-    for (int r = 0; r < NMAX; ++r) dev[r] = finite(r) ? fabs((double)x[r] - m) : inf;
+    // the largest deviation, when known without visiting every replica
+    double dmax = __builtin_huge_val();
     double d;
     if constexpr (NC > 0) {
         // m lies between the two middle sorted values, so the deviations of
@@ -231,10 +230,15 @@ __device__ __forceinline__ UnitVote statistical_tail(const V (&x)[NMAX], const V
 #pragma unroll
         for (int i = 2; i <= h; ++i) b = fmin(b, fmax(lo[i - 1], hi[h - i]));
         d = (a + b) * 0.5;
+        // lo and hi are the deviations of every value, computed as the flag
+        // test computes them, and each run ascends away from m: the largest
+        // deviation is the larger run end
+        dmax = fmax(lo[h - 1], hi[h - 1]);
     } else {
         double ds[NMAX];
 #pragma unroll
-        for (int r = 0; r < NMAX; ++r) ds[r] = dev[r];
+        for (int r = 0; r < NMAX; ++r)
+            ds[r] = finite(r) ? fabs((double)x[r] - m) : __builtin_huge_val();
         sort_network<NMAX>(ds);
         d = median_sorted<NMAX>(ds, nf);
     }
@@ -247,10 +251,19 @@ __device__ __forceinline__ UnitVote statistical_tail(const V (&x)[NMAX], const V
     uint64_t B = nonfin;
     if (d != 0.0) {
         const double thr = kappa * d;
+        // no replica can be flagged when even the largest deviation is not
+        // above the threshold (the usual unit): skip the per-replica tests
+        if (dmax > thr) {
 #pragma unroll
-        for (int r = 0; r < NMAX; ++r)
-            if (finite(r) && dev[r] > thr) B |= 1ull << r;
+            for (int r = 0; r < NMAX; ++r)
+                if (finite(r) && fabs((double)x[r] - m) > thr) B |= 1ull << r;
+        }
     }
+    UnitVote v;
+    v.status = B ? C3_ATTRIBUTED : C3_AGREE;
+    v.bitmap = B;
+    v.majority = -1;
+    if constexpr (!MAJ) return v;
     // lower-median replica: stable position (nf - 1) / 2 in (value, replica) order
     const V target = pick<NMAX>(s, (nf - 1) / 2);
     int want = (nf - 1) / 2;
@@ -264,9 +277,6 @@ __device__ __forceinline__ UnitVote statistical_tail(const V (&x)[NMAX], const V
             --want;
         }
     }
-    UnitVote v;
-    v.status = B ? C3_ATTRIBUTED : C3_AGREE;
-    v.bitmap = B;
     v.majority = med;
     return v;
 }
@@ -274,7 +284,7 @@ __device__ __forceinline__ UnitVote statistical_tail(const V (&x)[NMAX], const V
 // `bits` hold the fp32 (KIND == C3_EV_F32, zero-extended) or fp64 patterns.
 // fp32 values are ordered and compared in fp32 (exact: the conversion to
 // fp64 is monotonic and exact); every arithmetic step is fp64.
-template <int NMAX, int KIND>
+template <int NMAX, int KIND, bool MAJ = true>
 __device__ __forceinline__ UnitVote statistical_vote_row(const uint64_t (&bits)[NMAX], int R,
                                                          double kappa) {
     using V = typename std::conditional<KIND == C3_EV_F32, float, double>::type;
@@ -284,13 +294,18 @@ __device__ __forceinline__ UnitVote statistical_vote_row(const uint64_t (&bits)[
     for (int r = 0; r < NMAX; ++r) {
         if constexpr (KIND == C3_EV_F32) x[r] = __uint_as_float((uint32_t)bits[r]);
         else x[r] = __longlong_as_double((long long)bits[r]);
-        const bool f = r < R && __builtin_isfinite(x[r]);
-        fin |= (uint64_t)f << r;
-        s[r] = f ? x[r] : (V)__builtin_huge_val();   // excluded values sort last
+        fin |= (uint64_t)(r < R && __builtin_isfinite(x[r])) << r;
     }
     const uint64_t valid = R == 64 ? ~0ull : ((1ull << R) - 1);
     const uint64_t nonfin = valid & ~fin;
     const int nf = __builtin_popcountll(fin);
+    if (nf == NMAX) {
+        // every slot holds a finite value (the usual unit): sort them as they are
+#pragma unroll
+        for (int r = 0; r < NMAX; ++r) s[r] = x[r];
+        sort_network<NMAX>(s);
+        return statistical_tail<NMAX, NMAX, V, MAJ>(x, s, fin, nonfin, nf, kappa);
+    }
     if (2 * nf <= R) {
         UnitVote v;
         v.status = C3_INCONCLUSIVE;
@@ -298,9 +313,11 @@ __device__ __forceinline__ UnitVote statistical_vote_row(const uint64_t (&bits)[
         v.majority = -1;
         return v;
     }
+#pragma unroll
+    for (int r = 0; r < NMAX; ++r)   // excluded values sort last
+        s[r] = ((fin >> r) & 1ull) ? x[r] : (V)__builtin_huge_val();
     sort_network<NMAX>(s);
-    if (nf == NMAX) return statistical_tail<NMAX, NMAX>(x, s, fin, nonfin, nf, kappa);
-    return statistical_tail<NMAX, 0>(x, s, fin, nonfin, nf, kappa);
+    return statistical_tail<NMAX, 0, V, MAJ>(x, s, fin, nonfin, nf, kappa);
 }
 
 }  // namespace c3
