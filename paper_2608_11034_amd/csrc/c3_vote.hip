@@ -1,33 +1,30 @@
 // Consensus kernels of C3 for gfx950: the decision step of Algorithm 1.
 //
 // Which kernel decides a unit depends on the group size R:
-//   R <= 16            one thread per unit, the R values in registers
-//                      (128-bit row loads when replicas are adjacent),
-//                      deciding with the per-unit functions of c3_vote_row.h;
-//   EXACT, R > 16 and  one wave per unit: lane l holds replicas l, l + 64,
-//   STATISTICAL,       ... (see the wave kernels below), every peer value
-//   R > 32             reaches all lanes by readlane, and bitmap word s is
-//                      one ballot;
-//   STATISTICAL,       one lane per (unit, replica): a unit's values sit in
-//   17 <= R <= 32      32 consecutive lanes, two units per wave, peers
-//                      compared by shuffles.
-// Measured on 1M-unit rows: the wave kernel's exact vote is 1.5x (R = 17) to
-// 7.6x (R = 64) faster than lane-per-replica counting, and its statistical
-// vote faster from R = 48, slower at R <= 32 where two units share a wave.
+//   R <= 16   one thread per unit, the R values in registers (128-bit row
+//             loads when replicas are adjacent), deciding with the per-unit
+//             functions of c3_vote_row.h;
+//   R > 16    one wave per unit: lane l holds replicas l, l + 64, ... (see
+//             the wave kernels below) and bitmap word s is one ballot.  The
+//             exact vote broadcasts candidate values by readlane; the
+//             statistical vote sorts the wave's values once.
+// Measured on 1M-unit rows, the wave kernel's exact vote is 1.5x (R = 17) to
+// 7.6x (R = 64) faster than lane-per-replica counting.  Per 256K units its
+// statistical vote takes 0.09-0.11 ms up to R = 64 and 0.26-0.37 ms at
+// R = 129-256 (fp32-fp64), 1.8x to 8x faster than the rank loops and
+// (value, replica) double sorts it replaced.
 //
 // EXACT (Sec. 5.3): a strict majority exists iff some value is held by more
 // than R / 2 replicas; those are the majority, the bitmap marks the others
 // and the majority index is the lowest majority replica.
 //
 // STATISTICAL (Sec. 5.4), in fp64: order statistics of the finite values in
-// the stable (value, then replica index) order -- from each value's rank in
-// the lane-per-replica kernel, from a sort across the wave in the wave
-// kernel -- give the median, the median absolute deviation, the type-7
-// quartiles and the range, in the fallback order MAD -> IQR / 2 ->
-// range / n_finite.  Non-finite values are outliers and take no part in m
-// or d.  No floating-point contraction is allowed in this file (the host
-// compiles it with -ffp-contract=off), so the decision rounds exactly as the
-// plain definition does.
+// the stable (value, then replica index) order give the median, the median
+// absolute deviation, the type-7 quartiles and the range, in the fallback
+// order MAD -> IQR / 2 -> range / n_finite.  Non-finite values are outliers
+// and take no part in m or d.  No floating-point contraction is allowed in
+// this file (the host compiles it with -ffp-contract=off), so the decision
+// rounds exactly as the plain definition does.
 #include "c3_device.h"
 #include "c3_internal.h"
 #include "c3_vote_row.h"
@@ -36,114 +33,10 @@ namespace c3 {
 
 constexpr int kVoteThreads = 256;
 
-__device__ inline double load_ev_f64(const char* p, int kind) {
-    if (kind == C3_EV_F32) return (double)*reinterpret_cast<const float*>(p);
-    return *reinterpret_cast<const double*>(p);
-}
-
-__device__ inline uint64_t group_bits(uint64_t ballot, int gbase, uint64_t gmask) {
-    return (ballot >> gbase) & gmask;
-}
-
-// Order statistic k (0-based) of the finite values of a lane group, given
-// every lane's stable rank among them.
-__device__ inline double order_stat(double x, bool fin, int rank, int k, int gbase, uint64_t gmask) {
-    const uint64_t b = group_bits(ballot64(fin && rank == k), gbase, gmask);
-    const int src = gbase + (b ? __builtin_ctzll(b) : 0);
-    return shfl_f64(x, src);
-}
-
-__device__ inline int stable_rank(double x, bool fin, int R, int r, int gbase) {
-    int rank = 0;
-    for (int j = 0; j < R; ++j) {
-        const double y = shfl_f64(x, gbase + j);
-        const bool fy = __shfl((int)fin, gbase + j, 64) != 0;
-        rank += (fy && (y < x || (y == x && j < r))) ? 1 : 0;
-    }
-    return rank;
-}
-
-__device__ inline double median_of(double x, bool fin, int rank, int nf, int gbase, uint64_t gmask) {
-    if (nf & 1) return order_stat(x, fin, rank, (nf - 1) / 2, gbase, gmask);
-    const double a = order_stat(x, fin, rank, nf / 2 - 1, gbase, gmask);
-    const double b = order_stat(x, fin, rank, nf / 2, gbase, gmask);
-    return (a + b) * 0.5;
-}
-
-// Hyndman-Fan type 7: h = (n - 1) p; Q = s[floor h] + frac(h) (s[floor h + 1] - s[floor h]).
-__device__ inline double quantile7(double x, bool fin, int rank, int nf, double p, int gbase,
-                                   uint64_t gmask) {
-    const double h = (double)(nf - 1) * p;
-    const double fl = floor(h);
-    const int lo = (int)fl;
-    const double frac = h - fl;
-    if (lo + 1 >= nf) return order_stat(x, fin, rank, nf - 1, gbase, gmask);
-    const double a = order_stat(x, fin, rank, lo, gbase, gmask);
-    const double b = order_stat(x, fin, rank, lo + 1, gbase, gmask);
-    const double diff = b - a;
-    const double prod = frac * diff;
-    return a + prod;
-}
-
-__global__ void __launch_bounds__(kVoteThreads) statistical_vote_kernel(
-    const char* __restrict__ ev, int kind, int64_t rstride, int64_t ustride, int R, int gw_log2,
-    int64_t n_units, double kappa, uint8_t* __restrict__ status, uint64_t* __restrict__ bitmap,
-    int32_t* __restrict__ majority_idx) {
-    const int gw = 1 << gw_log2;
-    const int lane = threadIdx.x & 63;
-    const int r = lane & (gw - 1);
-    const int gbase = lane - r;
-    const uint64_t gmask = gw == 64 ? ~0ull : ((1ull << gw) - 1);
-    const int64_t units_per_block = (int64_t)(kVoteThreads >> gw_log2);
-    const int64_t u = (int64_t)blockIdx.x * units_per_block + (threadIdx.x >> gw_log2);
-    const bool valid = u < n_units && r < R;
-    const double x = valid ? load_ev_f64(ev + u * ustride + (int64_t)r * rstride, kind) : 0.0;
-    const bool fin = valid && __builtin_isfinite(x);
-    const uint64_t finb = group_bits(ballot64(fin), gbase, gmask);
-    const uint64_t nonfin = group_bits(ballot64(valid && !fin), gbase, gmask);
-    const int nf = __builtin_popcountll(finb);
-    if (2 * nf <= R) {  // finite values are not a strict majority
-        if (valid && r == 0) {
-            status[u] = C3_INCONCLUSIVE;
-            bitmap[u] = 0;
-            majority_idx[u] = -1;
-        }
-        return;
-    }
-    const int rank = stable_rank(x, fin, R, r, gbase);
-    const double m = median_of(x, fin, rank, nf, gbase, gmask);
-    const double dev = fin ? fabs(x - m) : 0.0;
-    const int drank = stable_rank(dev, fin, R, r, gbase);
-    double d = median_of(dev, fin, drank, nf, gbase, gmask);
-    if (d == 0.0) {
-        const double q3 = quantile7(x, fin, rank, nf, 0.75, gbase, gmask);
-        const double q1 = quantile7(x, fin, rank, nf, 0.25, gbase, gmask);
-        d = (q3 - q1) * 0.5;
-    }
-    if (d == 0.0) {
-        const double hi = order_stat(x, fin, rank, nf - 1, gbase, gmask);
-        const double lo = order_stat(x, fin, rank, 0, gbase, gmask);
-        d = (hi - lo) / (double)nf;
-    }
-    bool flag = false;
-    if (d != 0.0) {
-        const double thr = kappa * d;
-        flag = fin && dev > thr;
-    }
-    const uint64_t B = nonfin | group_bits(ballot64(flag), gbase, gmask);
-    const uint64_t medb = group_bits(ballot64(fin && rank == (nf - 1) / 2), gbase, gmask);
-    if (valid && r == 0) {
-        status[u] = B ? C3_ATTRIBUTED : C3_AGREE;
-        bitmap[u] = B;
-        majority_idx[u] = medb ? __builtin_ctzll(medb) : -1;
-    }
-}
-
 // ---------------------------------------------------------------------------
-// Small groups (R <= 16): one thread per unit with the R values in registers.
-// Cross-lane traffic dominates the lane-per-replica kernels at these sizes;
-// here the whole decision is register arithmetic.  NMAX is R rounded up to
-// a power of two; slots past R are padding that never takes part.
+// Small groups (R <= 16): one thread per unit with the R values in registers,
+// so the whole decision is register arithmetic.  NMAX is R rounded up to a
+// power of two; slots past R are padding that never takes part.
 // ---------------------------------------------------------------------------
 template <int NMAX>
 __global__ void __launch_bounds__(kVoteThreads) exact_vote_small_kernel(
@@ -176,11 +69,11 @@ __global__ void __launch_bounds__(kVoteThreads) statistical_vote_small_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// Wave per unit (EXACT above 16 replicas, STATISTICAL above 32).  Lane l
+// Wave per unit (every group above 16 replicas).  Lane l
 // holds the values of replicas l, l + 64, l + 128 and l + 192 (NS =
 // ceil(R / 64) slots; slot s holds replica 64 s + l), so bitmap word s is the
 // ballot of slot s.  The exact vote broadcasts candidate values by readlane
-// at a wave-uniform index; the statistical vote sorts the wave's keys.
+// at a wave-uniform index; the statistical vote sorts the wave's values.
 // ---------------------------------------------------------------------------
 constexpr int kWideUnitsPerBlock = kVoteThreads / 64;
 
@@ -280,110 +173,196 @@ __global__ void __launch_bounds__(kVoteThreads) exact_vote_wide_kernel(
     wide_write<NS>(u, any ? C3_ATTRIBUTED : C3_AGREE, ob, mj, status, bitmap, majority_idx);
 }
 
-// Bitonic sort of the wave's 64 * NP (value, replica) keys, ascending by
-// value, then replica: position p = 64 s + lane ends up holding the p-th
-// smallest key.  Keys are unique (the replica breaks ties), so the order is
-// the stable (value, replica) order.  Partners within a slot are 2^i lanes
-// apart (xor shuffles); partners 64 and more apart sit in the same lane.
-__device__ inline bool key_less(double av, int ai, double bv, int bi) {
-    return av < bv || (av == bv && ai < bi);
+// STATISTICAL over more than 32 replicas: the wave sorts the finite values
+// once and reads every order statistic off the sorted copy.
+//
+// Sorted position p = NP lane + i lives in register i of lane `lane` (NP =
+// ceil(R / 64) rounded up to a power of two, excluded values as +inf), so
+// the network's shortest distances -- the most frequent ones -- are
+// compare-exchanges between a lane's own registers, and the rest pair lane l
+// with lane l ^ M.  The network is the bitonic sorter in its one-direction
+// form: merging blocks of K, position p first meets p ^ (K - 1) (the
+// reversed other half), then p ^ j for j = K / 4 .. 1, the smaller key
+// always going to the lower position.  Values only: equal values are
+// interchangeable, and the lower-median replica is found afterwards by
+// counting.
+
+// Lane l's copy of v from lane l ^ M: DPP where a row of 16 can express the
+// pattern (quad permutes, mirrors), ds_swizzle inside 32 lanes, ds_bpermute
+// across the halves.
+template <int M>
+__device__ __forceinline__ uint32_t xor_lane_u32(uint32_t v) {
+    const int iv = (int)v;
+    if constexpr (M == 1) return (uint32_t)__builtin_amdgcn_mov_dpp(iv, 0xB1, 0xF, 0xF, false);
+    else if constexpr (M == 2) return (uint32_t)__builtin_amdgcn_mov_dpp(iv, 0x4E, 0xF, 0xF, false);
+    else if constexpr (M == 3) return (uint32_t)__builtin_amdgcn_mov_dpp(iv, 0x1B, 0xF, 0xF, false);
+    else if constexpr (M == 7) return (uint32_t)__builtin_amdgcn_mov_dpp(iv, 0x141, 0xF, 0xF, false);
+    else if constexpr (M == 15) return (uint32_t)__builtin_amdgcn_mov_dpp(iv, 0x140, 0xF, 0xF, false);
+    else if constexpr (M < 32) return (uint32_t)__builtin_amdgcn_ds_swizzle(iv, 0x1F | (M << 10));
+    else return (uint32_t)__shfl_xor(iv, M, 64);
 }
 
-template <int NP>
-__device__ inline void wave_sort(double (&v)[NP], int (&id)[NP]) {
-    const int lane = threadIdx.x & 63;
+template <int M>
+__device__ __forceinline__ float xor_lane(float v) {
+    return __uint_as_float(xor_lane_u32<M>(__float_as_uint(v)));
+}
+
+template <int M>
+__device__ __forceinline__ double xor_lane(double v) {
+    const uint64_t b = (uint64_t)__double_as_longlong(v);
+    const uint64_t lo = xor_lane_u32<M>((uint32_t)b), hi = xor_lane_u32<M>((uint32_t)(b >> 32));
+    return __longlong_as_double((long long)((hi << 32) | lo));
+}
+
+template <typename V>
+__device__ __forceinline__ void order_pair(V& a, V& b) {
+    const bool sw = b < a;
+    const V lo = sw ? b : a, hi = sw ? a : b;
+    a = lo;
+    b = hi;
+}
+
+// Between lanes: a lane in the lower half of the pair keeps the smaller key.
+template <typename V>
+__device__ __forceinline__ V keep(V mine, V other, bool upper) {
+    return ((other < mine) != upper) ? other : mine;
+}
+
+template <int NP, int K, typename V>
+__device__ __forceinline__ void sort_flip(V (&k)[NP], int lane) {
+    if constexpr (K <= NP) {
 #pragma unroll
-    for (int k = 2; k <= 64 * NP; k <<= 1) {
+        for (int i = 0; i < NP; ++i)
+            if (i < (i ^ (K - 1))) order_pair(k[i], k[i ^ (K - 1)]);
+    } else {
+        constexpr int M = K / NP - 1;               // (lane, i) meets (lane ^ M, i ^ (NP - 1))
+        const bool upper = (lane & (K / NP / 2)) != 0;
+        V o[NP];
 #pragma unroll
-        for (int j = k >> 1; j > 0; j >>= 1) {
-            if (j >= 64) {
+        for (int i = 0; i < NP; ++i) o[i] = xor_lane<M>(k[i ^ (NP - 1)]);
 #pragma unroll
-                for (int s = 0; s < NP; ++s) {
-                    const int t = s ^ (j >> 6);
-                    if (t < s) continue;                 // each slot pair once
-                    const bool asc = ((64 * s) & k) == 0;
-                    const bool tl = key_less(v[t], id[t], v[s], id[s]);
-                    if (asc ? tl : !tl) {
-                        const double w = v[s];
-                        v[s] = v[t];
-                        v[t] = w;
-                        const int q = id[s];
-                        id[s] = id[t];
-                        id[t] = q;
-                    }
-                }
-            } else {
-#pragma unroll
-                for (int s = 0; s < NP; ++s) {
-                    const double ov = shfl_xor_f64(v[s], j);
-                    const int oi = (int)shfl_xor_u32((uint32_t)id[s], j);
-                    const bool lower = (lane & j) == 0;
-                    const bool asc = ((64 * s + lane) & k) == 0;
-                    const bool ol = key_less(ov, oi, v[s], id[s]);
-                    if (lower == asc ? ol : !ol) {
-                        v[s] = ov;
-                        id[s] = oi;
-                    }
-                }
-            }
-        }
+        for (int i = 0; i < NP; ++i) k[i] = keep(k[i], o[i], upper);
     }
 }
 
-// The key at sorted position k (wave-uniform).
-template <int NP>
-__device__ inline double sorted_at(const double (&v)[NP], int k) {
-    double r = 0.0;
+template <int NP, int J, typename V>
+__device__ __forceinline__ void sort_halves(V (&k)[NP], int lane) {
+    if constexpr (J >= 1) {
+        if constexpr (J < NP) {
 #pragma unroll
-    for (int s = 0; s < NP; ++s)
-        if (s == (k >> 6)) r = readlane_f64(v[s], k & 63);
-    return r;
+            for (int i = 0; i < NP; ++i)
+                if ((i & J) == 0) order_pair(k[i], k[i | J]);
+        } else {
+            constexpr int M = J / NP;
+            const bool upper = (lane & M) != 0;
+#pragma unroll
+            for (int i = 0; i < NP; ++i) k[i] = keep(k[i], xor_lane<M>(k[i]), upper);
+        }
+        sort_halves<NP, J / 2>(k, lane);
+    }
 }
 
-template <int NP>
-__device__ inline double sorted_median(const double (&v)[NP], int nf) {
-    if (nf & 1) return sorted_at<NP>(v, (nf - 1) / 2);
-    const double a = sorted_at<NP>(v, nf / 2 - 1);
-    const double b = sorted_at<NP>(v, nf / 2);
+template <int NP, int K, typename V>
+__device__ __forceinline__ void wave_sort(V (&k)[NP], int lane) {
+    if constexpr (K <= 64 * NP) {
+        sort_flip<NP, K>(k, lane);
+        sort_halves<NP, K / 4>(k, lane);
+        wave_sort<NP, 2 * K>(k, lane);
+    }
+}
+
+// The key at sorted position p (wave-uniform).
+template <int NP, typename V>
+__device__ __forceinline__ double sorted_at(const V (&k)[NP], int p) {
+    const int l = p / NP, i = p % NP;
+    V r = 0;
+#pragma unroll
+    for (int t = 0; t < NP; ++t)
+        if (t == i) {
+            if constexpr (sizeof(V) == 4)
+                r = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(k[t]), l));
+            else
+                r = __longlong_as_double((long long)readlane_u64((uint64_t)__double_as_longlong(k[t]), l));
+        }
+    return (double)r;
+}
+
+template <int NP, typename V>
+__device__ __forceinline__ double sorted_median(const V (&k)[NP], int nf) {
+    if (nf & 1) return sorted_at<NP>(k, (nf - 1) / 2);
+    const double a = sorted_at<NP>(k, nf / 2 - 1);
+    const double b = sorted_at<NP>(k, nf / 2);
     return (a + b) * 0.5;
 }
 
-// Hyndman-Fan type 7, as quantile7 above.
-template <int NP>
-__device__ inline double sorted_quantile7(const double (&v)[NP], int nf, double p) {
+// Hyndman-Fan type 7: h = (n - 1) p; Q = s[floor h] + frac(h) (s[floor h + 1] - s[floor h]).
+template <int NP, typename V>
+__device__ __forceinline__ double sorted_quantile7(const V (&k)[NP], int nf, double p) {
     const double h = (double)(nf - 1) * p;
     const double fl = floor(h);
     const int lo = (int)fl;
     const double frac = h - fl;
-    if (lo + 1 >= nf) return sorted_at<NP>(v, nf - 1);
-    const double a = sorted_at<NP>(v, lo);
-    const double b = sorted_at<NP>(v, lo + 1);
+    if (lo + 1 >= nf) return sorted_at<NP>(k, nf - 1);
+    const double a = sorted_at<NP>(k, lo);
+    const double b = sorted_at<NP>(k, lo + 1);
     const double diff = b - a;
     const double prod = frac * diff;
     return a + prod;
 }
 
-template <int NS>
+// Median of |s - m| over the nf sorted finite values s, without sorting the
+// deviations: the `split` values below m give m - s[split - 1 - i], the
+// others s[split + i] - m, two ascending runs (each deviation rounds as
+// |s - m| does, since rounding is symmetric).  Order statistic k of their
+// union is found by bisecting how many of the k + 1 smallest come from the
+// first run.
+template <int NP, typename V>
+__device__ __forceinline__ double deviation_median(const V (&k)[NP], int nf, int split, double m) {
+    const int nl = split, nh = nf - split;
+    auto L = [&](int i) { return m - sorted_at<NP>(k, split - 1 - i); };
+    auto H = [&](int i) { return sorted_at<NP>(k, split + i) - m; };
+    const int q = (nf - 1) / 2;                     // lower middle position
+    int lo = q + 1 - nh > 0 ? q + 1 - nh : 0;
+    int hi = q + 1 < nl ? q + 1 : nl;
+    while (lo < hi) {                               // uniform bisection
+        const int mid = (lo + hi) >> 1;
+        if (L(mid) < H(q - mid)) lo = mid + 1;
+        else hi = mid;
+    }
+    const int i = lo;                               // q + 1 smallest: i from L, q + 1 - i from H
+    double a = -__builtin_huge_val();
+    if (i > 0) a = L(i - 1);
+    if (q - i >= 0) a = fmax(a, H(q - i));
+    if (nf & 1) return a;
+    double b = __builtin_huge_val();
+    if (i < nl) b = L(i);
+    if (q + 1 - i < nh) b = fmin(b, H(q + 1 - i));
+    return (a + b) * 0.5;
+}
+
+template <int NS, int KIND>
 __global__ void __launch_bounds__(kVoteThreads) statistical_vote_wide_kernel(
-    const char* __restrict__ ev, int kind, int64_t rstride, int64_t ustride, int R, int64_t n_units,
+    const char* __restrict__ ev, int64_t rstride, int64_t ustride, int R, int64_t n_units,
     double kappa, uint8_t* __restrict__ status, uint64_t* __restrict__ bitmap,
     int32_t* __restrict__ majority_idx) {
+    // fp32 evidence is ordered and compared in fp32 (the widening to fp64 is
+    // exact and monotonic); every arithmetic step is fp64
+    using V = typename std::conditional<KIND == C3_EV_F32, float, double>::type;
     const int lane = threadIdx.x & 63;
     const int64_t u = (int64_t)blockIdx.x * kWideUnitsPerBlock + (threadIdx.x >> 6);
     if (u >= n_units) return;  // the whole wave leaves together
-    double x[NS];
+    V x[NS];
     bool fin[NS];
-    uint64_t finb[NS], B[NS];
+    uint64_t B[NS];
     int nf = 0;
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
         const int r = 64 * s + lane;
         const bool valid = r < R;
-        x[s] = valid ? load_ev_f64(ev + u * ustride + (int64_t)r * rstride, kind) : 0.0;
+        x[s] = valid ? *reinterpret_cast<const V*>(ev + u * ustride + (int64_t)r * rstride) : (V)0;
         fin[s] = valid && __builtin_isfinite(x[s]);
-        finb[s] = ballot64(fin[s]);
+        nf += __builtin_popcountll(ballot64(fin[s]));
         B[s] = ballot64(valid && !fin[s]);  // a non-finite value is an outlier
-        nf += __builtin_popcountll(finb[s]);
     }
     if (2 * nf <= R) {  // finite values are not a strict majority
 #pragma unroll
@@ -391,54 +370,53 @@ __global__ void __launch_bounds__(kVoteThreads) statistical_vote_wide_kernel(
         wide_write<NS>(u, C3_INCONCLUSIVE, B, -1, status, bitmap, majority_idx);
         return;
     }
-    // sorted copies (NP slots: NS padded to a power of two); excluded values
-    // sort last as +inf
     constexpr int NP = NS == 3 ? 4 : NS;
-    const double inf = __builtin_huge_val();
-    double sv[NP];
-    int si[NP];
+    V k[NP];
 #pragma unroll
-    for (int s = 0; s < NP; ++s) {
-        sv[s] = s < NS && fin[s < NS ? s : 0] ? x[s < NS ? s : 0] : inf;
-        si[s] = 64 * s + lane;
-    }
-    wave_sort<NP>(sv, si);
-    const double m = sorted_median<NP>(sv, nf);
-    // lower-median replica: stable position (nf - 1) / 2
-    int mj = -1;
-    const int pm = (nf - 1) / 2;
+    for (int i = 0; i < NP; ++i)
+        k[i] = i < NS && fin[i < NS ? i : 0] ? x[i < NS ? i : 0] : (V)__builtin_huge_val();
+    wave_sort<NP, 2>(k, lane);
+    const double m = sorted_median<NP>(k, nf);
+    int split = 0;                                  // finite values below m
 #pragma unroll
-    for (int s = 0; s < NP; ++s)
-        if (s == (pm >> 6)) mj = __builtin_amdgcn_readlane(si[s], pm & 63);
-    double dev[NS];
-#pragma unroll
-    for (int s = 0; s < NS; ++s) dev[s] = fin[s] ? fabs(x[s] - m) : 0.0;
-    double sd[NP];
-    int sdi[NP];
-#pragma unroll
-    for (int s = 0; s < NP; ++s) {
-        sd[s] = s < NS && fin[s < NS ? s : 0] ? dev[s < NS ? s : 0] : inf;
-        sdi[s] = 64 * s + lane;
-    }
-    wave_sort<NP>(sd, sdi);
-    double d = sorted_median<NP>(sd, nf);
+    for (int s = 0; s < NS; ++s) split += __builtin_popcountll(ballot64(fin[s] && (double)x[s] < m));
+    double d = deviation_median<NP>(k, nf, split, m);
     if (d == 0.0) {
-        const double q3 = sorted_quantile7<NP>(sv, nf, 0.75);
-        const double q1 = sorted_quantile7<NP>(sv, nf, 0.25);
+        const double q3 = sorted_quantile7<NP>(k, nf, 0.75);
+        const double q1 = sorted_quantile7<NP>(k, nf, 0.25);
         d = (q3 - q1) * 0.5;
     }
     if (d == 0.0) {
-        const double hi = sorted_at<NP>(sv, nf - 1);
-        const double lo = sorted_at<NP>(sv, 0);
+        const double hi = sorted_at<NP>(k, nf - 1);
+        const double lo = sorted_at<NP>(k, 0);
         d = (hi - lo) / (double)nf;
     }
     const double thr = kappa * d;
     bool any = false;
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
-        const bool flag = d != 0.0 && fin[s] && dev[s] > thr;
+        const bool flag = d != 0.0 && fin[s] && fabs((double)x[s] - m) > thr;
         B[s] |= ballot64(flag);
         any = any || B[s] != 0;
+    }
+    // lower-median replica: position (nf - 1) / 2 of the stable (value,
+    // replica) order is the want-th replica, by index, holding the value
+    // there, after the replicas holding smaller values
+    const int pm = (nf - 1) / 2;
+    const V target = (V)sorted_at<NP>(k, pm);
+    int want = pm;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) want -= __builtin_popcountll(ballot64(fin[s] && x[s] < target));
+    int mj = -1;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+        uint64_t eq = ballot64(fin[s] && x[s] == target);
+        const int c = __builtin_popcountll(eq);
+        if (mj < 0 && want < c) {
+            for (int w = 0; w < want; ++w) eq &= eq - 1ull;
+            mj = 64 * s + __builtin_ctzll(eq);
+        }
+        want -= c;
     }
     wide_write<NS>(u, any ? C3_ATTRIBUTED : C3_AGREE, B, mj, status, bitmap, majority_idx);
 }
@@ -450,10 +428,14 @@ static void launch_wide(const char* e, int kind, int64_t rstride, int64_t ustrid
     if (mode == C3_EXACT)
         hipLaunchKernelGGL(exact_vote_wide_kernel<NS>, dim3(blocks), dim3(kVoteThreads), 0, stream,
                            e, kind, rstride, ustride, R, n_units, status, bitmap, majority_idx);
+    else if (kind == C3_EV_F32)
+        hipLaunchKernelGGL((statistical_vote_wide_kernel<NS, C3_EV_F32>), dim3(blocks),
+                           dim3(kVoteThreads), 0, stream, e, rstride, ustride, R, n_units, kappa,
+                           status, bitmap, majority_idx);
     else
-        hipLaunchKernelGGL(statistical_vote_wide_kernel<NS>, dim3(blocks), dim3(kVoteThreads), 0,
-                           stream, e, kind, rstride, ustride, R, n_units, kappa, status, bitmap,
-                           majority_idx);
+        hipLaunchKernelGGL((statistical_vote_wide_kernel<NS, C3_EV_F64>), dim3(blocks),
+                           dim3(kVoteThreads), 0, stream, e, rstride, ustride, R, n_units, kappa,
+                           status, bitmap, majority_idx);
 }
 
 template <int NMAX>
@@ -496,34 +478,22 @@ hipError_t launch_consensus(const void* evidence, int kind, int64_t rstride, int
                              majority_idx, stream, (unsigned)blocks);
         return hipGetLastError();
     }
-    if (mode == C3_EXACT || R > 32) {
-        const int64_t blocks = (n_units + kWideUnitsPerBlock - 1) / kWideUnitsPerBlock;
-        if (blocks > 0x7FFFFFFF || R > C3_MAX_PEERS) return hipErrorInvalidValue;
-        const char* e = static_cast<const char*>(evidence);
-        const unsigned nb = (unsigned)blocks;
-        if (R <= 64)
-            launch_wide<1>(e, kind, rstride, ustride, R, n_units, mode, kappa, status, bitmap,
-                           majority_idx, stream, nb);
-        else if (R <= 128)
-            launch_wide<2>(e, kind, rstride, ustride, R, n_units, mode, kappa, status, bitmap,
-                           majority_idx, stream, nb);
-        else if (R <= 192)
-            launch_wide<3>(e, kind, rstride, ustride, R, n_units, mode, kappa, status, bitmap,
-                           majority_idx, stream, nb);
-        else
-            launch_wide<4>(e, kind, rstride, ustride, R, n_units, mode, kappa, status, bitmap,
-                           majority_idx, stream, nb);
-        return hipGetLastError();
-    }
-    // STATISTICAL, 17 <= R <= 32: lane groups of 32
-    int gw_log2 = 0;
-    while ((1 << gw_log2) < R) ++gw_log2;
-    const int64_t units_per_block = kVoteThreads >> gw_log2;
-    const int64_t blocks = (n_units + units_per_block - 1) / units_per_block;
-    if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(statistical_vote_kernel, dim3((unsigned)blocks), dim3(kVoteThreads), 0,
-                       stream, static_cast<const char*>(evidence), kind, rstride, ustride, R,
-                       gw_log2, n_units, kappa, status, bitmap, majority_idx);
+    const int64_t blocks = (n_units + kWideUnitsPerBlock - 1) / kWideUnitsPerBlock;
+    if (blocks > 0x7FFFFFFF || R > C3_MAX_PEERS) return hipErrorInvalidValue;
+    const char* e = static_cast<const char*>(evidence);
+    const unsigned nb = (unsigned)blocks;
+    if (R <= 64)
+        launch_wide<1>(e, kind, rstride, ustride, R, n_units, mode, kappa, status, bitmap,
+                       majority_idx, stream, nb);
+    else if (R <= 128)
+        launch_wide<2>(e, kind, rstride, ustride, R, n_units, mode, kappa, status, bitmap,
+                       majority_idx, stream, nb);
+    else if (R <= 192)
+        launch_wide<3>(e, kind, rstride, ustride, R, n_units, mode, kappa, status, bitmap,
+                       majority_idx, stream, nb);
+    else
+        launch_wide<4>(e, kind, rstride, ustride, R, n_units, mode, kappa, status, bitmap,
+                       majority_idx, stream, nb);
     return hipGetLastError();
 }
 

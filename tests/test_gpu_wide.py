@@ -94,10 +94,10 @@ def test_exact_consensus_wide_matches_oracle(R):
     torch.cuda.synchronize()
 
 
-@pytest.mark.parametrize("R", [17, 32, 33, 48, 64, 65, 128, 192, 256])
+@pytest.mark.parametrize("R", [17, 32, 33, 48, 64, 65, 97, 128, 129, 192, 255, 256])
 @pytest.mark.parametrize("dt", [np.float32, np.float64])
 def test_statistical_consensus_wide_matches_oracle(R, dt):
-    """R 17-32 takes the lane-per-replica kernel, above that the wave kernel."""
+    """Every R above 16 takes the wave kernel: one sort of the finite values."""
     _case("statistical wide", R, dt)
     rng = np.random.default_rng(1000 + R)
     U = 1201
@@ -112,6 +112,10 @@ def test_statistical_consensus_wide_matches_oracle(R, dt):
     tau[9::23, 64 % R] = np.nan
     tau[10::29, : R // 2] = np.inf               # finite majority only for odd R
     tau[12::31, 1::2] = -np.inf
+    tau[14::37] = np.round(tau[14::37] * 16) / 16  # few distinct values, long runs of ties
+    tau[15::41] = rng.integers(-3, 4, size=R) * 0.25  # negatives and zeros
+    tau[16::43, ::3] = -0.0                       # signed zeros among the zeros
+    tau[18::47, : (R + 1) // 2] = 3.0             # half equal: MAD 0 (odd R), median between runs (even R)
     t = tau.astype(dt)
     st, bm, mj = c3.consensus(torch.from_numpy(t).to(DEV), c3.STATISTICAL)
     ost, obm, omj = oracle.vote_statistical(t, oracle.KAPPA_DEFAULT, replica_axis=1)
