@@ -101,6 +101,7 @@ __device__ __forceinline__ void wave_lds_sync() {
 }
 
 // Loads of one kind: the wave's rows start at wbase, nbytes of them exist
+// (non-temporal: every record is read once)
 // (whole rows, at least one); loads past them re-read the last 16 bytes.
 template <int CP>
 __device__ __forceinline__ void stage_load(const char* wbase, int64_t nbytes, int lane,
@@ -109,7 +110,7 @@ __device__ __forceinline__ void stage_load(const char* wbase, int64_t nbytes, in
     for (int j = 0; j < CP; ++j) {
         int64_t off = 1024 * j + 16 * lane;
         off = off < nbytes - 16 ? off : nbytes - 16;
-        g[j] = *reinterpret_cast<const vu32x4*>(wbase + off);
+        g[j] = __builtin_nontemporal_load(reinterpret_cast<const vu32x4*>(wbase + off));
     }
 }
 
@@ -369,7 +370,8 @@ struct PassShape {
 // Loads of one kind for one wave step: row i of the step (i = 0..63) is unit
 // (t0 + i / kPassGroups, g0 + i % kPassGroups), RB = 16 CP bytes long; load j
 // of lane l reads the step's bytes 1024 j + 16 l.  Rows outside the T x ng
-// block read row (0, g0) instead; their lanes store nothing.
+// block read row (0, g0) instead; their lanes store nothing.  Non-temporal:
+// every record is read once.
 template <int CP>
 __device__ __forceinline__ void pass_load(const char* __restrict__ base, int64_t G, int64_t T,
                                           int64_t g0, int ng, int64_t t0, int lane,
@@ -383,7 +385,7 @@ __device__ __forceinline__ void pass_load(const char* __restrict__ base, int64_t
         const int64_t t = t0 + ti;
         const bool ok = t < T && gi < ng;
         const int64_t off = ok ? (t * G + g0 + gi) * RB + (b % RB) : g0 * RB;
-        g[j] = *reinterpret_cast<const vu32x4*>(base + off);
+        g[j] = __builtin_nontemporal_load(reinterpret_cast<const vu32x4*>(base + off));
     }
 }
 
@@ -413,7 +415,8 @@ __device__ __forceinline__ void pass_load_full(const char* __restrict__ base, in
     constexpr int RB = 16 * CP;
     const char* step = base + (t0 * G + g0) * RB;
 #pragma unroll
-    for (int j = 0; j < CP; ++j) g[j] = *reinterpret_cast<const vu32x4*>(step + off[j]);
+    for (int j = 0; j < CP; ++j)
+        g[j] = __builtin_nontemporal_load(reinterpret_cast<const vu32x4*>(step + off[j]));
 }
 
 template <int NMAX, int KIND, bool SHORT>
