@@ -348,14 +348,14 @@ __global__ void __launch_bounds__(kConfirmThreads) timing_confirm_kernel(
 // step's rows of one kind are kPassIters contiguous runs of kPassGroups
 // rows, read with 16-byte loads and passed through the wave's LDS region as
 // in the staged kernel (lane l takes back row l: iteration t0 + l /
-// kPassGroups, group g0 + l % kPassGroups).  Used when no per-unit results
-// are requested, R equals the group bound, both kinds' rows are 16-byte
-// aligned, the masks fit kPassMaskLds bytes and there are at least as many
-// workgroups as compute units.  Per-unit results would be written here as
-// 16- to 128-byte pieces of each iteration's row: measured on the 32,768-
-// rank workload the pass then took 117 us against 115 us for the three
-// launches, whose workgroups write whole runs of consecutive units, so
-// calls that want them take the three launches.
+// kPassGroups, group g0 + l % kPassGroups).  Used without per-unit results
+// or with those of both kinds, when R equals the group bound, both kinds'
+// rows are 16-byte aligned, the masks fit kPassMaskLds bytes and there are
+// at least as many workgroups as compute units.  Per-unit results are
+// written as 16- to 128-byte pieces of each iteration's row; on the
+// 32,768-rank workload the pass then takes 101.9 us of kernel time against
+// 106.2 us for the three launches of the workspace path (clear, votes,
+// confirmation), which per-unit results of one kind only still take.
 // ---------------------------------------------------------------------------
 constexpr int kPassGroups = 16;                  // groups per workgroup
 constexpr int kPassIters = 64 / kPassGroups;     // iterations per wave step
@@ -365,6 +365,16 @@ constexpr int64_t kPassMaskLds = 64 * 1024;      // LDS bytes for the masks
 // iterations (R = 8) 71.3 us per call against 73.0 us with sixteen; the
 // streaming loop alone takes 60 us either way, the votes and the final
 // confirmation account for the rest.
+// Group block of workgroup b: with a grid of a multiple of eight workgroups,
+// the blocks that the hardware sends to one XCD (b mod 8) are consecutive,
+// so a cache line of per-unit results, which spans the groups of eight
+// neighbouring blocks, is written through a single L2 (108.8 against 110.8
+// us per call with per-unit results on 32,768 ranks x 1,024 iterations).
+__device__ __forceinline__ int64_t pass_group_block(unsigned b, unsigned n) {
+    if (n % 8u != 0u) return b;
+    return (int64_t)(b % 8u) * (n / 8u) + b / 8u;
+}
+
 template <int NMAX>
 struct PassShape {
     static constexpr int waves = 8;
@@ -374,8 +384,8 @@ struct PassShape {
 // Loads of one kind for one wave step: row i of the step (i = 0..63) is unit
 // (t0 + i / kPassGroups, g0 + i % kPassGroups), RB = 16 CP bytes long; load j
 // of lane l reads the step's bytes 1024 j + 16 l.  Rows outside the T x ng
-// block read row (0, g0) instead; their lanes store nothing.  Non-temporal:
-// every record is read once.
+// block read row (0, g0) instead, whole.  Non-temporal: every record is read
+// once.
 template <int CP>
 __device__ __forceinline__ void pass_load(const char* __restrict__ base, int64_t G, int64_t T,
                                           int64_t g0, int ng, int64_t t0, int lane,
@@ -388,7 +398,7 @@ __device__ __forceinline__ void pass_load(const char* __restrict__ base, int64_t
         const int ti = row / kPassGroups, gi = row % kPassGroups;
         const int64_t t = t0 + ti;
         const bool ok = t < T && gi < ng;
-        const int64_t off = ok ? (t * G + g0 + gi) * RB + (b % RB) : g0 * RB;
+        const int64_t off = (ok ? (t * G + g0 + gi) * RB : g0 * RB) + (b % RB);
         g[j] = __builtin_nontemporal_load(reinterpret_cast<const vu32x4*>(base + off));
     }
 }
@@ -423,10 +433,10 @@ __device__ __forceinline__ void pass_load_full(const char* __restrict__ base, in
         g[j] = __builtin_nontemporal_load(reinterpret_cast<const vu32x4*>(step + off[j]));
 }
 
-template <int NMAX, int KIND, bool SHORT>
+template <int NMAX, int KIND, bool SHORT, bool PU>
 __global__ void __launch_bounds__(PassShape<NMAX>::threads) timing_pass_kernel(
     const char* __restrict__ fp, const char* __restrict__ tp, int64_t G, int64_t T, double kappa,
-    int Wt, c3_rank_verdict_t* __restrict__ verdicts) {
+    int Wt, c3_rank_verdict_t* __restrict__ verdicts, VoteOut fo, VoteOut to) {
     constexpr int R = NMAX;
     constexpr int NW = PassShape<NMAX>::waves;
     constexpr int CPF = NMAX / 2;                                // u64 fingerprints
@@ -437,7 +447,10 @@ __global__ void __launch_bounds__(PassShape<NMAX>::threads) timing_pass_kernel(
     const int lane = threadIdx.x & 63;
     // the wave index, uniform across the wave (keeps the step addresses scalar)
     const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
-    const int64_t g0 = (int64_t)blockIdx.x * kPassGroups;
+    // per-unit results: XCD-aware block order (pass_group_block); without
+    // them the plain order reads faster (81.2 against 83.4 us per call)
+    const int64_t g0 = (PU ? pass_group_block(blockIdx.x, gridDim.x) : (int64_t)blockIdx.x) *
+                       kPassGroups;
     const int ng = G - g0 < kPassGroups ? (int)(G - g0) : kPassGroups;
     const int64_t n_seg = (T + kSegIters - 1) / kSegIters;
     uint32_t* fmask = pass_masks;
@@ -466,8 +479,7 @@ __global__ void __launch_bounds__(PassShape<NMAX>::threads) timing_pass_kernel(
         }
     };
     vu32x4 gf[CPF], gt[CPT];
-    if (wave < n_steps) load_step((int64_t)wave * kPassIters, gf, gt);
-    for (int64_t st = wave; st < n_steps; st += NW) {
+    auto do_step = [&](int64_t st) {
         const int64_t t0 = st * kPassIters;
         vu32x4 vf[CPF], vt[CPT];
         stage_swap<CPF>(stage[wave], lane, gf, vf);
@@ -475,7 +487,7 @@ __global__ void __launch_bounds__(PassShape<NMAX>::threads) timing_pass_kernel(
         const int64_t tn = (st + NW < n_steps ? st + NW : st) * kPassIters;
         load_step(tn, gf, gt);
         const int64_t t = t0 + ti;
-        if (t >= T || gi >= ng) continue;
+        const bool valid = t < T && gi < ng;
         uint64_t ef[NMAX], et[NMAX];
 #pragma unroll
         for (int c = 0; c < CPF; ++c) {
@@ -495,14 +507,37 @@ __global__ void __launch_bounds__(PassShape<NMAX>::threads) timing_pass_kernel(
             }
         }
         const UnitVote vfp = exact_vote_row<NMAX>(ef, R);
-        // only the bitmaps reach the masks: no lower-median replica
-        const UnitVote vtm = statistical_vote_row<NMAX, KIND, false>(et, R, kappa);
+        // without per-unit results only the bitmaps are kept: no lower-median replica
+        const UnitVote vtm = statistical_vote_row<NMAX, KIND, PU>(et, R, kappa);
+        if constexpr (PU) {
+            // Every lane stores: a path without the stores would make the
+            // wait for the next step's loads cover them.  A lane outside
+            // the block holds the row it loaded instead -- (t, g0) in a whole
+            // step, (0, g0) in the last one -- and writes that unit's
+            // results again, unchanged.
+            const int64_t u = valid ? t * G + g0 + gi : (t0 + kPassIters <= T ? t * G + g0 : g0);
+            fo.status[u] = vfp.status;
+            fo.bitmap[u] = vfp.bitmap;
+            fo.majority[u] = vfp.majority;
+            to.status[u] = vtm.status;
+            to.bitmap[u] = vtm.bitmap;
+            to.majority[u] = vtm.majority;
+        }
+        if (!valid) return;
         const uint32_t bit = 1u << (t & (kSegIters - 1));
         const int64_t w0 = (t / kSegIters) * SEGW + gi;
         for (uint64_t b = vfp.bitmap; b != 0ull; b &= b - 1ull)
             atomicOr(fmask + w0 + __builtin_ctzll(b) * kPassGroups, bit);
         for (uint64_t b = vtm.bitmap; b != 0ull; b &= b - 1ull)
             atomicOr(tmask + w0 + __builtin_ctzll(b) * kPassGroups, bit);
+    };
+    if (wave < n_steps) {
+        load_step((int64_t)wave * kPassIters, gf, gt);
+        // The first step outside the loop, so that every path into the
+        // loop ends with one step's loads and then (with per-unit results)
+        // its stores, and the waits for the loads never cover the stores.
+        do_step(wave);
+        for (int64_t st = wave + NW; st < n_steps; st += NW) do_step(st);
     }
     __syncthreads();
 
@@ -561,15 +596,23 @@ static hipError_t launch_votes(const uint64_t* fp, const char* tp, int time_kind
 
 template <int NMAX, int KIND>
 static hipError_t launch_pass(const char* fp, const char* tp, int64_t G, int64_t T, double kappa,
-                              int Wt, c3_rank_verdict_t* verdicts, size_t lds, hipStream_t stream) {
+                              int Wt, c3_rank_verdict_t* verdicts, const VoteOut& fo,
+                              const VoteOut& to, size_t lds, hipStream_t stream) {
     const dim3 grid((unsigned)((G + kPassGroups - 1) / kPassGroups));
     const dim3 block(PassShape<NMAX>::threads);
-    if (Wt <= 32)
-        hipLaunchKernelGGL((timing_pass_kernel<NMAX, KIND, true>), grid, block, lds, stream, fp, tp,
-                           G, T, kappa, Wt, verdicts);
+    const bool pu = fo.status != nullptr;
+    if (Wt <= 32 && pu)
+        hipLaunchKernelGGL((timing_pass_kernel<NMAX, KIND, true, true>), grid, block, lds, stream,
+                           fp, tp, G, T, kappa, Wt, verdicts, fo, to);
+    else if (Wt <= 32)
+        hipLaunchKernelGGL((timing_pass_kernel<NMAX, KIND, true, false>), grid, block, lds, stream,
+                           fp, tp, G, T, kappa, Wt, verdicts, fo, to);
+    else if (pu)
+        hipLaunchKernelGGL((timing_pass_kernel<NMAX, KIND, false, true>), grid, block, lds, stream,
+                           fp, tp, G, T, kappa, Wt, verdicts, fo, to);
     else
-        hipLaunchKernelGGL((timing_pass_kernel<NMAX, KIND, false>), grid, block, lds, stream, fp,
-                           tp, G, T, kappa, Wt, verdicts);
+        hipLaunchKernelGGL((timing_pass_kernel<NMAX, KIND, false, false>), grid, block, lds,
+                           stream, fp, tp, G, T, kappa, Wt, verdicts, fo, to);
     return hipGetLastError();
 }
 
@@ -602,21 +645,24 @@ hipError_t launch_timing_consensus(const uint64_t* fp, const void* times, int ti
     if ((ranks * kConfirmLanes + kConfirmThreads - 1) / kConfirmThreads > 0x7FFFFFFF)
         return hipErrorInvalidValue;
     if (ranks == 0) return hipSuccess;
-    if (fp_status == nullptr && t_status == nullptr) {
+    // the single pass: verdicts only, or with the per-unit results of both kinds
+    if ((fp_status == nullptr) == (t_status == nullptr)) {
         const int Wt = (int64_t)window < T ? window : (int)T;
         size_t lds = 0;
         if (pass_applies(fp, times, time_kind, R, G, T, Wt, stream, lds)) {
             const char* f = reinterpret_cast<const char*>(fp);
             const char* tp = static_cast<const char*>(times);
             const bool f64 = time_kind == C3_EV_F64;
+            const VoteOut fo = {fp_status, fp_bitmap, fp_majority, nullptr};
+            const VoteOut to = {t_status, t_bitmap, t_majority, nullptr};
             if (R == 4)
-                return f64 ? launch_pass<4, C3_EV_F64>(f, tp, G, T, kappa, Wt, verdicts, lds, stream)
-                           : launch_pass<4, C3_EV_F32>(f, tp, G, T, kappa, Wt, verdicts, lds, stream);
+                return f64 ? launch_pass<4, C3_EV_F64>(f, tp, G, T, kappa, Wt, verdicts, fo, to, lds, stream)
+                           : launch_pass<4, C3_EV_F32>(f, tp, G, T, kappa, Wt, verdicts, fo, to, lds, stream);
             if (R == 8)
-                return f64 ? launch_pass<8, C3_EV_F64>(f, tp, G, T, kappa, Wt, verdicts, lds, stream)
-                           : launch_pass<8, C3_EV_F32>(f, tp, G, T, kappa, Wt, verdicts, lds, stream);
-            return f64 ? launch_pass<16, C3_EV_F64>(f, tp, G, T, kappa, Wt, verdicts, lds, stream)
-                       : launch_pass<16, C3_EV_F32>(f, tp, G, T, kappa, Wt, verdicts, lds, stream);
+                return f64 ? launch_pass<8, C3_EV_F64>(f, tp, G, T, kappa, Wt, verdicts, fo, to, lds, stream)
+                           : launch_pass<8, C3_EV_F32>(f, tp, G, T, kappa, Wt, verdicts, fo, to, lds, stream);
+            return f64 ? launch_pass<16, C3_EV_F64>(f, tp, G, T, kappa, Wt, verdicts, fo, to, lds, stream)
+                       : launch_pass<16, C3_EV_F32>(f, tp, G, T, kappa, Wt, verdicts, fo, to, lds, stream);
         }
     }
     const int64_t half = timing_masks_bytes(R, G, T) / 2;

@@ -103,7 +103,8 @@ CASES = [
 
 
 # Shapes of the single-pass kernel (taken when no per-unit results are
-# requested): R a group bound (4, 8, 16), at least one 16-group workgroup per
+# requested, or those of both kinds): R a group bound (4, 8, 16), at least one
+# 16-group workgroup per
 # compute unit (G >= 4081 on 256 CUs), masks within the LDS budget (T <= 2048
 # at R = 8).  Ragged G leaves the last workgroup 1-15 groups; ragged T leaves
 # a partial 4-iteration step and a partial 32-iteration mask segment.
@@ -114,18 +115,52 @@ PASS_CASES = [
 ]
 
 
-@pytest.mark.parametrize("R,G,T,W,f64", CASES + PASS_CASES[:3])
+@pytest.mark.parametrize("R,G,T,W,f64", CASES)
 def test_timing_consensus_matches_oracle(R, G, T, W, f64):
     _case("timing", R, G, T, W, f64)
     fp, tau = _inputs(R, G, T, seed=R * 1000 + G * 7 + T, f64=f64)
     _check(fp, tau, W)
 
 
+@pytest.mark.parametrize("per_unit", [False, True])
 @pytest.mark.parametrize("R,G,T,W,f64", PASS_CASES)
-def test_timing_consensus_single_pass_matches_oracle(R, G, T, W, f64):
-    _case("timing single pass", R, G, T, W, f64)
+def test_timing_consensus_single_pass_matches_oracle(R, G, T, W, f64, per_unit):
+    _case("timing single pass", R, G, T, W, f64, per_unit)
     fp, tau = _inputs(R, G, T, seed=R * 1000 + G * 7 + T, f64=f64)
-    _check(fp, tau, W, per_unit=False)
+    _check(fp, tau, W, per_unit=per_unit)
+
+
+@pytest.mark.parametrize("kind", ["fp", "time"])
+def test_timing_consensus_per_unit_results_of_one_kind(kind):
+    """Per-unit results of one kind only take the separate launches; the
+    other kind's outputs stay untouched."""
+    import ctypes
+    _case("timing one kind", kind)
+    R, G, T, W = 8, 4100, 37, 16
+    fp, tau = _inputs(R, G, T, seed=77)
+    (ost, obm, omj), (sst, sbm, smj), ref = _oracle(fp, tau, W)
+    dfp, dtau = torch.from_numpy(fp).to(DEV), torch.from_numpy(tau).to(DEV)
+    outs = (torch.full((T * G,), 0xEE, dtype=torch.uint8, device=DEV),
+            torch.full((T * G,), -5, dtype=torch.int64, device=DEV),
+            torch.full((T * G,), -7, dtype=torch.int32, device=DEV))
+    ver = torch.empty((R * G, 24), dtype=torch.uint8, device=DEV)
+    ws = torch.empty(c3.timing_consensus_workspace_size(R, G, T, W), dtype=torch.uint8, device=DEV)
+    p = lambda x: ctypes.c_void_p(x.data_ptr())
+    null = ctypes.c_void_p(0)
+    fo = tuple(p(x) for x in outs) if kind == "fp" else (null, null, null)
+    to = tuple(p(x) for x in outs) if kind == "time" else (null, null, null)
+    rc = c3.lib().c3_timing_consensus(p(dfp), p(dtau), c3.EV_F32, R, G, T, c3.KAPPA_DEFAULT, W,
+                                      *fo, *to, p(ver), p(ws), ws.numel(), null)
+    assert rc == 0
+    torch.cuda.synchronize()
+    st, bm, mj = (ost, obm, omj) if kind == "fp" else (sst, sbm, smj)
+    assert np.array_equal(outs[0].cpu().numpy(), st)
+    assert np.array_equal(outs[1].cpu().numpy().view(np.uint64), bm)
+    assert np.array_equal(outs[2].cpu().numpy(), mj)
+    v = c3.verdicts_numpy(ver)
+    assert np.array_equal(v["flags"], ref["flags"])
+    assert np.array_equal(v["slow_count"], ref["slow_count"])
+    assert np.array_equal(v["first_straggler_window"], ref["first_window"])
 
 
 @pytest.mark.parametrize("R,G,T,W", [(8, 100, 70, 16), (12, 70, 50, 16), (20, 10, 30, 16)])
