@@ -184,7 +184,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=None)
-    ap.add_argument("--config", type=int, default=3, choices=[1, 2, 3, 4, 5, 6, 7])
+    ap.add_argument("--config", type=int, default=3, choices=[1, 2, 3, 4, 5, 6, 7, 8])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--copy-calibration", action="store_true")
@@ -209,6 +209,8 @@ def main():
         return bench_timing(args, torch, workloads, c3, dev)
     if args.config == 6:
         return bench_optimizer(args, torch, workloads, c3, dev)
+    if args.config == 8:
+        return bench_wide(args, torch, workloads, c3, dev)
     log(f"[bench] generating config {args.config}")
     w = workloads.make(args.config, device=dev, scale="full")
     torch.cuda.synchronize()
@@ -418,8 +420,8 @@ def _kernel_ms(torch, fn, reps):
 
 def bench_timing(args, torch, workloads, c3, dev):
     """Progress/timing consensus: exact vote on fingerprints, statistical vote
-    on step times and temporal confirmation (c3_timing_consensus, fused
-    kernels), one step per pass over all records; per-unit results are
+    on step times and temporal confirmation (c3_timing_consensus, one kernel
+    on this shape), one step per pass over all records; per-unit results are
     written."""
     log("[bench] generating config 5")
     w = workloads.make(5, device=dev, scale="full")
@@ -472,11 +474,11 @@ def bench_timing(args, torch, workloads, c3, dev):
         c3.consensus(w.times, c3.STATISTICAL, out=sep_t)
         c3.confirm(sep_f[1].view(T, G), sep_t[1].view(T, G), R, 16, out=ver, workspace=cws)
     ms_sep = timed(separate)
-    # per-rank outlier masks: one 32-bit word per (kind, 32 iterations, rank),
-    # cleared and read once in the three-launch path
-    masks = 2 * 4 * (-(-T // 32)) * R * G
-    pass_bytes = U * R * (8 + 4) + 2 * U * 13 + masks + masks + R * G * 24
-    # the single pass (no per-unit results) reads the records and writes verdicts
+    # the single pass reads the records once and writes the per-unit results
+    # (status 1 + bitmap 8 + majority 4 bytes per unit and kind) and the
+    # verdicts; the outlier masks stay in LDS
+    pass_bytes = U * R * (8 + 4) + 2 * U * 13 + R * G * 24
+    # without per-unit results: the records and the verdicts
     vo_bytes = U * R * (8 + 4) + R * G * 24
     out = {
         "metric": "timing+fingerprint records GB/s voted+confirmed",
@@ -497,7 +499,7 @@ def bench_timing(args, torch, workloads, c3, dev):
         "roofline": {"bound": "hbm", "achieved": round(pass_bytes / (ms * 1e-3) / 1e9, 2),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(pass_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
-                     "traffic": None, "kernel": "timing_zero_kernel+timing_votes_staged_kernel+timing_confirm_kernel",
+                     "traffic": None, "kernel": "timing_pass_kernel (per-unit results)",
                      "kernel_ms": round(ms, 4), "algorithmic_bytes_per_launch": pass_bytes},
         "ms_per_step_verdicts_only": round(ms_verdicts, 4),
         "roofline_verdicts_only": {"bound": "hbm", "achieved": round(vo_bytes / (ms_verdicts * 1e-3) / 1e9, 2),
@@ -507,6 +509,46 @@ def bench_timing(args, torch, workloads, c3, dev):
         "ms_per_step_separate_calls": round(ms_sep, 4),
         "wall_s_timed": round(wall, 3),
     }
+    print(json.dumps(out), flush=True)
+
+
+def bench_wide(args, torch, workloads, c3, dev):
+    """Votes over wide peer groups (gathered tables of 33 to 256 peers): per
+    group size R, c3_consensus on 262,144 units, STATISTICAL on fp32 and fp64
+    step times and EXACT on 64-bit fingerprints; mean ms per call between
+    HIP events over `steps` calls."""
+    U = 1 << 18
+    rows = []
+    for R in (17, 33, 64, 65, 128, 129, 192, 256):
+        tau32, fp = workloads.wide_votes(R, U, device=dev)
+        tau64 = tau32.double()
+        line = {"R": R}
+        for name, ev, mode in (("stat_f32", tau32, c3.STATISTICAL), ("stat_f64", tau64, c3.STATISTICAL),
+                               ("exact_u64", fp, c3.EXACT)):
+            out = c3.consensus(ev, mode)
+            warm_up(torch, lambda: c3.consensus(ev, mode, out=out), args.warmup or 5)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            e0.record()
+            for _ in range(args.steps):
+                c3.consensus(ev, mode, out=out)
+            e1.record()
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / args.steps
+            line[name + "_ms"] = round(ms, 4)
+            line[name + "_GBps"] = round(ev.numel() * ev.element_size() / (ms * 1e-3) / 1e9, 1)
+            if name == "stat_f32":
+                st = out[0].cpu()
+                line["attributed_units"] = int((st == c3.ATTRIBUTED).sum())
+        rows.append(line)
+        log(f"[bench] wide R={R}: {line}")
+        del tau32, tau64, fp
+    out = {"metric": "wide-group consensus ms per 262,144 units", "value": rows[-1]["stat_f32_ms"],
+           "unit": "ms", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup or 5,
+           "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": "f32/f64/u64",
+           "data": "synthetic",
+           "config": {"workload": "wide_groups_units262144", "units": U, "layout": "unit-major [U][R]"},
+           "per_R": rows}
     print(json.dumps(out), flush=True)
 
 

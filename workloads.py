@@ -354,6 +354,32 @@ def config6(device="cuda", scale="full") -> OptimizerWorkload:
 CONFIGS = {1: config1, 2: config2, 3: config3, 4: config4, 5: config5, 6: config6}
 
 
+# --------------------------------------------------------------------------
+# wide peer groups (the vote over gathered tables of 33 to 256 peers, Table 2's
+# data-parallel degrees): U units x R peers, unit-major.  Step times
+# ~LogNormal(ln 1 s, 0.02) in fp32, with a 1.5x slow peer in every 7th unit,
+# a tie in every 11th, a majority of equal values (MAD 0: the IQR fallback)
+# in every 13th, a NaN in every 23rd; fingerprints: one seeded 64-bit value
+# per unit on every peer, one peer changed in every 9th unit and a two-way
+# split in every 97th.
+# --------------------------------------------------------------------------
+def wide_votes(R: int, U: int, device="cuda", seed: int = 8):
+    gen = torch.Generator(device=device)
+    gen.manual_seed(seed * 1000 + R)
+    tau = torch.randn((U, R), generator=gen, device=device, dtype=torch.float32)
+    tau.mul_(0.02).exp_()
+    tau[::7, 0] *= 1.5
+    tau[::11, R // 3] = tau[::11, 1]
+    tau[3::13, : R // 2 + 1] = 1.0
+    tau[9::23, R - 1] = float("nan")
+    lo, hi = -(2 ** 63), 2 ** 63 - 1
+    fp = torch.randint(lo, hi, (U, 1), generator=gen, device=device, dtype=torch.int64)
+    fp = fp.expand(U, R).contiguous()
+    fp[::9, R - 1] ^= 0x5A5A
+    fp[::97, : R // 2] ^= 3
+    return tau, fp
+
+
 def make(k: int, device="cuda", scale="full"):
     return CONFIGS[k](device=device, scale=scale)
 
