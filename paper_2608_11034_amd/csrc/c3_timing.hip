@@ -252,7 +252,9 @@ __device__ __forceinline__ ConfirmAcc confirm_lane(const uint32_t* fpm, const ui
                 // when all set bits of (segment : previous) could not.
                 const uint32_t ybits = (uint32_t)__builtin_popcount(tm) + __builtin_popcount(prev);
                 if (SHORT) {
-                    if ((ybits > a.mw || (2u * ybits > (uint32_t)Wt && a.fw < 0)) && lo_i < hi_i) {
+                    // a window holds at most Wt iterations
+                    const uint32_t ycap = ybits < (uint32_t)Wt ? ybits : (uint32_t)Wt;
+                    if ((ycap > a.mw || (2u * ycap > (uint32_t)Wt && a.fw < 0)) && lo_i < hi_i) {
                         // A window count only grows when a set bit enters, so
                         // the maximum and the first window over the threshold
                         // end at a set bit -- or at the lane's first window
@@ -271,10 +273,14 @@ __device__ __forceinline__ ConfirmAcc confirm_lane(const uint32_t* fpm, const ui
                             a.mw = c > a.mw ? c : a.mw;
                             if (2u * c > (uint32_t)Wt && a.fw < 0)
                                 a.fw = (int32_t)(t_lo + (int64_t)(q0 + i - wlo));
+                            // a full window: no later one raises the maximum
+                            // or comes first (a rank slow in every iteration)
+                            if (a.mw >= (uint32_t)Wt && a.fw >= 0) break;
                         }
                     }
                 } else {
-                    if ((tm != 0u || hist != 0ull)) {
+                    // once a window is full nothing the windows give can change
+                    if ((tm != 0u || hist != 0ull) && !(a.mw >= (uint32_t)Wt && a.fw >= 0)) {
                         for (uint32_t i = 0; i < n; ++i) {
                             hist = (hist << 1) | ((tm >> i) & 1u);
                             if (i >= lo_i && i < hi_i) {
