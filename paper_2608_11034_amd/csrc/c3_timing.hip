@@ -299,22 +299,23 @@ __device__ __forceinline__ ConfirmAcc confirm_lane(const uint32_t* fpm, const ui
     return a;
 }
 
-// Combines the kConfirmLanes lanes of one rank (sums, maxima, first --
-// smallest non-negative -- positions); lane `part` 0 of a live rank writes
-// its verdict.  Every lane of the wave must call it.
+// Combines the L lanes of one rank (sums, maxima, first -- smallest
+// non-negative -- positions); lane `part` 0 of a live rank writes its
+// verdict.  Every lane of the wave must call it.
+template <int L = kConfirmLanes>
 __device__ __forceinline__ void confirm_store(ConfirmAcc a, bool live, int part,
                                               c3_rank_verdict_t* __restrict__ verdicts,
                                               int64_t rank) {
 #pragma unroll
-    for (int o = 1; o < kConfirmLanes; o <<= 1) {
-        a.flags |= (uint32_t)__shfl_xor((int)a.flags, o, kConfirmLanes);
-        a.dc += (uint32_t)__shfl_xor((int)a.dc, o, kConfirmLanes);
-        a.sc += (uint32_t)__shfl_xor((int)a.sc, o, kConfirmLanes);
-        const uint32_t m2 = (uint32_t)__shfl_xor((int)a.mw, o, kConfirmLanes);
+    for (int o = 1; o < L; o <<= 1) {
+        a.flags |= (uint32_t)__shfl_xor((int)a.flags, o, L);
+        a.dc += (uint32_t)__shfl_xor((int)a.dc, o, L);
+        a.sc += (uint32_t)__shfl_xor((int)a.sc, o, L);
+        const uint32_t m2 = (uint32_t)__shfl_xor((int)a.mw, o, L);
         a.mw = m2 > a.mw ? m2 : a.mw;
-        const int32_t f2 = __shfl_xor(a.fd, o, kConfirmLanes);
+        const int32_t f2 = __shfl_xor(a.fd, o, L);
         a.fd = (a.fd < 0 || (f2 >= 0 && f2 < a.fd)) ? f2 : a.fd;
-        const int32_t w2 = __shfl_xor(a.fw, o, kConfirmLanes);
+        const int32_t w2 = __shfl_xor(a.fw, o, L);
         a.fw = (a.fw < 0 || (w2 >= 0 && w2 < a.fw)) ? w2 : a.fw;
     }
     if (!live || part != 0) return;
@@ -328,6 +329,77 @@ __device__ __forceinline__ void confirm_store(ConfirmAcc a, bool live, int part,
     v.max_window_slow = a.mw;
     v.first_straggler_window = a.fw;
     verdicts[rank] = v;
+}
+
+// Confirmation of one rank from masks in LDS, windows of at most 32
+// iterations, by L lanes: lane `part` owns segments [part * per, part * per
+// + per) and evaluates every window that ends in them, so it reads nothing
+// past its own segments (the segment before its first gives the bits that
+// windows ending early in it reach back to).  Within a segment a window's
+// count rises only where a set bit enters, so the windows evaluated are
+// those ending at a set bit or at the segment's first position.  A window
+// ending before position Wt - 1 is a prefix of the first whole window
+// (start 0) and never counts more, so it is evaluated as if whole, with its
+// start clamped to 0: it raises the maximum or passes the threshold only
+// when the first whole window does.  All arithmetic is 32-bit and the loop
+// count is the same on every lane.
+template <int L>
+__device__ __forceinline__ ConfirmAcc confirm_owned(const uint32_t* fpm, const uint32_t* tpm,
+                                                    int stride, int n_seg, int Wt, int part,
+                                                    bool live) {
+    const int per = (n_seg + L - 1) / L;
+    const int s_lo = part * per;
+    const uint32_t w = (uint32_t)Wt;
+    const uint32_t wm = w >= 32u ? ~0u : (1u << w) - 1u;
+    ConfirmAcc a{0u, 0u, 0u, 0u, -1, -1};
+    uint32_t pairs = 0u;
+    uint32_t prev = live && s_lo > 0 && s_lo <= n_seg ? tpm[(s_lo - 1) * stride] : 0u;
+    for (int j = 0; j < per; ++j) {
+        const int sg = s_lo + j;
+        const bool in = live && sg < n_seg;
+        const uint32_t f = in ? fpm[sg * stride] : 0u;
+        const uint32_t tm = in ? tpm[sg * stride] : 0u;
+        if (f != 0u && a.fd < 0) a.fd = sg * kSegIters + __builtin_ctz(f);
+        a.dc += (uint32_t)__builtin_popcount(f);
+        const uint32_t nt = (uint32_t)__builtin_popcount(tm);
+        a.sc += nt;
+        pairs |= tm & ((tm << 1) | (prev >> 31));
+        // a window ending here holds at most the set bits of this segment
+        // and the previous one, and at most Wt
+        const uint32_t yb = nt + (uint32_t)__builtin_popcount(prev);
+        const uint32_t ycap = yb < w ? yb : w;
+        if (ycap > a.mw || (2u * ycap > w && a.fw < 0)) {
+            const uint64_t y = ((uint64_t)tm << 32) | prev;
+            const int st0 = sg * kSegIters - Wt + 1;    // start of the window ending at position 0
+            auto window = [&](uint32_t i) {
+                const uint32_t c = (uint32_t)__builtin_popcount((uint32_t)(y >> (33u + i - w)) & wm);
+                a.mw = c > a.mw ? c : a.mw;
+                if (2u * c > w && a.fw < 0) a.fw = st0 + (int)i > 0 ? st0 + (int)i : 0;
+            };
+            // The first position and the two lowest set bits without a
+            // branch (a missing bit repeats position 0), so that a wave loops
+            // only where a lane has a third set bit in this segment; the
+            // windows are taken in ascending order, so the first over the
+            // threshold is the one kept.
+            window(0u);
+            uint32_t ev = tm & ~1u;
+            const uint32_t i1 = ev != 0u ? (uint32_t)__builtin_ctz(ev) : 0u;
+            ev &= ev - 1u;
+            window(i1);
+            const uint32_t i2 = ev != 0u ? (uint32_t)__builtin_ctz(ev) : 0u;
+            ev &= ev - 1u;
+            window(i2);
+            // a full window: no later one raises the maximum or comes first
+            while (ev != 0u && !(a.mw >= w && a.fw >= 0)) {
+                const uint32_t i = (uint32_t)__builtin_ctz(ev);
+                ev &= ev - 1u;
+                window(i);
+            }
+        }
+        prev = tm;
+    }
+    if (pairs != 0u) a.flags |= C3_RANK_CONSEC2;
+    return a;
 }
 
 template <bool SHORT>
@@ -349,7 +421,9 @@ __global__ void __launch_bounds__(kConfirmThreads) timing_confirm_kernel(
 // groups over all T iterations, so every outlier bit of its ranks lands in
 // its own LDS: the votes OR the bits into per-rank masks [kind][segment][r]
 // [group] there (no global atomics and no clearing launch), and after one
-// workgroup barrier the same workgroup confirms its ranks from LDS.  A
+// workgroup barrier the same workgroup confirms its ranks from LDS (windows
+// of at most 32 iterations: every rank at once, its segments split among
+// the lanes left per rank, confirm_owned).  A
 // wave's step is 64 units, kPassIters iterations x kPassGroups groups; the
 // step's rows of one kind are kPassIters contiguous runs of kPassGroups
 // rows, read with 16-byte loads and passed through the wave's LDS region as
@@ -367,10 +441,12 @@ constexpr int kPassGroups = 16;                  // groups per workgroup
 constexpr int kPassIters = 64 / kPassGroups;     // iterations per wave step
 constexpr int64_t kPassMaskLds = 64 * 1024;      // LDS bytes for the masks
 
-// Eight waves per workgroup, two per SIMD: on 32,768 ranks x 1,024
-// iterations (R = 8) 71.3 us per call against 73.0 us with sixteen; the
-// streaming loop alone takes 60 us either way, the votes and the final
-// confirmation account for the rest.
+// Eight waves per workgroup, two per SIMD.  On 32,768 ranks x 1,024
+// iterations (R = 8, one workgroup per compute unit), per call with HIP
+// events, verdicts only / with per-unit results: 79.0 / 110.8 us; sixteen
+// waves 78.8 / 116.4 (the per-unit form spills at 128 VGPRs); eight groups
+// per workgroup, two workgroups per compute unit, 79.7 / 121.2; two steps
+// of loads in flight per wave 81.5 us verdicts only.
 // Group block of workgroup b: with a grid of a multiple of eight workgroups,
 // the blocks that the hardware sends to one XCD (b mod 8) are consecutive,
 // so a cache line of per-unit results, which spans the groups of eight
@@ -547,7 +623,22 @@ __global__ void __launch_bounds__(PassShape<NMAX>::threads) timing_pass_kernel(
     }
     __syncthreads();
 
-    // confirmation of the workgroup's ranks (r, g0 + gi), kConfirmLanes lanes each
+    // confirmation of the workgroup's ranks (r, g0 + gi)
+    if constexpr (SHORT) {
+        // every rank at once: CL lanes each, each lane owning whole segments
+        constexpr int CL = PassShape<NMAX>::threads / (R * kPassGroups);
+        static_assert(CL >= 1 && (CL & (CL - 1)) == 0 && CL <= 64, "lanes per rank");
+        const int lr = (int)threadIdx.x / CL;            // r * kPassGroups + gi
+        const int part = (int)threadIdx.x % CL;
+        const int r = lr / kPassGroups, gr = lr % kPassGroups;
+        const bool live = gr < ng;
+        const int off = live ? r * kPassGroups + gr : 0;
+        const ConfirmAcc a =
+            confirm_owned<CL>(fmask + off, tmask + off, SEGW, (int)n_seg, Wt, part, live);
+        confirm_store<CL>(a, live, part, verdicts, (int64_t)r * G + g0 + gr);
+        return;
+    }
+    // longer windows: kConfirmLanes lanes per rank, in rounds
     constexpr int per_pass = PassShape<NMAX>::threads / kConfirmLanes;
 #pragma unroll 1
     for (int base = 0; base < R * kPassGroups; base += per_pass) {

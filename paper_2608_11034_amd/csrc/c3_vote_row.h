@@ -95,6 +95,20 @@ __device__ __forceinline__ uint64_t equal_mask(const uint64_t (&e)[NMAX], int R,
 // majority value whenever there is one.
 template <int NMAX>
 __device__ __forceinline__ UnitVote exact_vote_row(const uint64_t (&e)[NMAX], int R) {
+    UnitVote v;
+    // Every replica holding replica 0's value (the usual unit) is settled by
+    // R - 1 compares whose results combine as lane masks; the units of a
+    // wave that need the general rule below take it together, and a wave
+    // with none skips it.
+    bool same = true;
+#pragma unroll
+    for (int r = 1; r < NMAX; ++r) same &= (r >= R) | (e[r] == e[0]);
+    if (same) {
+        v.status = C3_AGREE;
+        v.bitmap = 0;
+        v.majority = 0;
+        return v;
+    }
     uint64_t maj = equal_mask<NMAX>(e, R, e[0]);
     if (2 * __builtin_popcountll(maj) <= R) {
         uint64_t cand = e[0];
@@ -108,7 +122,6 @@ __device__ __forceinline__ UnitVote exact_vote_row(const uint64_t (&e)[NMAX], in
         }
         maj = equal_mask<NMAX>(e, R, cand);
     }
-    UnitVote v;
     if (2 * __builtin_popcountll(maj) <= R) {
         v.status = C3_INCONCLUSIVE;
         v.bitmap = 0;
@@ -124,11 +137,35 @@ __device__ __forceinline__ UnitVote exact_vote_row(const uint64_t (&e)[NMAX], in
 
 // Batcher's odd-even merge sort over N register slots (N a power of two,
 // values without NaN): 5, 19 and 63 comparators for 4, 8 and 16 slots, each
-// one min and one max.
-__device__ __forceinline__ float vmin(float a, float b) { return fminf(a, b); }
-__device__ __forceinline__ float vmax(float a, float b) { return fmaxf(a, b); }
-__device__ __forceinline__ double vmin(double a, double b) { return fmin(a, b); }
-__device__ __forceinline__ double vmax(double a, double b) { return fmax(a, b); }
+// one min and one max.  The slots never hold a NaN, so the hardware min and
+// max are used as they are: fminf / fmaxf would first quiet each input
+// (one more instruction per slot), which only matters for signaling NaNs.
+__device__ __forceinline__ float vmin(float a, float b) {
+    float r;
+    asm("v_min_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+    return r;
+}
+__device__ __forceinline__ float vmax(float a, float b) {
+    float r;
+    asm("v_max_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+    return r;
+}
+__device__ __forceinline__ double vmin(double a, double b) {
+    double r;
+    asm("v_min_f64 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+    return r;
+}
+__device__ __forceinline__ double vmax(double a, double b) {
+    double r;
+    asm("v_max_f64 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+    return r;
+}
+// max(|a|, |b|) of two values without NaN, in one instruction
+__device__ __forceinline__ double vmax_abs(double a, double b) {
+    double r;
+    asm("v_max_f64 %0, |%1|, |%2|" : "=v"(r) : "v"(a), "v"(b));
+    return r;
+}
 
 template <int N, typename V>
 __device__ __forceinline__ void sort_network(V (&v)[N]) {
@@ -217,12 +254,15 @@ __device__ __forceinline__ UnitVote statistical_tail(const V (&x)[NMAX], const V
         // statistics h - 1 and h of their merge: the minimum, over the ways
         // of taking i from lo and the rest from hi, of the larger last taken.
         constexpr int h = NC / 2;
+        const double dlo = (double)s[0] - m, dhi = (double)s[NC - 1] - m;
         double lo[h], hi[h];
 #pragma unroll
-        for (int k = 0; k < h; ++k) {
+        for (int k = 0; k < h - 1; ++k) {
             lo[k] = fabs((double)s[h - 1 - k] - m);
             hi[k] = fabs((double)s[h + k] - m);
         }
+        lo[h - 1] = fabs(dlo);
+        hi[h - 1] = fabs(dhi);
         double a = fmin(hi[h - 1], lo[h - 1]);
 #pragma unroll
         for (int i = 1; i < h; ++i) a = fmin(a, fmax(lo[i - 1], hi[h - 1 - i]));
@@ -233,7 +273,7 @@ __device__ __forceinline__ UnitVote statistical_tail(const V (&x)[NMAX], const V
         // lo and hi are the deviations of every value, computed as the flag
         // test computes them, and each run ascends away from m: the largest
         // deviation is the larger run end
-        dmax = fmax(lo[h - 1], hi[h - 1]);
+        dmax = vmax_abs(dlo, dhi);
     } else {
         double ds[NMAX];
 #pragma unroll
@@ -242,12 +282,15 @@ __device__ __forceinline__ UnitVote statistical_tail(const V (&x)[NMAX], const V
         sort_network<NMAX>(ds);
         d = median_sorted<NMAX>(ds, nf);
     }
-    if (d == 0.0) {
-        const double q3 = quantile7_sorted<NMAX>(s, nf, 0.75);
-        const double q1 = quantile7_sorted<NMAX>(s, nf, 0.25);
-        d = (q3 - q1) * 0.5;
+    // the fallbacks of a zero MAD, skipped by waves where no unit has one
+    if (ballot64(d == 0.0) != 0ull) {
+        if (d == 0.0) {
+            const double q3 = quantile7_sorted<NMAX>(s, nf, 0.75);
+            const double q1 = quantile7_sorted<NMAX>(s, nf, 0.25);
+            d = (q3 - q1) * 0.5;
+        }
+        if (d == 0.0) d = ((double)pick<NMAX>(s, nf - 1) - (double)s[0]) / (double)nf;
     }
-    if (d == 0.0) d = ((double)pick<NMAX>(s, nf - 1) - (double)s[0]) / (double)nf;
     uint64_t B = nonfin;
     if (d != 0.0) {
         const double thr = kappa * d;
@@ -289,23 +332,28 @@ __device__ __forceinline__ UnitVote statistical_vote_row(const uint64_t (&bits)[
                                                          double kappa) {
     using V = typename std::conditional<KIND == C3_EV_F32, float, double>::type;
     V x[NMAX], s[NMAX];
-    uint64_t fin = 0;
+    // every slot a valid finite value (the usual unit): one class test per
+    // slot, combined as lane masks
+    bool allfin = true;
 #pragma unroll
     for (int r = 0; r < NMAX; ++r) {
         if constexpr (KIND == C3_EV_F32) x[r] = __uint_as_float((uint32_t)bits[r]);
         else x[r] = __longlong_as_double((long long)bits[r]);
-        fin |= (uint64_t)(r < R && __builtin_isfinite(x[r])) << r;
+        allfin &= (r < R) & __builtin_isfinite(x[r]);
     }
     const uint64_t valid = R == 64 ? ~0ull : ((1ull << R) - 1);
-    const uint64_t nonfin = valid & ~fin;
-    const int nf = __builtin_popcountll(fin);
-    if (nf == NMAX) {
-        // every slot holds a finite value (the usual unit): sort them as they are
+    if (allfin) {
+        // sort the values as they are
 #pragma unroll
         for (int r = 0; r < NMAX; ++r) s[r] = x[r];
         sort_network<NMAX>(s);
-        return statistical_tail<NMAX, NMAX, V, MAJ>(x, s, fin, nonfin, nf, kappa);
+        return statistical_tail<NMAX, NMAX, V, MAJ>(x, s, valid, 0ull, NMAX, kappa);
     }
+    uint64_t fin = 0;
+#pragma unroll
+    for (int r = 0; r < NMAX; ++r) fin |= (uint64_t)(r < R && __builtin_isfinite(x[r])) << r;
+    const uint64_t nonfin = valid & ~fin;
+    const int nf = __builtin_popcountll(fin);
     if (2 * nf <= R) {
         UnitVote v;
         v.status = C3_INCONCLUSIVE;
