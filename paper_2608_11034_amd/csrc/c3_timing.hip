@@ -537,8 +537,10 @@ __global__ void __launch_bounds__(PassShape<NMAX>::threads) timing_pass_kernel(
     const int64_t n_seg = (T + kSegIters - 1) / kSegIters;
     uint32_t* fmask = pass_masks;
     uint32_t* tmask = pass_masks + n_seg * SEGW;
+    __shared__ int32_t step_ctr;     // the next step index to hand out
     for (int64_t i = threadIdx.x; i < 2 * n_seg * SEGW; i += PassShape<NMAX>::threads)
         pass_masks[i] = 0u;
+    if (threadIdx.x == 0) step_ctr = 2 * NW;
     __syncthreads();
 
     const int ti = lane / kPassGroups, gi = lane % kPassGroups;
@@ -546,8 +548,8 @@ __global__ void __launch_bounds__(PassShape<NMAX>::threads) timing_pass_kernel(
     // The next step's rows are loaded before this step's results are
     // stored: the vector-memory counter retires loads and stores in issue
     // order, so waiting for loads issued after the stores would wait for
-    // the stores too.  The last step re-reads its own rows (L2 hits) rather
-    // than branch around the prefetch.
+    // the stores too.  A wave's last step loads nothing more: a load left
+    // in flight would hold registers that the confirmation reuses.
     uint32_t off_f[CPF], off_t[CPT];
     pass_lane_offsets<CPF>(G, ng, lane, off_f);
     pass_lane_offsets<CPT>(G, ng, lane, off_t);
@@ -561,13 +563,14 @@ __global__ void __launch_bounds__(PassShape<NMAX>::threads) timing_pass_kernel(
         }
     };
     vu32x4 gf[CPF], gt[CPT];
-    auto do_step = [&](int64_t st) {
+    auto do_step = [&](int64_t st, int64_t nx) -> int64_t {
         const int64_t t0 = st * kPassIters;
         vu32x4 vf[CPF], vt[CPT];
         stage_swap<CPF>(stage[wave], lane, gf, vf);
         stage_swap<CPT>(stage[wave], lane, gt, vt);
-        const int64_t tn = (st + NW < n_steps ? st + NW : st) * kPassIters;
-        load_step(tn, gf, gt);
+        if (nx < n_steps) load_step(nx * kPassIters, gf, gt);
+        int32_t nn = 0;
+        if (lane == 0) nn = atomicAdd(&step_ctr, 1);
         const int64_t t = t0 + ti;
         const bool valid = t < T && gi < ng;
         uint64_t ef[NMAX], et[NMAX];
@@ -605,21 +608,31 @@ __global__ void __launch_bounds__(PassShape<NMAX>::threads) timing_pass_kernel(
             to.bitmap[u] = vtm.bitmap;
             to.majority[u] = vtm.majority;
         }
-        if (!valid) return;
-        const uint32_t bit = 1u << (t & (kSegIters - 1));
-        const int64_t w0 = (t / kSegIters) * SEGW + gi;
-        for (uint64_t b = vfp.bitmap; b != 0ull; b &= b - 1ull)
-            atomicOr(fmask + w0 + __builtin_ctzll(b) * kPassGroups, bit);
-        for (uint64_t b = vtm.bitmap; b != 0ull; b &= b - 1ull)
-            atomicOr(tmask + w0 + __builtin_ctzll(b) * kPassGroups, bit);
+        if (valid) {
+            const uint32_t bit = 1u << (t & (kSegIters - 1));
+            const int64_t w0 = (t / kSegIters) * SEGW + gi;
+            for (uint64_t b = vfp.bitmap; b != 0ull; b &= b - 1ull)
+                atomicOr(fmask + w0 + __builtin_ctzll(b) * kPassGroups, bit);
+            for (uint64_t b = vtm.bitmap; b != 0ull; b &= b - 1ull)
+                atomicOr(tmask + w0 + __builtin_ctzll(b) * kPassGroups, bit);
+        }
+        return (int64_t)__builtin_amdgcn_readfirstlane(nn);
     };
     if (wave < n_steps) {
         load_step((int64_t)wave * kPassIters, gf, gt);
         // The first step outside the loop, so that every path into the
         // loop ends with one step's loads and then (with per-unit results)
         // its stores, and the waits for the loads never cover the stores.
-        do_step(wave);
-        for (int64_t st = wave + NW; st < n_steps; st += NW) do_step(st);
+        // Wave w takes steps w and w + NW, then steps from the workgroup's
+        // counter; the ticket for the step after next is taken during a
+        // step, so its latency is hidden.
+        int64_t st = wave + NW;
+        int64_t nx = do_step(wave, st);
+        while (st < n_steps) {
+            const int64_t nn = do_step(st, nx);
+            st = nx;
+            nx = nn;
+        }
     }
     __syncthreads();
 
