@@ -27,7 +27,9 @@
 // writes one 64-byte partial.  When a chunk is a single tile the workgroup
 // writes the chunk record directly; otherwise a finalize kernel combines the
 // chunk's partials in tile order.  The per-tile arithmetic never depends on
-// which workgroup runs it, so results are independent of the grid size.
+// which workgroup runs it, so results are independent of the grid size and
+// of the tile order: large launches take their tiles through the XCD map
+// (xcd_map_tile), the others in order.
 //
 // Non-finite screen: a lane sums its elements in fp64 without looking at
 // them.  A non-finite element is the only way its sum or sum of squares can
@@ -345,7 +347,7 @@ __device__ inline void write_record(c3_chunk_record_t* rec, const TensorInfo* ti
 template <int DT, int U>
 __global__ void __launch_bounds__(kSigThreads, C3_SIG_WAVES_PER_EU)
     signature_kernel(const SigPlan* __restrict__ plan, c3_chunk_record_t* __restrict__ records,
-                     int gk0, int gk1, int64_t gtiles) {
+                     int gk0, int gk1, int64_t gtiles, int mapped) {
     __shared__ TilePartial lds[kSigThreads / 64];
     const int lane = threadIdx.x & 63;
     // the wave index, uniform across the wave (keeps beta and addresses scalar)
@@ -372,7 +374,10 @@ __global__ void __launch_bounds__(kSigThreads, C3_SIG_WAVES_PER_EU)
     K.k4 = nh_key(4u * lane + 4u);
     K.k5 = nh_key(4u * lane + 5u);
 
-    for (int64_t i = blockIdx.x; i < ntiles; i += gridDim.x) {
+    // a mapped launch: one tile per workgroup, from the XCD map; otherwise
+    // tiles blockIdx.x, blockIdx.x + gridDim.x, ...
+    for (int64_t i = mapped ? xcd_map_tile(blockIdx.x, ntiles) : (int64_t)blockIdx.x; i < ntiles;
+         i += mapped ? ntiles : (int64_t)gridDim.x) {
         const int64_t r = i / gtiles;
         const int64_t j = g0 + (i - r * gtiles);
         const int k = gk0 + find_segment(gtile + gk0, gk1 - gk0, j);
@@ -849,14 +854,17 @@ hipError_t launch_plan_fetch(const void* host_src, void* dst, size_t bytes, hipS
 
 template <int DT>
 static hipError_t launch_group(const SigPlan* dplan, c3_chunk_record_t* records, int gk0, int gk1,
-                               int64_t gtiles, int R, int grid_blocks, hipStream_t stream) {
+                               int64_t gtiles, int R, uint64_t tile_bytes, int grid_blocks,
+                               hipStream_t stream) {
     const int64_t ntiles = gtiles * R;
     if (ntiles <= 0) return hipSuccess;
     int64_t grid = grid_blocks > 0 ? grid_blocks : ntiles;
     if (grid > ntiles) grid = ntiles;
+    const int mapped = grid_blocks <= 0 && xcd_map_applies(ntiles, tile_bytes);
+    if (mapped) grid = xcd_map_grid(ntiles);
     if (grid > 0x7FFFFFFF) grid = 0x7FFFFFFF;
     hipLaunchKernelGGL((signature_kernel<DT, kUnroll>), dim3((unsigned)grid), dim3(kSigThreads), 0,
-                       stream, dplan, records, gk0, gk1, gtiles);
+                       stream, dplan, records, gk0, gk1, gtiles, mapped);
     return hipGetLastError();
 }
 
@@ -870,10 +878,10 @@ hipError_t launch_signature(const SigPlan* dplan, const SigPlan& hplan, const Si
         if (gk1 <= gk0) continue;
         const int64_t gt = groups.tiles[d];
         switch (d) {
-            case C3_F32: e = launch_group<C3_F32>(dplan, records, gk0, gk1, gt, hplan.R, grid_blocks, stream); break;
-            case C3_BF16: e = launch_group<C3_BF16>(dplan, records, gk0, gk1, gt, hplan.R, grid_blocks, stream); break;
-            case C3_F16: e = launch_group<C3_F16>(dplan, records, gk0, gk1, gt, hplan.R, grid_blocks, stream); break;
-            default: e = launch_group<C3_RAW>(dplan, records, gk0, gk1, gt, hplan.R, grid_blocks, stream); break;
+            case C3_F32: e = launch_group<C3_F32>(dplan, records, gk0, gk1, gt, hplan.R, hplan.tile_bytes, grid_blocks, stream); break;
+            case C3_BF16: e = launch_group<C3_BF16>(dplan, records, gk0, gk1, gt, hplan.R, hplan.tile_bytes, grid_blocks, stream); break;
+            case C3_F16: e = launch_group<C3_F16>(dplan, records, gk0, gk1, gt, hplan.R, hplan.tile_bytes, grid_blocks, stream); break;
+            default: e = launch_group<C3_RAW>(dplan, records, gk0, gk1, gt, hplan.R, hplan.tile_bytes, grid_blocks, stream); break;
         }
         if (e != hipSuccess) return e;
     }

@@ -67,6 +67,50 @@ constexpr uint64_t kDefaultTileMax = C3_SIG_TILE_MAX;
 constexpr int kSigThreads = 256;
 constexpr int kUnroll = C3_SIG_UNROLL;
 
+// Tile map of large launches.  The hardware hands workgroup b to XCD
+// b mod 8, and on MI355X XCDs 1, 3, 5 and 7 read about 6% slower than the
+// others (the read probe over 4 GiB: 874-930 against 939-981 GB/s each, for
+// any pairing of tiles with XCDs), so one tile per workgroup in order lets
+// the odd XCDs set the end of the launch.  With the map, tiles go in rounds
+// of kXcdRound: within a round an even XCD takes kXcdEven consecutive tiles
+// and an odd one kXcdOdd, in XCD order, and every XCD has the same number of
+// workgroups, the odd ones' spare workgroups at the end taking no tile.  A
+// round of 256 KiB tiles is 64 MiB, and all XCDs stream the same round at
+// once.  The read probe over 4 GiB of 256 KiB tiles: 7.16-7.17 TB/s against
+// 7.06-7.08 in order (33/31 tiles); 16 or 32 tiles each without a skew
+// 7.09-7.12; 64 each 6.68.  The signature kernel gains 1.4-1.6% on the 1B
+// bf16 parameters and the 2B fp32 Adam shard (256 KiB tiles) and loses
+// 1.2-2.5% on the Llama-layer gradients (128 KiB tiles, where the probe
+// still gains), so only launches of tiles of 256 KiB or more use it.
+constexpr unsigned kXcdEven = 33, kXcdOdd = 31;
+constexpr unsigned kXcdRound = 4 * (kXcdEven + kXcdOdd);
+constexpr int64_t kXcdMapMinTiles = 8 * kXcdRound;     // smaller launches keep the order
+constexpr uint64_t kXcdMapMinTileBytes = 256 * 1024;
+
+// Workgroups of a mapped launch of n tiles.
+inline int64_t xcd_map_grid(int64_t n) { return 8 * ((n + kXcdRound - 1) / kXcdRound) * kXcdEven; }
+
+// Whether a launch of n tiles of tile_bytes with the default grid is mapped.
+inline bool xcd_map_applies(int64_t n, uint64_t tile_bytes) {
+    return n >= kXcdMapMinTiles && tile_bytes >= kXcdMapMinTileBytes && xcd_map_grid(n) <= 0x7FFFFFFF;
+}
+
+// Tile of workgroup b in a mapped launch of n tiles (n when it takes none).
+// The last, partial round of m tiles is split in the same proportions: XCD x
+// takes [m off_x / R, m (off_x + cnt_x) / R) of it, R the round size.
+__device__ __forceinline__ int64_t xcd_map_tile(unsigned b, int64_t n) {
+    const unsigned x = b % 8u, k = b / 8u;
+    const unsigned cnt = (x & 1u) ? kXcdOdd : kXcdEven;
+    const unsigned off = (x / 2u) * (kXcdEven + kXcdOdd) + ((x & 1u) ? kXcdEven : 0u);
+    const int64_t full = n / kXcdRound;
+    const int64_t round = k / cnt;
+    if (round < full) return round * kXcdRound + off + k % cnt;
+    const int64_t m = n - full * kXcdRound;
+    const int64_t lo = m * off / kXcdRound, hi = m * (off + cnt) / kXcdRound;
+    const int64_t j = (int64_t)k - full * cnt;
+    return j < hi - lo ? full * kXcdRound + lo + j : n;
+}
+
 // Position range [k0, k1) of each dtype in the grouped tensor order and the
 // tiles per replica of that group.
 struct SigGroups {

@@ -239,6 +239,39 @@ def test_random_shapes_chunks_and_tiles(seed):
     compare_all_records(c3.records_numpy(rec), ref)
 
 
+@pytest.mark.parametrize("chunk", [256 << 10, 1 << 20])
+def test_xcd_tile_map_every_record(chunk):
+    """Launches of at least 2,048 tiles of 256 KiB take their tiles through
+    the XCD map (uneven rounds of 256 tiles, a proportional last round,
+    workgroups without a tile).  Two ragged tensors of two dtypes over three
+    replicas give launches of 5,283 fp32 and 2,163 bf16 tiles, both with a
+    partial last round: every record against the oracle and against the
+    same launches in plain order (an explicit grid), with faults in the
+    first and the last chunk."""
+    _print_case("xcd tile map", chunk)
+    gen = torch.Generator(device=DEV)
+    gen.manual_seed(chunk)
+    base = [torch.randn(110 * (1 << 20) + 4099, generator=gen, device=DEV) * 1e-2,
+            torch.randn(90 * (1 << 20) + 77, generator=gen, device=DEV).to(torch.bfloat16)]
+    reps = [[t.clone() for t in base] for _ in range(3)]
+    reps[2][0].view(torch.uint8)[11] ^= 0x10
+    reps[1][1].view(torch.uint8)[-1] ^= 0x01
+    plan = c3.SignaturePlan(reps, chunk, 256 << 10)
+    rec = plan.new_records()
+    ws = plan.new_workspace()
+    plan.run(rec, ws)
+    rec_plain = plan.new_records()
+    plan.run(rec_plain, ws, grid_blocks=997)
+    torch.cuda.synchronize()
+    g = c3.records_numpy(rec)
+    assert g.tobytes() == c3.records_numpy(rec_plain).tobytes()
+    metas = [(workloads.F32, tuple(base[0].shape)), (workloads.BF16, tuple(base[1].shape))]
+    ref = oracle.signature([[workloads.host_bytes(t) for t in rep] for rep in reps], metas, chunk)
+    compare_all_records(g, ref)
+    diff = np.argwhere(ref["sig"] != ref["sig"][0:1])
+    assert sorted(map(tuple, diff.tolist())) == [(1, int(ref["sig"].shape[1]) - 1), (2, 0)]
+
+
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16, torch.float16])
 def test_absmax_finite_extremes_every_record(dtype):
     """Chunks without NaN or Inf (the kernel's unclassified path) whose largest
