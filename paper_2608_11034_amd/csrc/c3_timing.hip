@@ -433,7 +433,7 @@ __global__ void __launch_bounds__(kConfirmThreads) timing_confirm_kernel(
 // rows are 16-byte aligned, the masks fit kPassMaskLds bytes and there are
 // at least as many workgroups as compute units.  Per-unit results are
 // written as 16- to 128-byte pieces of each iteration's row; on the
-// 32,768-rank workload the pass then takes 101.9 us of kernel time against
+// 32,768-rank workload the pass then takes 91.2 us of kernel time against
 // 106.2 us for the three launches of the workspace path (clear, votes,
 // confirmation), which per-unit results of one kind only still take.
 // ---------------------------------------------------------------------------
