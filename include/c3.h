@@ -492,12 +492,13 @@ size_t c3_timing_consensus_workspace_size(int R, int64_t G, int64_t T, int windo
  *                 wanted (then only the verdicts are produced for it).
  *   verdicts      device [R*G], rank = r*G + g, as c3_confirm.
  * Execution (results do not depend on it):
- *   - per-unit results of neither kind or of both, R in {4, 8, 16}, both
- *     arrays 16-byte aligned, 2 * ceil(T / 32) * R * 64 bytes <= 64 KiB and
- *     G / 16 at least the device's compute-unit count: one kernel; each
- *     workgroup votes 16 groups over all T iterations (writing their
- *     per-unit results when requested), collects its ranks' outlier bits in
- *     LDS and confirms them there (the workspace is not touched);
+ *   - R in {4, 8, 16}, both arrays 16-byte aligned, W <= 64,
+ *     2 * ceil(T / 32) * R * 64 bytes <= 64 KiB and G / 16 at least the
+ *     device's compute-unit count: one kernel, with the per-unit results of
+ *     either kind, both or neither; each workgroup votes 16 groups over all
+ *     T iterations (writing their per-unit results when requested),
+ *     collects its ranks' outlier bits in LDS and confirms them there (the
+ *     workspace is not touched);
  *   - otherwise, for R <= 16 and W <= 64: a clearing kernel, one kernel
  *     voting both kinds that ORs each outlier bit into per-rank masks in the
  *     workspace, and a confirmation kernel over those masks;

@@ -428,14 +428,14 @@ __global__ void __launch_bounds__(kConfirmThreads) timing_confirm_kernel(
 // step's rows of one kind are kPassIters contiguous runs of kPassGroups
 // rows, read with 16-byte loads and passed through the wave's LDS region as
 // in the staged kernel (lane l takes back row l: iteration t0 + l /
-// kPassGroups, group g0 + l % kPassGroups).  Used without per-unit results
-// or with those of both kinds, when R equals the group bound, both kinds'
-// rows are 16-byte aligned, the masks fit kPassMaskLds bytes and there are
-// at least as many workgroups as compute units.  Per-unit results are
-// written as 16- to 128-byte pieces of each iteration's row; on the
-// 32,768-rank workload the pass then takes 91.2 us of kernel time against
-// 106.2 us for the three launches of the workspace path (clear, votes,
-// confirmation), which per-unit results of one kind only still take.
+// kPassGroups, group g0 + l % kPassGroups).  Used with the per-unit results
+// of either kind, both or neither, when R equals the group bound, both
+// kinds' rows are 16-byte aligned, W <= 64, the masks fit kPassMaskLds
+// bytes and there are at least as many workgroups as compute units.
+// Per-unit results are written as 16- to 128-byte pieces of each
+// iteration's row; on the 32,768-rank workload the pass with those of both
+// kinds takes 91.2 us of kernel time against 106.2 us for the three
+// launches of the workspace path (clear, votes, confirmation).
 // ---------------------------------------------------------------------------
 constexpr int kPassGroups = 16;                  // groups per workgroup
 constexpr int kPassIters = 64 / kPassGroups;     // iterations per wave step
@@ -515,7 +515,9 @@ __device__ __forceinline__ void pass_load_full(const char* __restrict__ base, in
         g[j] = __builtin_nontemporal_load(reinterpret_cast<const vu32x4*>(step + off[j]));
 }
 
-template <int NMAX, int KIND, bool SHORT, bool PU>
+// PU: per-unit results written, bit 0 those of the fingerprints, bit 1
+// those of the step times.
+template <int NMAX, int KIND, bool SHORT, int PU>
 __global__ void __launch_bounds__(PassShape<NMAX>::threads) timing_pass_kernel(
     const char* __restrict__ fp, const char* __restrict__ tp, int64_t G, int64_t T, double kappa,
     int Wt, c3_rank_verdict_t* __restrict__ verdicts, VoteOut fo, VoteOut to) {
@@ -531,7 +533,7 @@ __global__ void __launch_bounds__(PassShape<NMAX>::threads) timing_pass_kernel(
     const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
     // per-unit results: XCD-aware block order (pass_group_block); without
     // them the plain order reads faster (81.2 against 83.4 us per call)
-    const int64_t g0 = (PU ? pass_group_block(blockIdx.x, gridDim.x) : (int64_t)blockIdx.x) *
+    const int64_t g0 = (PU != 0 ? pass_group_block(blockIdx.x, gridDim.x) : (int64_t)blockIdx.x) *
                        kPassGroups;
     const int ng = G - g0 < kPassGroups ? (int)(G - g0) : kPassGroups;
     const int64_t n_seg = (T + kSegIters - 1) / kSegIters;
@@ -592,21 +594,26 @@ __global__ void __launch_bounds__(PassShape<NMAX>::threads) timing_pass_kernel(
             }
         }
         const UnitVote vfp = exact_vote_row<NMAX>(ef, R);
-        // without per-unit results only the bitmaps are kept: no lower-median replica
-        const UnitVote vtm = statistical_vote_row<NMAX, KIND, PU>(et, R, kappa);
-        if constexpr (PU) {
+        // without the times' per-unit results only the bitmaps are kept: no
+        // lower-median replica
+        const UnitVote vtm = statistical_vote_row<NMAX, KIND, (PU & 2) != 0>(et, R, kappa);
+        if constexpr (PU != 0) {
             // Every lane stores: a path without the stores would make the
             // wait for the next step's loads cover them.  A lane outside
             // the block holds the row it loaded instead -- (t, g0) in a whole
             // step, (0, g0) in the last one -- and writes that unit's
             // results again, unchanged.
             const int64_t u = valid ? t * G + g0 + gi : (t0 + kPassIters <= T ? t * G + g0 : g0);
-            fo.status[u] = vfp.status;
-            fo.bitmap[u] = vfp.bitmap;
-            fo.majority[u] = vfp.majority;
-            to.status[u] = vtm.status;
-            to.bitmap[u] = vtm.bitmap;
-            to.majority[u] = vtm.majority;
+            if constexpr ((PU & 1) != 0) {
+                fo.status[u] = vfp.status;
+                fo.bitmap[u] = vfp.bitmap;
+                fo.majority[u] = vfp.majority;
+            }
+            if constexpr ((PU & 2) != 0) {
+                to.status[u] = vtm.status;
+                to.bitmap[u] = vtm.bitmap;
+                to.majority[u] = vtm.majority;
+            }
         }
         if (valid) {
             const uint32_t bit = 1u << (t & (kSegIters - 1));
@@ -710,19 +717,26 @@ static hipError_t launch_pass(const char* fp, const char* tp, int64_t G, int64_t
                               const VoteOut& to, size_t lds, hipStream_t stream) {
     const dim3 grid((unsigned)((G + kPassGroups - 1) / kPassGroups));
     const dim3 block(PassShape<NMAX>::threads);
-    const bool pu = fo.status != nullptr;
-    if (Wt <= 32 && pu)
-        hipLaunchKernelGGL((timing_pass_kernel<NMAX, KIND, true, true>), grid, block, lds, stream,
-                           fp, tp, G, T, kappa, Wt, verdicts, fo, to);
-    else if (Wt <= 32)
-        hipLaunchKernelGGL((timing_pass_kernel<NMAX, KIND, true, false>), grid, block, lds, stream,
-                           fp, tp, G, T, kappa, Wt, verdicts, fo, to);
-    else if (pu)
-        hipLaunchKernelGGL((timing_pass_kernel<NMAX, KIND, false, true>), grid, block, lds, stream,
-                           fp, tp, G, T, kappa, Wt, verdicts, fo, to);
-    else
-        hipLaunchKernelGGL((timing_pass_kernel<NMAX, KIND, false, false>), grid, block, lds,
-                           stream, fp, tp, G, T, kappa, Wt, verdicts, fo, to);
+    const int pu = (fo.status != nullptr ? 1 : 0) | (to.status != nullptr ? 2 : 0);
+#define C3_PASS(S, P)                                                                     \
+    hipLaunchKernelGGL((timing_pass_kernel<NMAX, KIND, S, P>), grid, block, lds, stream, fp, \
+                       tp, G, T, kappa, Wt, verdicts, fo, to)
+    if (Wt <= 32) {
+        switch (pu) {
+            case 0: C3_PASS(true, 0); break;
+            case 1: C3_PASS(true, 1); break;
+            case 2: C3_PASS(true, 2); break;
+            default: C3_PASS(true, 3); break;
+        }
+    } else {
+        switch (pu) {
+            case 0: C3_PASS(false, 0); break;
+            case 1: C3_PASS(false, 1); break;
+            case 2: C3_PASS(false, 2); break;
+            default: C3_PASS(false, 3); break;
+        }
+    }
+#undef C3_PASS
     return hipGetLastError();
 }
 
@@ -755,8 +769,8 @@ hipError_t launch_timing_consensus(const uint64_t* fp, const void* times, int ti
     if ((ranks * kConfirmLanes + kConfirmThreads - 1) / kConfirmThreads > 0x7FFFFFFF)
         return hipErrorInvalidValue;
     if (ranks == 0) return hipSuccess;
-    // the single pass: verdicts only, or with the per-unit results of both kinds
-    if ((fp_status == nullptr) == (t_status == nullptr)) {
+    // the single pass, with the per-unit results of either kind, both or neither
+    {
         const int Wt = (int64_t)window < T ? window : (int)T;
         size_t lds = 0;
         if (pass_applies(fp, times, time_kind, R, G, T, Wt, stream, lds)) {

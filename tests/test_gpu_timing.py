@@ -102,8 +102,8 @@ CASES = [
 ]
 
 
-# Shapes of the single-pass kernel (taken when no per-unit results are
-# requested, or those of both kinds): R a group bound (4, 8, 16), at least one
+# Shapes of the single-pass kernel (with the per-unit results of either
+# kind, both or neither): R a group bound (4, 8, 16), at least one
 # 16-group workgroup per
 # compute unit (G >= 4081 on 256 CUs), masks within the LDS budget (T <= 2048
 # at R = 8).  Ragged G leaves the last workgroup 1-15 groups; ragged T leaves
@@ -130,14 +130,20 @@ def test_timing_consensus_single_pass_matches_oracle(R, G, T, W, f64, per_unit):
     _check(fp, tau, W, per_unit=per_unit)
 
 
+@pytest.mark.parametrize("R,G,T,W,f64", [
+    (8, 4100, 37, 16, False),     # the single pass: ragged G and T
+    (16, 4096, 20, 1, True),      # the single pass: fp64 times, W = 1
+    (4, 4097, 33, 64, False),     # the single pass: a window over 32
+    (8, 100, 40, 16, False),      # too few groups for the pass: the workspace path
+])
 @pytest.mark.parametrize("kind", ["fp", "time"])
-def test_timing_consensus_per_unit_results_of_one_kind(kind):
-    """Per-unit results of one kind only take the separate launches; the
-    other kind's outputs stay untouched."""
+def test_timing_consensus_per_unit_results_of_one_kind(kind, R, G, T, W, f64):
+    """Per-unit results of one kind only: the single pass where its shape
+    conditions hold, the workspace path otherwise; every per-unit result of
+    that kind and every verdict field against the oracle."""
     import ctypes
-    _case("timing one kind", kind)
-    R, G, T, W = 8, 4100, 37, 16
-    fp, tau = _inputs(R, G, T, seed=77)
+    _case("timing one kind", kind, R, G, T, W, f64)
+    fp, tau = _inputs(R, G, T, seed=77 + R + T, f64=f64)
     (ost, obm, omj), (sst, sbm, smj), ref = _oracle(fp, tau, W)
     dfp, dtau = torch.from_numpy(fp).to(DEV), torch.from_numpy(tau).to(DEV)
     outs = (torch.full((T * G,), 0xEE, dtype=torch.uint8, device=DEV),
@@ -149,8 +155,8 @@ def test_timing_consensus_per_unit_results_of_one_kind(kind):
     null = ctypes.c_void_p(0)
     fo = tuple(p(x) for x in outs) if kind == "fp" else (null, null, null)
     to = tuple(p(x) for x in outs) if kind == "time" else (null, null, null)
-    rc = c3.lib().c3_timing_consensus(p(dfp), p(dtau), c3.EV_F32, R, G, T, c3.KAPPA_DEFAULT, W,
-                                      *fo, *to, p(ver), p(ws), ws.numel(), null)
+    rc = c3.lib().c3_timing_consensus(p(dfp), p(dtau), c3.EV_F64 if f64 else c3.EV_F32, R, G, T,
+                                      c3.KAPPA_DEFAULT, W, *fo, *to, p(ver), p(ws), ws.numel(), null)
     assert rc == 0
     torch.cuda.synchronize()
     st, bm, mj = (ost, obm, omj) if kind == "fp" else (sst, sbm, smj)
@@ -159,7 +165,10 @@ def test_timing_consensus_per_unit_results_of_one_kind(kind):
     assert np.array_equal(outs[2].cpu().numpy(), mj)
     v = c3.verdicts_numpy(ver)
     assert np.array_equal(v["flags"], ref["flags"])
+    assert np.array_equal(v["first_divergent_iter"], ref["first_div"])
+    assert np.array_equal(v["divergent_count"], ref["div_count"])
     assert np.array_equal(v["slow_count"], ref["slow_count"])
+    assert np.array_equal(v["max_window_slow"], ref["max_window"])
     assert np.array_equal(v["first_straggler_window"], ref["first_window"])
 
 
