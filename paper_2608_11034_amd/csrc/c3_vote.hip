@@ -1,18 +1,18 @@
 // Consensus kernels of C3 for gfx950: the decision step of Algorithm 1.
 //
 // Which kernel decides a unit depends on the group size R:
-//   R <= 16   one thread per unit, the R values in registers (128-bit row
+//   R <= 32   one thread per unit, the R values in registers (128-bit row
 //             loads when replicas are adjacent), deciding with the per-unit
 //             functions of c3_vote_row.h;
-//   R > 16    one wave per unit: lane l holds replicas l, l + 64, ... (see
+//   R > 32    one wave per unit: lane l holds replicas l, l + 64, ... (see
 //             the wave kernels below) and bitmap word s is one ballot.  The
 //             exact vote broadcasts candidate values by readlane; the
 //             statistical vote sorts the wave's values once.
-// Measured on 1M-unit rows, the wave kernel's exact vote is 1.5x (R = 17) to
-// 7.6x (R = 64) faster than lane-per-replica counting.  Per 256K units its
-// statistical vote takes 0.09-0.11 ms up to R = 64 and 0.26-0.37 ms at
-// R = 129-256 (fp32-fp64), 1.8x to 8x faster than the rank loops and
-// (value, replica) double sorts it replaced.
+// Per 256K units the wave kernel's statistical vote takes 0.09-0.11 ms at
+// R = 33-64 and 0.26-0.37 ms at R = 129-256 (fp32-fp64), 1.8x to 8x faster
+// than the rank loops and (value, replica) double sorts it replaced; on 1M-unit
+// rows its exact vote was up to 7.6x (R = 64) faster than lane-per-replica
+// counting.
 //
 // EXACT (Sec. 5.3): a strict majority exists iff some value is held by more
 // than R / 2 replicas; those are the majority, the bitmap marks the others
@@ -34,7 +34,7 @@ namespace c3 {
 constexpr int kVoteThreads = 256;
 
 // ---------------------------------------------------------------------------
-// Small groups (R <= 16): one thread per unit with the R values in registers,
+// Small groups (R <= 32): one thread per unit with the R values in registers,
 // so the whole decision is register arithmetic.  NMAX is R rounded up to a
 // power of two; slots past R are padding that never takes part.
 // ---------------------------------------------------------------------------
@@ -69,7 +69,7 @@ __global__ void __launch_bounds__(kVoteThreads) statistical_vote_small_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// Wave per unit (every group above 16 replicas).  Lane l
+// Wave per unit (every group above 32 replicas).  Lane l
 // holds the values of replicas l, l + 64, l + 128 and l + 192 (NS =
 // ceil(R / 64) slots; slot s holds replica 64 s + l), so bitmap word s is the
 // ballot of slot s.  The exact vote broadcasts candidate values by readlane
@@ -463,7 +463,11 @@ hipError_t launch_consensus(const void* evidence, int kind, int64_t rstride, int
                             int64_t n_units, int mode, double kappa, uint8_t* status,
                             uint64_t* bitmap, int32_t* majority_idx, hipStream_t stream) {
     if (n_units <= 0) return hipSuccess;
-    if (R <= 16) {
+    // Up to 32 replicas one thread decides a unit: against a wave per unit,
+    // 0.035-0.044 against 0.092-0.102 ms per 262,144 units of fp32 times at
+    // R = 17-32, 0.055-0.072 against 0.106-0.117 for fp64, 0.027-0.046
+    // against 0.044-0.046 for 64-bit fingerprints; the same results.
+    if (R <= 32) {
         const int64_t blocks = (n_units + kVoteThreads - 1) / kVoteThreads;
         if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
         const char* e = static_cast<const char*>(evidence);
@@ -473,8 +477,11 @@ hipError_t launch_consensus(const void* evidence, int kind, int64_t rstride, int
         else if (R <= 8)
             launch_small<8>(e, kind, rstride, ustride, R, n_units, mode, kappa, status, bitmap,
                             majority_idx, stream, (unsigned)blocks);
-        else
+        else if (R <= 16)
             launch_small<16>(e, kind, rstride, ustride, R, n_units, mode, kappa, status, bitmap,
+                             majority_idx, stream, (unsigned)blocks);
+        else
+            launch_small<32>(e, kind, rstride, ustride, R, n_units, mode, kappa, status, bitmap,
                              majority_idx, stream, (unsigned)blocks);
         return hipGetLastError();
     }

@@ -1,4 +1,4 @@
-// Per-unit decisions of Algorithm 1 for groups of up to 16 replicas, one
+// Per-unit decisions of Algorithm 1 for groups of up to 32 replicas, one
 // thread per unit with the R values in registers.  Used by the consensus
 // kernels (c3_vote.hip) and the fused timing-consensus kernel
 // (c3_timing.hip), so both decide every unit with the same code.
@@ -136,8 +136,8 @@ __device__ __forceinline__ UnitVote exact_vote_row(const uint64_t (&e)[NMAX], in
 }
 
 // Batcher's odd-even merge sort over N register slots (N a power of two,
-// values without NaN): 5, 19 and 63 comparators for 4, 8 and 16 slots, each
-// one min and one max.  The slots never hold a NaN, so the hardware min and
+// values without NaN): 5, 19, 63 and 191 comparators for 4, 8, 16 and 32
+// slots, each one min and one max.  The slots never hold a NaN, so the hardware min and
 // max are used as they are: fminf / fmaxf would first quiet each input
 // (one more instruction per slot), which only matters for signaling NaNs.
 __device__ __forceinline__ float vmin(float a, float b) {

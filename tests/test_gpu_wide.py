@@ -68,9 +68,12 @@ def _check_votes(st, bm, mj, ost, obm, omj, R, where):
     assert np.array_equal(mj.cpu().numpy(), omj), where
 
 
-@pytest.mark.parametrize("R", [17, 33, 64, 65, 100, 127, 128, 129, 192, 255, 256])
+@pytest.mark.parametrize("R", [17, 24, 31, 32, 33, 64, 65, 100, 127, 128, 129, 192, 255, 256])
 def test_exact_consensus_wide_matches_oracle(R):
-    """Every R above 16 takes the wave-per-unit kernel."""
+    """R = 17-32 takes the 32-slot thread-per-unit kernel (128-bit row loads
+    where a unit-major row is a whole number of 16-byte words, R = 24 and
+    32; strided loads otherwise and replica-major), every R above 32 the
+    wave-per-unit kernel."""
     _case("exact wide", R)
     rng = np.random.default_rng(R)
     U = 3001                                   # ragged against 4 units per workgroup
@@ -94,10 +97,12 @@ def test_exact_consensus_wide_matches_oracle(R):
     torch.cuda.synchronize()
 
 
-@pytest.mark.parametrize("R", [17, 32, 33, 48, 64, 65, 97, 128, 129, 192, 255, 256])
+@pytest.mark.parametrize("R", [17, 20, 31, 32, 33, 48, 64, 65, 97, 128, 129, 192, 255, 256])
 @pytest.mark.parametrize("dt", [np.float32, np.float64])
 def test_statistical_consensus_wide_matches_oracle(R, dt):
-    """Every R above 16 takes the wave kernel: one sort of the finite values."""
+    """R = 17-32 takes the 32-slot thread-per-unit kernel (padding slots
+    past R, so the sort runs over the finite values and +inf), every R above
+    32 the wave kernel: one sort of the finite values."""
     _case("statistical wide", R, dt)
     rng = np.random.default_rng(1000 + R)
     U = 1201
