@@ -268,8 +268,13 @@ def main():
 
     log(f"[bench] timing {args.steps} steps")
     ms_per_step, wall = timed(staged=False)
-    value = total / (ms_per_step * 1e-3) / 1e9
     step_med, step_min = per_step()
+    ms_back_to_back = ms_per_step
+    cold = total < COLD_BELOW_BYTES
+    if cold:
+        # a working set the caches could hold: each step from HBM, timed alone
+        ms_per_step, step_med, step_min = cold_calls(torch, lambda: step(False), args.steps, dev)
+    value = total / (ms_per_step * 1e-3) / 1e9
     # the same steps when the plan staged by the previous call is reused
     ms_staged, _ = timed(staged=True)
     # the three separate calls, for comparison (same outputs)
@@ -379,6 +384,9 @@ def main():
                      "frac_of_achievable": round(achieved / achievable, 4)},
         "cpu_baseline": cpu,
         "wall_s_timed": round(wall, 3),
+        "timing": ("per call after a 1 GiB cache-evicting read" if cold
+                   else "back-to-back calls between one pair of events"),
+        "ms_per_step_back_to_back": round(ms_back_to_back, 4),
         "ms_per_step_plan_reused": round(ms_staged, 4),
         "value_plan_reused": round(total / (ms_staged * 1e-3) / 1e9, 2),
         "step": "c3_check (signature + exact vote + localize in one call)",
@@ -387,6 +395,35 @@ def main():
         "value_three_calls": round(total / (ms_three * 1e-3) / 1e9, 2),
     }
     print(json.dumps(out), flush=True)
+
+
+# Working sets below this size are timed call by call with the caches
+# evicted first: reading 1 GiB before each call clears the 256 MB MALL and
+# the L2s, so the call reads its inputs from HBM.  The eviction is a plain
+# (cache-allocating) read, a torch reduction, rather than a write, so that
+# no dirty lines are left for the timed call to write back.
+COLD_BELOW_BYTES = 1 << 30
+_scratch = {}
+
+
+def cold_calls(torch, fn, steps, dev):
+    """Per-call ms of `steps` calls, each after reading a 1 GiB buffer (not
+    timed) and between its own pair of events: (mean, median, min)."""
+    if dev not in _scratch:
+        _scratch[dev] = torch.full((1 << 28,), 7, dtype=torch.int32, device=dev)
+    junk = _scratch[dev]
+    ts = []
+    for i in range(steps):
+        junk.sum()
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record()
+        fn()
+        b.record()
+        torch.cuda.synchronize()
+        ts.append(a.elapsed_time(b))
+    ts.sort()
+    return sum(ts) / len(ts), ts[len(ts) // 2], ts[0]
 
 
 def warm_up(torch, step, warmup, min_s=0.25, min_steps=10):
@@ -461,9 +498,14 @@ def bench_timing(args, torch, workloads, c3, dev):
         return e0.elapsed_time(e1) / args.steps
 
     t0 = time.perf_counter()
-    ms = timed(step)
+    ms_b2b = timed(step)
+    ms_verdicts_b2b = timed(step_verdicts_only)
+    # the 403 MB of records are 1.6 times the 256 MB MALL: each call is timed
+    # alone after a 1 GiB read that evicts the caches (back-to-back calls
+    # keep part of the records and results cached)
+    ms, ms_med, ms_min = cold_calls(torch, step, args.steps, dev)
     wall = time.perf_counter() - t0
-    ms_verdicts = timed(step_verdicts_only)
+    ms_verdicts, ms_verdicts_med, _ = cold_calls(torch, step_verdicts_only, args.steps, dev)
     # the three separate calls, for comparison
     sep_f = (torch.empty_like(fp_out[0]), torch.empty_like(fp_out[1]), torch.empty_like(fp_out[2]))
     sep_t = (torch.empty_like(t_out[0]), torch.empty_like(t_out[1]), torch.empty_like(t_out[2]))
@@ -473,7 +515,8 @@ def bench_timing(args, torch, workloads, c3, dev):
         c3.consensus(w.fingerprints, c3.EXACT, out=sep_f)
         c3.consensus(w.times, c3.STATISTICAL, out=sep_t)
         c3.confirm(sep_f[1].view(T, G), sep_t[1].view(T, G), R, 16, out=ver, workspace=cws)
-    ms_sep = timed(separate)
+    ms_sep_b2b = timed(separate)
+    ms_sep, _, _ = cold_calls(torch, separate, args.steps, dev)
     # the single pass reads the records once and writes the per-unit results
     # (status 1 + bitmap 8 + majority 4 bytes per unit and kind) and the
     # verdicts; the outlier masks stay in LDS
@@ -488,11 +531,14 @@ def bench_timing(args, torch, workloads, c3, dev):
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms, 4),
+        "ms_per_step_median": round(ms_med, 4),
+        "ms_per_step_min": round(ms_min, 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "u64+f64",
         "data": "synthetic",
+        "timing": "per call after a 1 GiB cache-evicting read",
         "config": {"workload": w.name, "ranks": R * G, "group": R, "iterations": T,
                    "record_bytes_total": total, "stragglers_found": strag,
                    "protocol_outliers_found": proto},
@@ -501,12 +547,16 @@ def bench_timing(args, torch, workloads, c3, dev):
                      "frac": round(pass_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
                      "traffic": None, "kernel": "timing_pass_kernel (per-unit results)",
                      "kernel_ms": round(ms, 4), "algorithmic_bytes_per_launch": pass_bytes},
+        "ms_per_step_back_to_back": round(ms_b2b, 4),
         "ms_per_step_verdicts_only": round(ms_verdicts, 4),
+        "ms_per_step_verdicts_only_median": round(ms_verdicts_med, 4),
+        "ms_per_step_verdicts_only_back_to_back": round(ms_verdicts_b2b, 4),
         "roofline_verdicts_only": {"bound": "hbm", "achieved": round(vo_bytes / (ms_verdicts * 1e-3) / 1e9, 2),
                                    "peak": HBM_PEAK_GBS, "unit": "GB/s",
                                    "frac": round(vo_bytes / (ms_verdicts * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
                                    "kernel": "timing_pass_kernel", "algorithmic_bytes_per_launch": vo_bytes},
         "ms_per_step_separate_calls": round(ms_sep, 4),
+        "ms_per_step_separate_calls_back_to_back": round(ms_sep_b2b, 4),
         "wall_s_timed": round(wall, 3),
     }
     print(json.dumps(out), flush=True)
