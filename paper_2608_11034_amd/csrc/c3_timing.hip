@@ -7,9 +7,10 @@
 // bit into a per-rank mask (one 32-bit word per rank, kind and 32
 // iterations), so the confirmation reads 8 bytes per rank and 32 iterations
 // instead of the per-unit bitmaps, and walks them a word at a time.  The
-// masks live in the workspace (three launches: clear, votes, confirmation)
-// or, when no per-unit results are wanted, in the LDS of a single kernel
-// whose workgroups each own a set of groups over all iterations.
+// masks live in the LDS of a single kernel whose workgroups each own a set
+// of groups over all iterations (the shapes it takes, with or without
+// per-unit results), or else in the workspace (three launches: clear,
+// votes, confirmation).
 #include "c3_device.h"
 #include "c3_internal.h"
 #include "c3_vote_row.h"
@@ -443,7 +444,8 @@ constexpr int64_t kPassMaskLds = 64 * 1024;      // LDS bytes for the masks
 
 // Eight waves per workgroup, two per SIMD.  On 32,768 ranks x 1,024
 // iterations (R = 8, one workgroup per compute unit), per call with HIP
-// events, verdicts only / with per-unit results: 79.0 / 110.8 us; sixteen
+// events, in the build before the one-round confirmation and the step
+// counter, verdicts only / with per-unit results: 79.0 / 110.8 us; sixteen
 // waves 78.8 / 116.4 (the per-unit form spills at 128 VGPRs); eight groups
 // per workgroup, two workgroups per compute unit, 79.7 / 121.2; two steps
 // of loads in flight per wave 81.5 us verdicts only.
