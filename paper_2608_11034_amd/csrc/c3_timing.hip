@@ -542,10 +542,6 @@ __global__ void __launch_bounds__(PassShape<NMAX>::threads) timing_pass_kernel(
     uint32_t* fmask = pass_masks;
     uint32_t* tmask = pass_masks + n_seg * SEGW;
     __shared__ int32_t step_ctr;     // the next step index to hand out
-    for (int64_t i = threadIdx.x; i < 2 * n_seg * SEGW; i += PassShape<NMAX>::threads)
-        pass_masks[i] = 0u;
-    if (threadIdx.x == 0) step_ctr = 2 * NW;
-    __syncthreads();
 
     const int ti = lane / kPassGroups, gi = lane % kPassGroups;
     const int64_t n_steps = (T + kPassIters - 1) / kPassIters;
@@ -627,8 +623,13 @@ __global__ void __launch_bounds__(PassShape<NMAX>::threads) timing_pass_kernel(
         }
         return (int64_t)__builtin_amdgcn_readfirstlane(nn);
     };
+    // the first step's rows are requested before the masks are cleared
+    if (wave < n_steps) load_step((int64_t)wave * kPassIters, gf, gt);
+    for (int64_t i = threadIdx.x; i < 2 * n_seg * SEGW; i += PassShape<NMAX>::threads)
+        pass_masks[i] = 0u;
+    if (threadIdx.x == 0) step_ctr = 2 * NW;
+    __syncthreads();
     if (wave < n_steps) {
-        load_step((int64_t)wave * kPassIters, gf, gt);
         // The first step outside the loop, so that every path into the
         // loop ends with one step's loads and then (with per-unit results)
         // its stores, and the waits for the loads never cover the stores.
