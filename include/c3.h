@@ -264,9 +264,9 @@ size_t c3_check_workspace_size(const c3_tensor_meta_t *metas, int T, int R, uint
  *               streaming kernels; C3_OPT_PLAN_STAGED skips staging when a
  *               previous c3_signature_ex or c3_check call staged the same
  *               plan into this workspace.
- * For R <= 16 the tile partials are combined, the chunks voted and (for up
- * to 8,192 chunks) the lists written by one kernel after the streaming pass;
- * larger groups run the separate steps.  Errors as the three calls.
+ * For R <= 32 the tile partials are combined and the chunks voted by one
+ * kernel after the streaming pass, and (for up to 8,192 chunks) the lists
+ * written by a second; larger groups run the separate steps.  Errors as the three calls.
  */
 int c3_check(const void *const *ptrs, const c3_tensor_meta_t *metas, int T, int R,
              uint64_t chunk_bytes, c3_chunk_record_t *records, uint8_t *status, uint64_t *bitmap,

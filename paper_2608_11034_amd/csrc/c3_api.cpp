@@ -480,9 +480,10 @@ int c3_check(const void* const* ptrs, const c3_tensor_meta_t* metas, int T, int 
     const bool staged = opts != nullptr && (opts->flags & C3_OPT_PLAN_STAGED) != 0;
     if (!staged && stage_to_device(ws, buf.data(), buf.size(), s) != hipSuccess) return C3_E_HIP;
     const SigPlan* dplan = static_cast<const SigPlan*>(ws);
-    // Up to 16 replicas: the streaming kernels, then one tail kernel that
-    // combines partials, votes and (for up to 8,192 chunks) lists in its
-    // last workgroup.  Larger groups: the separate steps.
+    // Up to 32 replicas: the streaming kernels, then a tail kernel that
+    // combines partials and votes, and (for up to 8,192 chunks) a
+    // one-workgroup kernel that places the lists it staged.  Larger groups:
+    // the separate steps.
     const bool fused = c3::check_group_bound(R) != 0;
     hipError_t e = c3::launch_signature(
         dplan, p.h, p.groups, records, opts ? opts->grid_blocks : 0, !fused, s,

@@ -31,7 +31,7 @@ hipError_t launch_small_tail(const SigPlan* dplan, c3_chunk_record_t* records, u
                              int64_t out_cap, int64_t* undecided, int64_t und_cap, int64_t* counts,
                              hipStream_t stream);
 
-// Tail of c3_check for R <= 16 (check_group_bound(R) != 0): records from
+// Tail of c3_check for R <= 32 (check_group_bound(R) != 0): records from
 // partials and exact votes in one kernel; with stage_ws (check_stage_bytes(R,
 // C) bytes, 256-byte aligned; C up to 8,192) also the lists of c3_localize,
 // staged per segment by that kernel and placed by a one-workgroup kernel.

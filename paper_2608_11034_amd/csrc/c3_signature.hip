@@ -564,9 +564,10 @@ hipError_t launch_small_tail(const SigPlan* dplan, c3_chunk_record_t* records, u
 // ---------------------------------------------------------------------------
 constexpr int kCheckThreads = 256;
 constexpr int kCheckMaxListUnits = 8192;   // chunks whose lists go through the staging area
-constexpr int kCheckMaxSegments = kCheckMaxListUnits / (kCheckThreads / 16);
-// per step of 64 segments: outliers < 64 * kCheckThreads * 8 / 2, units <= 64 * 64
-static_assert(64ll * kCheckThreads * 4 < (1ll << 24) && 64 * 64 < (1 << 20), "packed counts");
+constexpr int kCheckMaxSegments = kCheckMaxListUnits / (kCheckThreads / 32);
+// per step of 64 segments: outliers < 64 * CPB * N / 2 = 64 * kCheckThreads / 2,
+// units <= 64 * 64
+static_assert(64ll * kCheckThreads / 2 < (1ll << 24) && 64 * 64 < (1 << 20), "packed counts");
 
 struct CheckStage {
     int32_t* seg_counts;      // [n_seg][4]: outliers, undecided, attributed units
@@ -686,8 +687,8 @@ __global__ void __launch_bounds__(kCheckThreads) check_lists_kernel(
     if (wave == 0) {
         // segment offsets in segment order: one wave, 64 segments per step,
         // the three counts packed into one word (outliers 24 bits, undecided
-        // and attributed 20 bits each: a step of 64 segments holds at most
-        // 64 * 256 * 8 outliers and 64 * 64 units)
+        // and attributed 20 bits each: a step of 64 segments holds fewer
+        // than 64 * kCheckThreads / 2 outliers and at most 64 * 64 units)
         int64_t carry_o = 0, carry_u = 0, carry_a = 0;
         for (int base = 0; base < n_seg; base += 64) {
             const int sgi = base + lane;
@@ -732,7 +733,7 @@ __global__ void __launch_bounds__(kCheckThreads) check_lists_kernel(
     }
 }
 
-int check_group_bound(int R) { return R <= 4 ? 4 : R <= 8 ? 8 : R <= 16 ? 16 : 0; }
+int check_group_bound(int R) { return R <= 4 ? 4 : R <= 8 ? 8 : R <= 16 ? 16 : R <= 32 ? 32 : 0; }
 
 // Staging bytes for the fused lists of C chunks at group bound N (0 when
 // the tail leaves the lists to a separate localization).
@@ -788,8 +789,12 @@ hipError_t launch_check_tail(const SigPlan* dplan, const SigPlan& hplan, c3_chun
             hipLaunchKernelGGL(check_vote_kernel<8>, dim3((unsigned)blocks), dim3(kCheckThreads), 0,
                                stream, dplan, records, status, bitmap, majority, st);
             break;
-        default:
+        case 16:
             hipLaunchKernelGGL(check_vote_kernel<16>, dim3((unsigned)blocks), dim3(kCheckThreads), 0,
+                               stream, dplan, records, status, bitmap, majority, st);
+            break;
+        default:
+            hipLaunchKernelGGL(check_vote_kernel<32>, dim3((unsigned)blocks), dim3(kCheckThreads), 0,
                                stream, dplan, records, status, bitmap, majority, st);
             break;
     }

@@ -1,10 +1,11 @@
 """c3_check (signature, exact vote and localization in one call) against the
 three separate calls it replaces and against the oracle, through the C ABI:
 every record, status, bitmap word, majority index, list entry and count bit
-for bit.  Covers the fused tail (R <= 16, lists in the last workgroup up to
-8,192 chunks, a separate localization above), the separate steps of larger
-groups, repeated calls on a staged plan (the done counter must return to
-zero), truncated lists and graph replay."""
+for bit.  Covers the fused tail (R <= 32: a vote kernel that stages the
+lists per segment and a one-workgroup kernel that places them, up to 8,192
+chunks; a separate localization above), the separate steps of larger
+groups, repeated calls on a staged plan, truncated lists and graph
+replay."""
 import numpy as np
 import pytest
 import torch
@@ -111,7 +112,8 @@ def _random_reps(seed, R, n_max=300_000, T_max=6, chunk=None):
 
 
 @pytest.mark.parametrize("seed,R", [(0, 2), (1, 3), (2, 4), (3, 5), (4, 8), (5, 13), (6, 16),
-                                    (7, 17), (8, 40), (9, 130)])
+                                    (7, 17), (10, 24), (11, 32), (12, 33), (8, 40),
+                                    (9, 130)])
 def test_random_plans_equal_three_calls_and_oracle(seed, R):
     reps, chunk, tile = _random_reps(2000 + seed, R, n_max=200_000 if R < 40 else 40_000)
     _case("check random", seed, R, chunk, tile)
@@ -120,7 +122,8 @@ def test_random_plans_equal_three_calls_and_oracle(seed, R):
     _vs_oracle(g, reps, chunk)
 
 
-@pytest.mark.parametrize("n_chunks,R", [(8192, 8), (8193, 8), (40_000, 4), (9000, 16)])
+@pytest.mark.parametrize("n_chunks,R", [(8192, 8), (8193, 8), (40_000, 4), (9000, 16),
+                                         (8192, 32), (8193, 20)])
 def test_many_chunks_take_the_separate_localization(n_chunks, R):
     """Above 8,192 chunks the tail kernel votes and a separate localization
     lists; above 32,768 that localization is the three-pass one."""
@@ -148,7 +151,8 @@ def test_truncated_lists():
 
 def test_repeated_calls_on_a_staged_plan():
     """Five calls on one staged plan with the bytes changed between calls:
-    the last workgroup of each call must find the counter at zero again."""
+    every call must see the new bytes and leave nothing that changes the
+    next."""
     _case("check repeated staged")
     w = workloads.make(3, device=DEV, scale="small")
     plan = c3.SignaturePlan(w.replicas, w.chunk_bytes)
