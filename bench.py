@@ -42,34 +42,48 @@ METRIC = "replica GB/s fingerprinted+localized; % of MI355X HBM peak"
 # figures are reported only while these are unchanged
 SIG_SOURCES = ["paper_2608_11034_amd/csrc/c3_signature.hip", "paper_2608_11034_amd/csrc/c3_device.h",
                "paper_2608_11034_amd/csrc/c3_sigplan.h"]
+# the same for the single-pass timing kernel
+TIMING_SOURCES = ["paper_2608_11034_amd/csrc/c3_timing.hip", "paper_2608_11034_amd/csrc/c3_vote_row.h",
+                  "paper_2608_11034_amd/csrc/c3_device.h"]
 
 
-def traffic_file(workload: str) -> str:
-    return os.path.join(ROOT, "profiles", f"signature_kernel_{workload}_traffic.json")
+def traffic_file(workload: str, kernel: str = "signature_kernel") -> str:
+    return os.path.join(ROOT, "profiles", f"{kernel}_{workload}_traffic.json")
 
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def kernel_source_hash() -> str:
+def kernel_source_hash(sources=SIG_SOURCES) -> str:
     h = hashlib.sha256()
-    for p in SIG_SOURCES:
+    for p in sources:
         with open(os.path.join(ROOT, p), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
 
 
-def measured_traffic(workload: str):
+def measured_traffic(workload: str, kernel: str = "signature_kernel", sources=SIG_SOURCES):
     """HBM bytes per launch from committed counter runs, if the kernel is unchanged."""
     try:
-        with open(traffic_file(workload)) as f:
+        with open(traffic_file(workload, kernel)) as f:
             t = json.load(f)
     except (OSError, ValueError):
         return None
-    if t.get("kernel_source_hash") != kernel_source_hash():
+    if t.get("kernel_source_hash") != kernel_source_hash(sources):
         return None
     return t.get("hbm_bytes_per_launch")
+
+
+def copy_calibration(torch, dev):
+    """Three 1 GiB device-to-device copies, whose counter readings scale
+    FETCH_SIZE and WRITE_SIZE to bytes in a counter run."""
+    log("[bench] copy calibration: 1 GiB device copy x3")
+    src = torch.empty(1 << 30, dtype=torch.uint8, device=dev).fill_(1)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
 
 
 def host_cpu():
@@ -331,13 +345,7 @@ def main():
     del probe_buf, probe_cs
 
     if args.copy_calibration:
-        log("[bench] copy calibration: 1 GiB device copy x3")
-        src = torch.empty(1 << 30, dtype=torch.uint8, device=dev).fill_(1)
-        dst = torch.empty_like(src)
-        for _ in range(3):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
+        copy_calibration(torch, dev)
 
     cpu = None
     parity = None
@@ -523,6 +531,8 @@ def bench_timing(args, torch, workloads, c3, dev):
         c3.confirm(sep_f[1].view(T, G), sep_t[1].view(T, G), R, 16, out=ver, workspace=cws)
     ms_sep_b2b = timed(separate)
     ms_sep, _, _ = cold_calls(torch, separate, args.steps, dev)
+    if args.copy_calibration:
+        copy_calibration(torch, dev)
     # the single pass reads the records once and writes the per-unit results
     # (status 1 + bitmap 8 + majority 4 bytes per unit and kind) and the
     # verdicts; the outlier masks stay in LDS
@@ -551,7 +561,8 @@ def bench_timing(args, torch, workloads, c3, dev):
         "roofline": {"bound": "hbm", "achieved": round(pass_bytes / (ms * 1e-3) / 1e9, 2),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(pass_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
-                     "traffic": None, "kernel": "timing_pass_kernel (per-unit results)",
+                     "traffic": measured_traffic(w.name, "timing_pass_kernel", TIMING_SOURCES),
+                     "kernel": "timing_pass_kernel (per-unit results)",
                      "kernel_ms": round(ms, 4), "algorithmic_bytes_per_launch": pass_bytes},
         "ms_per_step_back_to_back": round(ms_b2b, 4),
         "ms_per_step_verdicts_only": round(ms_verdicts, 4),
