@@ -193,6 +193,52 @@ def cpu_baseline(w, budget_s: float, gpu=None):
     return out
 
 
+def timing_cpu_baseline(w, gpu):
+    """The oracle's timing consensus (exact vote on the fingerprints,
+    statistical vote on the step times, window confirmation) over the whole
+    workload, one thread pinned to one host core; its per-unit results and
+    verdicts are compared with the GPU's (`gpu`: numpy copies of the last
+    call's outputs)."""
+    import numpy as np
+    import oracle
+
+    T, G, R = w.T, w.G, w.R
+    t0 = time.perf_counter()
+    fp = w.fingerprints.cpu().numpy().reshape(T * G, R).view(np.uint64)
+    tau = w.times.cpu().numpy().reshape(T * G, R)
+    d2h = time.perf_counter() - t0
+    affinity = os.sched_getaffinity(0)
+    core = min(affinity)
+    os.sched_setaffinity(0, {core})
+    try:
+        t0 = time.perf_counter()
+        ost, obm, omj = oracle.vote_exact(fp, replica_axis=1)
+        sst, sbm, smj = oracle.vote_statistical(tau, oracle.KAPPA_DEFAULT, replica_axis=1)
+        ref = oracle.confirm(obm.reshape(T, G), sbm.reshape(T, G), R, 16)
+        dt = time.perf_counter() - t0
+    finally:
+        os.sched_setaffinity(0, affinity)
+    nbytes = fp.nbytes + tau.nbytes
+    units_ok = (np.array_equal(gpu["fp"][0], ost) and np.array_equal(gpu["fp"][1], obm) and
+                np.array_equal(gpu["fp"][2], omj) and np.array_equal(gpu["t"][0], sst) and
+                np.array_equal(gpu["t"][1], sbm) and np.array_equal(gpu["t"][2], smj))
+    v = gpu["verdicts"]
+    fields = (("flags", "flags"), ("first_divergent_iter", "first_div"),
+              ("divergent_count", "div_count"), ("slow_count", "slow_count"),
+              ("max_window_slow", "max_window"), ("first_straggler_window", "first_window"))
+    bad = 0
+    for k, rk in fields:
+        bad = max(bad, int((np.asarray(v[k]) != np.asarray(ref[rk])).sum()))
+    return {"value": nbytes / dt / 1e9, "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": f"the whole workload: {R * G} ranks x {T} iterations ({nbytes} bytes of "
+                      f"records), exact vote, statistical vote and window confirmation, "
+                      f"{dt:.1f} s on host core {core}",
+            "seconds": dt, "d2h_seconds": round(d2h, 3), "host": host_cpu(),
+            "parity": {"ok": units_ok and bad == 0, "units_compared": int(T * G),
+                       "per_unit_results_equal": bool(units_ok),
+                       "ranks_compared": int(R * G), "verdict_fields_differing": bad}}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -533,6 +579,20 @@ def bench_timing(args, torch, workloads, c3, dev):
     ms_sep, _, _ = cold_calls(torch, separate, args.steps, dev)
     if args.copy_calibration:
         copy_calibration(torch, dev)
+    cpu = None
+    if not args.no_cpu_baseline:
+        import numpy as np
+        log("[bench] CPU oracle baseline over the whole workload")
+        step()
+        torch.cuda.synchronize()
+        gpu = {"fp": (fp_out[0].cpu().numpy(), fp_out[1].cpu().numpy().view(np.uint64),
+                      fp_out[2].cpu().numpy()),
+               "t": (t_out[0].cpu().numpy(), t_out[1].cpu().numpy().view(np.uint64),
+                     t_out[2].cpu().numpy()),
+               "verdicts": c3.verdicts_numpy(ver)}
+        cpu = timing_cpu_baseline(w, gpu)
+        log(f"[bench] oracle {cpu['value']:.3f} GB/s over {cpu['seconds']:.1f} s; "
+            f"parity {cpu['parity']}")
     # the single pass reads the records once and writes the per-unit results
     # (status 1 + bitmap 8 + majority 4 bytes per unit and kind) and the
     # verdicts; the outlier masks stay in LDS
@@ -574,6 +634,8 @@ def bench_timing(args, torch, workloads, c3, dev):
                                    "kernel": "timing_pass_kernel", "algorithmic_bytes_per_launch": vo_bytes},
         "ms_per_step_separate_calls": round(ms_sep, 4),
         "ms_per_step_separate_calls_back_to_back": round(ms_sep_b2b, 4),
+        "cpu_baseline": cpu,
+        "parity": cpu["parity"] if cpu else None,
         "wall_s_timed": round(wall, 3),
     }
     print(json.dumps(out), flush=True)
