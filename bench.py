@@ -645,9 +645,16 @@ def bench_wide(args, torch, workloads, c3, dev):
     """Votes over wide peer groups (gathered tables of 33 to 256 peers): per
     group size R, c3_consensus on 262,144 units, STATISTICAL on fp32 and fp64
     step times and EXACT on 64-bit fingerprints; mean ms per call between
-    HIP events over `steps` calls."""
+    HIP events over `steps` calls.  Unless --no-cpu-baseline, the oracle
+    votes the first `S` units of every table, one thread pinned to one host
+    core, and its status, bitmap words and majority index are compared with
+    the GPU's."""
+    import numpy as np
     U = 1 << 18
+    S = 1 << 14
     rows = []
+    oracle_s = {}
+    parity = {"ok": True, "units_compared_per_table": S, "tables": 0, "tables_differing": []}
     for R in (17, 33, 64, 65, 128, 129, 192, 256):
         tau32, fp = workloads.wide_votes(R, U, device=dev)
         tau64 = tau32.double()
@@ -669,6 +676,8 @@ def bench_wide(args, torch, workloads, c3, dev):
             if name == "stat_f32":
                 st = out[0].cpu()
                 line["attributed_units"] = int((st == c3.ATTRIBUTED).sum())
+            if not args.no_cpu_baseline:
+                oracle_s[(R, name)] = wide_oracle_sample(ev, mode, out, R, S, c3, np, parity, name)
         rows.append(line)
         log(f"[bench] wide R={R}: {line}")
         del tau32, tau64, fp
@@ -677,8 +686,52 @@ def bench_wide(args, torch, workloads, c3, dev):
            "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": "f32/f64/u64",
            "data": "synthetic",
            "config": {"workload": "wide_groups_units262144", "units": U, "layout": "unit-major [U][R]"},
-           "per_R": rows}
+           "per_R": rows, "cpu_baseline": None, "parity": None}
+    if oracle_s:
+        # the oracle at the headline's shape (R = 256, fp32 times), scaled from
+        # its S-unit sample to the 262,144 units the value is quoted on
+        t = oracle_s[(256, "stat_f32")]
+        out["cpu_baseline"] = {
+            "value": round(t * (U / S) * 1e3, 1), "unit": "ms", "cores": 1, "kind": "oracle",
+            "sample": f"the first {S} of {U} units of every table, each table voted once; "
+                      f"the value scales R = 256 fp32 ({t:.2f} s) to {U} units; "
+                      f"{sum(oracle_s.values()):.1f} s in all",
+            "per_table_seconds": {f"R{r}_{k}": round(v, 4) for (r, k), v in oracle_s.items()},
+            "host": host_cpu()}
+        out["parity"] = parity
     print(json.dumps(out), flush=True)
+
+
+def wide_oracle_sample(ev, mode, out, R, S, c3, np, parity, name):
+    """Oracle vote over the first S units of one wide table on one pinned
+    host core; records in `parity` whether the GPU's outputs agree.  Returns
+    the oracle's seconds."""
+    import oracle
+
+    host = ev[:S].cpu().numpy()
+    if host.dtype == np.int64:
+        host = host.view(np.uint64)
+    affinity = os.sched_getaffinity(0)
+    os.sched_setaffinity(0, {min(affinity)})
+    try:
+        t0 = time.perf_counter()
+        if mode == c3.EXACT:
+            ost, obm, omj = oracle.vote_exact(host, replica_axis=1)
+        else:
+            ost, obm, omj = oracle.vote_statistical(host, oracle.KAPPA_DEFAULT, replica_axis=1)
+        dt = time.perf_counter() - t0
+    finally:
+        os.sched_setaffinity(0, affinity)
+    words = c3.bitmap_words(R)
+    g_bm = out[1].cpu().numpy().view(np.uint64).reshape(-1, words)[:S]
+    same = (np.array_equal(out[0][:S].cpu().numpy(), ost) and
+            np.array_equal(g_bm, obm.reshape(S, words)) and
+            np.array_equal(out[2][:S].cpu().numpy(), omj))
+    parity["tables"] += 1
+    if not same:
+        parity["ok"] = False
+        parity["tables_differing"].append(f"R{R}_{name}")
+    return dt
 
 
 def bench_optimizer(args, torch, workloads, c3, dev):
