@@ -334,8 +334,11 @@ int prepare_signature(const void* const* ptrs, const c3_tensor_meta_t* metas, in
             if (q == nullptr) return C3_E_INVAL;
             if (!aligned(q, 16)) return C3_E_ALIGN;
         }
-    // the plan: header, pointer table, bases, tensor info
-    buf.assign(align_up(p.h.off_partials, 16), 0);
+    // the plan: header, pointer table, bases, tensor info and, when chunks
+    // span several tiles, the chunk-to-tensor table that the partial
+    // combine reads (one-tile chunks are written whole by the streaming
+    // kernel, so nothing reads it and it is not staged)
+    buf.assign(align_up(p.h.direct ? p.h.off_chunk_tensor : p.h.off_partials, 16), 0);
     memcpy(buf.data(), &p.h, sizeof(SigPlan));
     for (size_t i = 0; i < (size_t)R * (size_t)T; ++i) {
         const uint64_t a = (uint64_t)(uintptr_t)ptrs[i];
@@ -346,9 +349,11 @@ int prepare_signature(const void* const* ptrs, const c3_tensor_meta_t* metas, in
     memcpy(buf.data() + p.h.off_tmeta, p.tinfo.data(), sizeof(TensorInfo) * (size_t)T);
     memcpy(buf.data() + p.h.off_order, p.order.data(), 4ull * T);
     memcpy(buf.data() + p.h.off_gtile, p.gtile.data(), 8ull * (T + 1));
-    int32_t* ct = reinterpret_cast<int32_t*>(buf.data() + p.h.off_chunk_tensor);
-    for (int t = 0; t < T; ++t)
-        for (int64_t c = p.chunk_base[t]; c < p.chunk_base[t + 1]; ++c) ct[c] = t;
+    if (!p.h.direct) {
+        int32_t* ct = reinterpret_cast<int32_t*>(buf.data() + p.h.off_chunk_tensor);
+        for (int t = 0; t < T; ++t)
+            for (int64_t c = p.chunk_base[t]; c < p.chunk_base[t + 1]; ++c) ct[c] = t;
+    }
     return C3_OK;
 }
 
