@@ -579,7 +579,7 @@ def bench_timing(args, torch, workloads, c3, dev):
     ms_sep, _, _ = cold_calls(torch, separate, args.steps, dev)
     if args.copy_calibration:
         copy_calibration(torch, dev)
-    cpu = None
+    cpu = parity = None
     if not args.no_cpu_baseline:
         import numpy as np
         log("[bench] CPU oracle baseline over the whole workload")
@@ -593,6 +593,7 @@ def bench_timing(args, torch, workloads, c3, dev):
         cpu = timing_cpu_baseline(w, gpu)
         log(f"[bench] oracle {cpu['value']:.3f} GB/s over {cpu['seconds']:.1f} s; "
             f"parity {cpu['parity']}")
+        parity = cpu.pop("parity")
     # the single pass reads the records once and writes the per-unit results
     # (status 1 + bitmap 8 + majority 4 bytes per unit and kind) and the
     # verdicts; the outlier masks stay in LDS
@@ -635,7 +636,7 @@ def bench_timing(args, torch, workloads, c3, dev):
         "ms_per_step_separate_calls": round(ms_sep, 4),
         "ms_per_step_separate_calls_back_to_back": round(ms_sep_b2b, 4),
         "cpu_baseline": cpu,
-        "parity": cpu["parity"] if cpu else None,
+        "parity": parity,
         "wall_s_timed": round(wall, 3),
     }
     print(json.dumps(out), flush=True)
