@@ -266,8 +266,9 @@ size_t c3_check_workspace_size(const c3_tensor_meta_t *metas, int T, int R, uint
  *               plan into this workspace.
  * For R <= 32 the tile partials are combined and the chunks voted by one
  * kernel after the streaming pass, and (for up to 8,192 chunks) the lists
- * written by a second; larger groups run the separate steps.  Errors as the
- * three calls.
+ * written by a second; one workgroup does all three for plans of up to 256
+ * chunks and 1,024 records.  Larger groups run the separate steps.  Errors
+ * as the three calls.
  */
 int c3_check(const void *const *ptrs, const c3_tensor_meta_t *metas, int T, int R,
              uint64_t chunk_bytes, c3_chunk_record_t *records, uint8_t *status, uint64_t *bitmap,

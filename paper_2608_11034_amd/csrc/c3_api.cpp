@@ -487,8 +487,9 @@ int c3_check(const void* const* ptrs, const c3_tensor_meta_t* metas, int T, int 
     const SigPlan* dplan = static_cast<const SigPlan*>(ws);
     // Up to 32 replicas: the streaming kernels, then a tail kernel that
     // combines partials and votes, and (for up to 8,192 chunks) a
-    // one-workgroup kernel that places the lists it staged.  Larger groups:
-    // the separate steps.
+    // one-workgroup kernel that places the lists it staged; a plan small
+    // enough for one workgroup's LDS (small_tail_fits) has all three done by
+    // one workgroup in one launch.  Larger groups: the separate steps.
     const bool fused = c3::check_group_bound(R) != 0;
     hipError_t e = c3::launch_signature(
         dplan, p.h, p.groups, records, opts ? opts->grid_blocks : 0, !fused, s,
@@ -496,7 +497,10 @@ int c3_check(const void* const* ptrs, const c3_tensor_meta_t* metas, int T, int 
         opts ? reinterpret_cast<hipEvent_t>(opts->ev_kernel_end) : nullptr);
     if (e != hipSuccess) return C3_E_HIP;
     void* lws = static_cast<unsigned char*>(ws) + sig_ws;
-    if (fused) {
+    if (fused && c3::small_tail_fits(R, p.h.C)) {
+        e = c3::launch_small_tail(dplan, records, status, bitmap, majority_idx, outliers, out_cap,
+                                  undecided, und_cap, counts, s);
+    } else if (fused) {
         const bool lists = c3::check_stage_bytes(R, p.h.C) != 0;
         e = c3::launch_check_tail(dplan, p.h, records, status, bitmap, majority_idx, outliers,
                                   out_cap, undecided, und_cap, counts, lists ? lws : nullptr, s);

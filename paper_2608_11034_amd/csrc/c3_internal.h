@@ -24,7 +24,8 @@ hipError_t launch_signature(const SigPlan* dplan, const SigPlan& hplan, const Si
                             hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1);
 
 // Records (from partials unless chunks are whole tiles), exact votes and
-// lists of a small plan in one workgroup; see small_tail_fits.
+// lists of a small plan in one workgroup: at most 256 chunks and 1,024
+// records, R <= 64 (small_tail_fits checks the sizes).
 bool small_tail_fits(int R, int64_t C);
 hipError_t launch_small_tail(const SigPlan* dplan, c3_chunk_record_t* records, uint8_t* status,
                              uint64_t* bitmap, int32_t* majority, c3_outlier_t* outliers,

@@ -446,17 +446,46 @@ __global__ void __launch_bounds__(256) finalize_kernel(const SigPlan* __restrict
 
 // ---------------------------------------------------------------------------
 // Finalize, exact vote and localize of a small plan in one workgroup (the
-// optimizer-boundary check signs 7 chunks per replica): three launches of a
-// few microseconds each become one.  (1) Every record -- combined from its
-// tile partials, or as the streaming kernel wrote it when chunks are whole
-// tiles -- is written out and kept in LDS.  (2) One thread per chunk votes
-// with exact_vote_row, the rule c3_consensus applies, on the signatures.
-// (3) One thread lists the outliers (chunk ascending, replica ascending,
-// both replicas' summaries) and the undecided chunks, with the counts, as
-// c3_localize does.  Needs R * C <= kTailMaxRecords and C <= kTailThreads.
+// optimizer-boundary check signs 7 chunks per replica; c3_check takes it for
+// plans of up to kTailThreads chunks and kTailMaxRecords records): three
+// launches of a few microseconds each become one.  (1) Every record --
+// combined from its tile partials, or as the streaming kernel wrote it when
+// chunks are whole tiles -- is written out and kept in LDS.  (2) One thread
+// per chunk votes with exact_vote_row, the rule c3_consensus applies, on the
+// signatures.  (3) The lists of c3_localize: a scan over the chunks of their
+// outlier and undecided counts gives each chunk's thread the place of its
+// entries (chunk ascending, replica ascending within a chunk, both
+// replicas' summaries), and thread 0 writes the counts.
 // ---------------------------------------------------------------------------
 constexpr int kTailThreads = 256;
-constexpr int kTailMaxRecords = 512;
+constexpr int kTailMaxRecords = 1024;
+
+// Inclusive prefix sum over the 64 lanes of a wave.
+__device__ inline uint64_t wave_inclusive_scan(uint64_t x, int lane) {
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const uint64_t y = shfl_u64(x, lane >= d ? lane - d : lane);
+        if (lane >= d) x += y;
+    }
+    return x;
+}
+
+__device__ inline void outlier_from(c3_outlier_t& o, int64_t u, int r, int mj,
+                                    const c3_chunk_record_t& a, const c3_chunk_record_t& b) {
+    o.chunk = u;
+    o.replica = r;
+    o.majority_replica = mj;
+    o.nan_count[0] = a.nan_count;
+    o.nan_count[1] = b.nan_count;
+    o.inf_count[0] = a.inf_count;
+    o.inf_count[1] = b.inf_count;
+    o.absmax[0] = a.absmax;
+    o.absmax[1] = b.absmax;
+    o.sum[0] = a.sum;
+    o.sum[1] = b.sum;
+    o.sumsq[0] = a.sumsq;
+    o.sumsq[1] = b.sumsq;
+}
 
 __global__ void __launch_bounds__(kTailThreads) small_tail_kernel(
     const SigPlan* __restrict__ plan, c3_chunk_record_t* __restrict__ records,
@@ -464,7 +493,7 @@ __global__ void __launch_bounds__(kTailThreads) small_tail_kernel(
     c3_outlier_t* __restrict__ outliers, int64_t out_cap, int64_t* __restrict__ undecided,
     int64_t und_cap, int64_t* __restrict__ counts) {
     __shared__ c3_chunk_record_t rec[kTailMaxRecords];
-    __shared__ UnitVote votes[kTailThreads];
+    __shared__ uint64_t wave_total[kTailThreads / 64];
     const int R = plan->R;
     const int C = (int)plan->C;
     for (int i = threadIdx.x; i < R * C; i += kTailThreads) {
@@ -476,14 +505,19 @@ __global__ void __launch_bounds__(kTailThreads) small_tail_kernel(
         }
     }
     __syncthreads();
-    if ((int)threadIdx.x < C) {
-        const int u = threadIdx.x;
-        UnitVote v;
+    const int u = threadIdx.x;
+    UnitVote v{0ull, -1, (uint8_t)C3_AGREE};
+    if (u < C) {
         if (R <= 16) {
             uint64_t e[16];
 #pragma unroll
             for (int r = 0; r < 16; ++r) e[r] = r < R ? rec[r * C + u].sig : 0ull;
             v = exact_vote_row<16>(e, R);
+        } else if (R <= 32) {
+            uint64_t e[32];
+#pragma unroll
+            for (int r = 0; r < 32; ++r) e[r] = r < R ? rec[r * C + u].sig : 0ull;
+            v = exact_vote_row<32>(e, R);
         } else {
             uint64_t e[C3_MAX_REPLICAS];
             for (int r = 0; r < C3_MAX_REPLICAS; ++r) e[r] = r < R ? rec[r * C + u].sig : 0ull;
@@ -492,43 +526,37 @@ __global__ void __launch_bounds__(kTailThreads) small_tail_kernel(
         status[u] = v.status;
         bitmap[u] = v.bitmap;
         majority[u] = v.majority;
-        votes[u] = v;
     }
+    // counts packed as outliers (24 bits: at most 256 chunks x 63), undecided
+    // and attributed chunks (20 bits each)
+    const bool und = u < C && v.status == C3_INCONCLUSIVE;
+    const uint64_t n_o = u < C && !und ? (uint64_t)__builtin_popcountll(v.bitmap) : 0ull;
+    const uint64_t packed = n_o | ((uint64_t)und << 24) | ((uint64_t)(n_o != 0ull) << 44);
+    const int lane = u & 63, wave = u >> 6;
+    const uint64_t incl = wave_inclusive_scan(packed, lane);
+    if (lane == 63) wave_total[wave] = incl;
     __syncthreads();
-    if (threadIdx.x == 0) {
-        int64_t no = 0, nu = 0, na = 0;
-        for (int u = 0; u < C; ++u) {
-            const UnitVote v = votes[u];
-            if (v.status == C3_INCONCLUSIVE) {
-                if (nu < und_cap) undecided[nu] = u;
-                ++nu;
-                continue;
-            }
-            if (v.bitmap == 0ull) continue;
-            ++na;
-            for (uint64_t b = v.bitmap; b != 0ull; b &= b - 1ull) {
-                const int r = __builtin_ctzll(b);
-                if (no < out_cap) {
-                    c3_outlier_t o;
-                    o.chunk = u;
-                    o.replica = r;
-                    o.majority_replica = v.majority;
-                    const c3_chunk_record_t* s2[2] = {&rec[r * C + u], &rec[v.majority * C + u]};
-                    for (int z = 0; z < 2; ++z) {
-                        o.nan_count[z] = s2[z]->nan_count;
-                        o.inf_count[z] = s2[z]->inf_count;
-                        o.absmax[z] = s2[z]->absmax;
-                        o.sum[z] = s2[z]->sum;
-                        o.sumsq[z] = s2[z]->sumsq;
-                    }
-                    outliers[no] = o;
-                }
-                ++no;
-            }
-        }
-        counts[0] = no;
-        counts[1] = nu;
-        counts[2] = na;
+    uint64_t before = 0ull, total = 0ull;
+#pragma unroll
+    for (int w = 0; w < kTailThreads / 64; ++w) {
+        const uint64_t t = wave_total[w];
+        before += w < wave ? t : 0ull;
+        total += t;
+    }
+    const uint64_t excl = before + incl - packed;
+    int64_t po = (int64_t)(excl & 0xFFFFFFull);
+    const int64_t pu = (int64_t)((excl >> 24) & 0xFFFFFull);
+    for (uint64_t b = n_o ? v.bitmap : 0ull; b != 0ull && po < out_cap; b &= b - 1ull, ++po) {
+        const int r = __builtin_ctzll(b);
+        c3_outlier_t o;
+        outlier_from(o, u, r, v.majority, rec[r * C + u], rec[v.majority * C + u]);
+        outliers[po] = o;
+    }
+    if (und && pu < und_cap) undecided[pu] = u;
+    if (u == 0) {
+        counts[0] = (int64_t)(total & 0xFFFFFFull);
+        counts[1] = (int64_t)((total >> 24) & 0xFFFFFull);
+        counts[2] = (int64_t)((total >> 44) & 0xFFFFFull);
     }
 }
 
@@ -576,33 +604,6 @@ struct CheckStage {
     int32_t out_per_seg;
     int32_t cpb;
 };
-
-// Inclusive prefix sum over the 64 lanes of a wave.
-__device__ inline uint64_t wave_inclusive_scan(uint64_t x, int lane) {
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        const uint64_t y = shfl_u64(x, lane >= d ? lane - d : lane);
-        if (lane >= d) x += y;
-    }
-    return x;
-}
-
-__device__ inline void outlier_from(c3_outlier_t& o, int64_t u, int r, int mj,
-                                    const c3_chunk_record_t& a, const c3_chunk_record_t& b) {
-    o.chunk = u;
-    o.replica = r;
-    o.majority_replica = mj;
-    o.nan_count[0] = a.nan_count;
-    o.nan_count[1] = b.nan_count;
-    o.inf_count[0] = a.inf_count;
-    o.inf_count[1] = b.inf_count;
-    o.absmax[0] = a.absmax;
-    o.absmax[1] = b.absmax;
-    o.sum[0] = a.sum;
-    o.sum[1] = b.sum;
-    o.sumsq[0] = a.sumsq;
-    o.sumsq[1] = b.sumsq;
-}
 
 template <int N>
 __global__ void __launch_bounds__(kCheckThreads) check_vote_kernel(

@@ -3,9 +3,10 @@ three separate calls it replaces and against the oracle, through the C ABI:
 every record, status, bitmap word, majority index, list entry and count bit
 for bit.  Covers the fused tail (R <= 32: a vote kernel that stages the
 lists per segment and a one-workgroup kernel that places them, up to 8,192
-chunks; a separate localization above), the separate steps of larger
-groups, repeated calls on a staged plan, truncated lists and graph
-replay."""
+chunks; a separate localization above; one workgroup for records, votes
+and lists on plans of up to 256 chunks and 1,024 records), the separate
+steps of larger groups, repeated calls on a staged plan, truncated lists
+and graph replay."""
 import numpy as np
 import pytest
 import torch
@@ -26,14 +27,16 @@ def _case(*a):
     print("CASE", *a, flush=True)
 
 
-def _host(outs):
+def _host(outs, out_cap=None, und_cap=None):
     rec, st, bm, mj, outl, und, cnt = outs
     torch.cuda.synchronize()
     c = cnt.cpu().numpy()
+    oc = outl.shape[0] if out_cap is None else min(out_cap, outl.shape[0])
+    uc = und.numel() if und_cap is None else min(und_cap, und.numel())
     return dict(records=c3.records_numpy(rec), status=st.cpu().numpy(),
                 bitmap=bm.cpu().numpy().view(np.uint64), maj=mj.cpu().numpy(),
-                outliers=outl[:min(int(c[0]), outl.shape[0])].cpu().numpy(),
-                undecided=und.cpu().numpy()[:min(int(c[1]), und.numel())], counts=c)
+                outliers=outl[:min(int(c[0]), oc)].cpu().numpy(),
+                undecided=und.cpu().numpy()[:min(int(c[1]), uc)], counts=c)
 
 
 def _three_calls(reps, chunk, tile=0, out_cap=None, und_cap=None):
@@ -42,15 +45,15 @@ def _three_calls(reps, chunk, tile=0, out_cap=None, und_cap=None):
     plan.run(rec, plan.new_workspace())
     st, bm, mj = c3.consensus(rec, c3.EXACT)
     outl, und, cnt = c3.localize(st, bm, mj, rec, out_cap=out_cap, und_cap=und_cap)
-    return _host((rec, st, bm, mj, outl, und, cnt))
+    return _host((rec, st, bm, mj, outl, und, cnt), out_cap, und_cap)
 
 
 def _check(reps, chunk, tile=0, out_cap=None, und_cap=None):
     plan = c3.SignaturePlan(reps, chunk, tile)
     outs = plan.new_check_outputs(out_cap, und_cap)
     ws = torch.empty(plan.check_workspace_size(), dtype=torch.uint8, device=DEV)
-    plan.run_check(outs, ws)
-    return _host(outs)
+    plan.run_check(outs, ws, out_cap=out_cap, und_cap=und_cap)
+    return _host(outs, out_cap, und_cap)
 
 
 def _same(a, b):
@@ -120,6 +123,75 @@ def test_random_plans_equal_three_calls_and_oracle(seed, R):
     g = _check(reps, chunk, tile)
     _same(g, _three_calls(reps, chunk, tile))
     _vs_oracle(g, reps, chunk)
+
+
+def _small_reps(R, C, seed, two_tensors=False):
+    """R replicas of C chunks of 4 KiB (the last one short), faults in about
+    half of the chunks: a minority of replicas flipped (attributed), for
+    even R also half against half (undecided), and one replica's NaN."""
+    gen = torch.Generator(device=DEV)
+    gen.manual_seed(seed)
+    if two_tensors:
+        c1 = C // 3
+        base = [torch.randn(c1 * 2048 - 5, generator=gen, device=DEV).to(torch.bfloat16),
+                torch.randn((C - c1) * 1024 - 7, generator=gen, device=DEV)]
+    else:
+        base = [torch.randn(C * 1024 - 7, generator=gen, device=DEV)]
+    reps = [[t.clone() for t in base] for _ in range(R)]
+    rng = np.random.default_rng(seed)
+    for c in range(C):
+        kind = int(rng.integers(0, 6))
+        if c == 0:
+            kind = 0                                    # the first chunk always has a fault
+        if kind > 2:
+            continue
+        t = 0 if not two_tensors or c < C // 3 else 1
+        c0 = c if t == 0 else c - C // 3
+        nb = reps[0][t].numel() * reps[0][t].element_size()
+        pos = min(c0 * 4096 + int(rng.integers(0, 4096)), nb - 1)
+        if kind == 0 and R >= 3:                        # a minority flipped
+            who = rng.choice(R, size=int(rng.integers(1, (R - 1) // 2 + 1)), replace=False)
+        elif kind == 1 and R % 2 == 0:                  # half against half
+            who = rng.choice(R, size=R // 2, replace=False)
+        else:                                           # one replica's NaN
+            who = [int(rng.integers(0, R))]
+            if reps[0][t].dtype == torch.float32:
+                pos -= pos % 4
+                for r in who:
+                    reps[int(r)][t].view(torch.int32)[pos // 4] = 0x7FC00001
+                continue
+        for r in who:
+            reps[int(r)][t].view(torch.uint8)[pos] ^= 0x21
+    return reps
+
+
+# Plans of at most 256 chunks and 1,024 records take the one-workgroup tail:
+# records (from partials when chunks span several tiles), votes and lists in
+# one launch after the streaming kernel.
+@pytest.mark.parametrize("R,C,tile,caps,two", [
+    (3, 256, 4096, None, False),        # the 1M fp32 shape: 768 records, one-tile chunks
+    (2, 256, 1024, None, False),        # four partials per record combined in the workgroup
+    (4, 256, 4096, (5, 2), False),      # truncated lists; half-against-half chunks undecided
+    (8, 128, 2048, None, True),         # bf16 and fp32 tensors
+    (16, 64, 4096, (0, 0), False),      # lists of capacity zero
+    (32, 32, 4096, None, False),        # 1,024 records, the workgroup's limit
+    (5, 1, 4096, None, False),          # one chunk
+])
+def test_one_workgroup_tail_equals_three_calls_and_oracle(R, C, tile, caps, two):
+    _case("check one-workgroup tail", R, C, tile, caps, two)
+    reps = _small_reps(R, C, 100 + R + C, two)
+    oc, uc = caps if caps else (None, None)
+    g = _check(reps, 4096, tile, out_cap=oc, und_cap=uc)
+    assert len(g["status"]) == C
+    _same(g, _three_calls(reps, 4096, tile, out_cap=oc, und_cap=uc))
+    if caps is None:
+        _vs_oracle(g, reps, 4096)
+        assert g["counts"][0] > 0 or R == 2           # two replicas never outvote one
+    else:
+        assert len(g["outliers"]) == min(oc, g["counts"][0])
+        assert len(g["undecided"]) == min(uc, g["counts"][1])
+    if R % 2 == 0 and C > 1:
+        assert g["counts"][1] > 0
 
 
 @pytest.mark.parametrize("n_chunks,R", [(8192, 8), (8193, 8), (40_000, 4), (9000, 16),
