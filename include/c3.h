@@ -264,11 +264,11 @@ size_t c3_check_workspace_size(const c3_tensor_meta_t *metas, int T, int R, uint
  *               streaming kernels; C3_OPT_PLAN_STAGED skips staging when a
  *               previous c3_signature_ex or c3_check call staged the same
  *               plan into this workspace.
- * For R <= 32 the tile partials are combined and the chunks voted by one
- * kernel after the streaming pass, and (for up to 8,192 chunks) the lists
- * written by a second; one workgroup does all three for plans of up to 256
- * chunks and 1,024 records.  Larger groups run the separate steps.  Errors
- * as the three calls.
+ * One workgroup combines the tile partials, votes the chunks and writes the
+ * lists after the streaming pass for plans of up to 256 chunks, 1,024
+ * records and 64 replicas.  Otherwise, for R <= 32, one kernel combines and
+ * votes and (for up to 8,192 chunks) a second writes the lists; larger
+ * groups run the separate steps.  Errors as the three calls.
  */
 int c3_check(const void *const *ptrs, const c3_tensor_meta_t *metas, int T, int R,
              uint64_t chunk_bytes, c3_chunk_record_t *records, uint8_t *status, uint64_t *bitmap,

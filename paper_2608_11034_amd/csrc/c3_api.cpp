@@ -485,19 +485,21 @@ int c3_check(const void* const* ptrs, const c3_tensor_meta_t* metas, int T, int 
     const bool staged = opts != nullptr && (opts->flags & C3_OPT_PLAN_STAGED) != 0;
     if (!staged && stage_to_device(ws, buf.data(), buf.size(), s) != hipSuccess) return C3_E_HIP;
     const SigPlan* dplan = static_cast<const SigPlan*>(ws);
-    // Up to 32 replicas: the streaming kernels, then a tail kernel that
-    // combines partials and votes, and (for up to 8,192 chunks) a
-    // one-workgroup kernel that places the lists it staged; a plan small
-    // enough for one workgroup's LDS (small_tail_fits) has all three done by
-    // one workgroup in one launch.  Larger groups: the separate steps.
+    // A plan small enough for one workgroup's LDS (small_tail_fits, up to 64
+    // replicas): the streaming kernels, then one workgroup that combines
+    // partials, votes and lists.  Otherwise, up to 32 replicas: a tail
+    // kernel that combines partials and votes, and (for up to 8,192 chunks)
+    // a one-workgroup kernel that places the lists it staged.  Larger
+    // groups: the separate steps.
+    const bool small = R <= C3_MAX_REPLICAS && c3::small_tail_fits(R, p.h.C);
     const bool fused = c3::check_group_bound(R) != 0;
     hipError_t e = c3::launch_signature(
-        dplan, p.h, p.groups, records, opts ? opts->grid_blocks : 0, !fused, s,
+        dplan, p.h, p.groups, records, opts ? opts->grid_blocks : 0, !(small || fused), s,
         opts ? reinterpret_cast<hipEvent_t>(opts->ev_kernel_begin) : nullptr,
         opts ? reinterpret_cast<hipEvent_t>(opts->ev_kernel_end) : nullptr);
     if (e != hipSuccess) return C3_E_HIP;
     void* lws = static_cast<unsigned char*>(ws) + sig_ws;
-    if (fused && c3::small_tail_fits(R, p.h.C)) {
+    if (small) {
         e = c3::launch_small_tail(dplan, records, status, bitmap, majority_idx, outliers, out_cap,
                                   undecided, und_cap, counts, s);
     } else if (fused) {

@@ -165,9 +165,9 @@ def _small_reps(R, C, seed, two_tensors=False):
     return reps
 
 
-# Plans of at most 256 chunks and 1,024 records take the one-workgroup tail:
-# records (from partials when chunks span several tiles), votes and lists in
-# one launch after the streaming kernel.
+# Plans of at most 256 chunks, 1,024 records and 64 replicas take the
+# one-workgroup tail: records (from partials when chunks span several
+# tiles), votes and lists in one launch after the streaming kernel.
 @pytest.mark.parametrize("R,C,tile,caps,two", [
     (3, 256, 4096, None, False),        # the 1M fp32 shape: 768 records, one-tile chunks
     (2, 256, 1024, None, False),        # four partials per record combined in the workgroup
@@ -176,6 +176,8 @@ def _small_reps(R, C, seed, two_tensors=False):
     (16, 64, 4096, (0, 0), False),      # lists of capacity zero
     (32, 32, 4096, None, False),        # 1,024 records, the workgroup's limit
     (5, 1, 4096, None, False),          # one chunk
+    (40, 25, 2048, None, False),        # above the 32-replica tail, partials combined
+    (64, 16, 4096, (3, 1), False),      # 64 replicas: one bitmap word
 ])
 def test_one_workgroup_tail_equals_three_calls_and_oracle(R, C, tile, caps, two):
     _case("check one-workgroup tail", R, C, tile, caps, two)
