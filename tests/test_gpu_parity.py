@@ -110,6 +110,34 @@ def test_tensor_signatures_match_oracle(k):
     assert np.array_equal(mj.cpu().numpy(), omj)
 
 
+def test_tensor_signatures_of_many_ragged_tensors():
+    """300 tensors per replica of 0 to 12 KB (empty tensors included, each
+    one chunk): every tensor's chunk range, which the kernel finds by a
+    64-way search over the records' tensor ids, and so every per-tensor
+    signature equals the oracle's; the one changed tensor is the only
+    outlier."""
+    _print_case("tensor signatures, 300 ragged tensors")
+    rng = np.random.default_rng(7)
+    gen = torch.Generator(device=DEV)
+    gen.manual_seed(7)
+    base = [torch.randn(int(rng.choice([0, 1, 5, 255, 256, 257, 1000, 3000])), generator=gen,
+                        device=DEV) for _ in range(300)]
+    R, chunk = 3, 1024
+    reps = [[t.clone() for t in base] for _ in range(R)]
+    hit = next(i for i in range(17, 300) if base[i].numel() > 0)
+    reps[1][hit].view(torch.uint8)[0] ^= 1
+    rec = c3.signature(reps, chunk)
+    ts = c3.tensor_signature(rec, len(base))
+    torch.cuda.synchronize()
+    metas = [(workloads.F32, tuple(t.shape)) for t in base]
+    ref = oracle.signature([[workloads.host_bytes(t) for t in rep] for rep in reps], metas, chunk)
+    want = oracle.tensor_signature(ref, len(base))
+    got = ts.cpu().numpy().view(np.uint64)
+    assert np.array_equal(got, want)
+    diff = {(r, t) for r in range(R) for t in range(len(base)) if got[r, t] != got[0 if r else 2, t]}
+    assert {t for _, t in diff} == {hit}
+
+
 @pytest.mark.parametrize("k", [1, 2, 3, 4])
 def test_three_step_protocol_on_gpu(k):
     """Fault-injection protocol of the paper's evaluation: clean replicas give
