@@ -320,9 +320,14 @@ __device__ inline double maxbits_to_f64(uint32_t bits, int dtype) {
 
 __device__ inline void write_record(c3_chunk_record_t* rec, const TensorInfo* tip, int t,
                                     uint64_t k, uint64_t n, const TilePartial& p) {
-    const int dtype = tip->dtype, ndim = tip->ndim;
+    // the tensor's description in one batch of loads, so that the chain over
+    // the dimensions runs on registers instead of waiting for each in turn
+    const TensorInfo ti = *tip;
+    const int dtype = ti.dtype, ndim = ti.ndim;
     uint64_t h = fmix64(kTag ^ ((uint64_t)(uint32_t)dtype << 32) ^ (uint64_t)(uint32_t)ndim);
-    for (int d = 0; d < ndim; ++d) h = fmix64(h ^ (uint64_t)tip->shape[d]);
+#pragma unroll
+    for (int d = 0; d < C3_MAX_NDIM; ++d)
+        if (d < ndim) h = fmix64(h ^ (uint64_t)ti.shape[d]);
     h = fmix64(h ^ k);
     h = fmix64(h ^ n);
     h = fmix64(h ^ p.A);
@@ -426,7 +431,16 @@ __device__ inline void combine_chunk(const SigPlan* __restrict__ plan, int64_t r
     const int64_t nt = min((int64_t)plan->tiles_per_chunk, tiles_t - lt0);
     const TilePartial* pp = partials + r * plan->tiles_per_replica + tile_base[t] + lt0;
     TilePartial p = pp[0];
-    for (int64_t x = 1; x < nt; ++x) partial_add(p, pp[x]);
+    // in tile order, four partials loaded at a time before they are added
+    for (int64_t x0 = 1; x0 < nt; x0 += 4) {
+        TilePartial q[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            if (x0 + j < nt) q[j] = pp[x0 + j];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            if (x0 + j < nt) partial_add(p, q[j]);
+    }
     const uint64_t coff = k * plan->chunk_bytes;
     const uint64_t n = nbytes > coff ? min(plan->chunk_bytes, nbytes - coff) : 0;
     write_record(out, tinfo + t, t, k, n, p);
