@@ -71,7 +71,7 @@ typedef enum {
     C3_OK = 0,
     C3_E_INVAL = -1,       /* bad size, count, code or NULL pointer        */
     C3_E_ALIGN = -2,       /* a pointer or stride violates its alignment   */
-    C3_E_UNSUPPORTED = -3, /* valid request this build does not implement  */
+    C3_E_UNSUPPORTED = -3, /* valid request the library does not implement */
     C3_E_WORKSPACE = -4,   /* workspace NULL, misaligned or too small      */
     C3_E_HIP = -5          /* a HIP runtime call or kernel launch failed   */
 } c3_status_t;
